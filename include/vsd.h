@@ -1,0 +1,280 @@
+/*
+ * vsd.h -- C ABI of the Variational Speculative Decoding (VSD) EM path-scoring
+ * library for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes, for a batch of training positions, the data-parallel
+ * part of one VSD EM step (Appendix "Algorithm Detail": Alg. 1, the MC-based EM
+ * framework, and Alg. 2, the oracle):
+ *
+ *   vsd_sample_paths      E-step proposals: N draft paths, N target correction
+ *                         paths and N greedy target reference paths of depth L
+ *                         per position (Alg. 1 proposal/correction draws,
+ *                         Alg. 2 greedy baseline).
+ *   vsd_score_paths       Row softmax statistics, acceptance ratios (Sec.
+ *                         "Preliminary", Eq. acc), survival and expected
+ *                         accepted length (Sec. "Theoretical Analysis",
+ *                         Eqs. survival_def / accepted_len_cond), the oracle
+ *                         gate (Alg. 2), target correction (Alg. 1), ARW beta
+ *                         (Eq. beta_update), CAR zeta (Eq. zeta_update), the
+ *                         weighted-likelihood loss (Eq. advance / Eq. basic)
+ *                         and the per-row gradient coefficients.
+ *   vsd_weighted_loss_bwd Gradient of that loss with respect to the draft
+ *                         logits (derivative of Eq. advance).
+ *
+ * Terminology and layout
+ * ----------------------
+ *   position x = (b, t), b < B, t < T;  P = B*T positions.
+ *   path slot s < N (the paper's sample size S);  depth i = 1..L (the paper's
+ *   sampling length L).
+ *   row r = ((b*T + t)*N + s)*L + (i-1);  R = P*N*L rows.  One row is one
+ *   "path-token": it owns one draft logit row X_r (v_draft entries) and one
+ *   target logit row Y_r (v_target entries).  Rows are given per slot: all
+ *   three path families at slot (s,i) are scored against the same two rows
+ *   (the draft and target conditionals along the sampled draft path).
+ *   Level l = 1..L of slot s denotes the length-l prefix of path s.
+ *   Per-row quantities indexed by level (flags, o', beta, zeta) live at row
+ *   ((b*T + t)*N + s)*L + (l-1).
+ *   Families: 0 = draft proposal z~, 1 = target correction z', 2 = greedy z-bar.
+ *   All tokens are in draft-index space [0, v_draft).  When v_draft !=
+ *   v_target an injective map d2t: [0, v_draft) -> [0, v_target) is required;
+ *   the target probability of draft token v is p(d2t[v]) with the target
+ *   softmax taken over all v_target entries.  Without a map, d2t is the
+ *   identity.
+ *   valid_depth[b,t,s] = d_s in [1, L] (NULL means d_s = L for all paths):
+ *   slot (s,i) exists iff i <= d_s.  Rows with i > d_s are "masked": their
+ *   tokens are -1, their score outputs are 0 and their gradient rows are 0.
+ *
+ * Memory, ownership, streams
+ * --------------------------
+ *   Every array argument is a DEVICE pointer owned by the caller; struct
+ *   arguments (vsd_dims, vsd_params, vsd_src, vsd_score_out, vsd_grad) are
+ *   HOST pointers read during the call only.  The library never allocates or
+ *   frees memory, never synchronises, never reads device memory on the host
+ *   and keeps no mutable global state other than a thread-local error string.
+ *   All work is enqueued on `hip_stream` (a hipStream_t; NULL = default
+ *   stream) and is complete only when that stream is.
+ *   Logit rows: row r starts at element r*ld of its array; the array holds R
+ *   rows of ld elements (ld >= v).  Base pointers and ld*element_size must be
+ *   multiples of 16 bytes (rows are read with 128-bit loads).
+ *
+ * Errors
+ * ------
+ *   Host-side validation runs before anything is launched; on failure the
+ *   call returns a non-zero vsd_status, launches nothing and writes nothing.
+ *   vsd_last_error() then holds a message naming the offending argument.
+ *   Data errors only visible on the device (a token outside [-1, v_draft), a
+ *   d2t entry outside [0, v_target), a depth outside [1, L]) make the kernels
+ *   skip the offending access and atomically store the first VSD_DEVERR_* code
+ *   into *device_error (a slot the caller zeroes beforehand; the library only
+ *   ever replaces 0 by a non-zero code).  The outputs of such a call are
+ *   unspecified.  A failed HIP launch returns VSD_ERR_HIP.
+ *
+ * Determinism
+ * -----------
+ *   Every output is a pure function of the inputs: bitwise identical run to
+ *   run and independent of launch geometry.  Tokens depend only on (seed,
+ *   offset, row index, vocabulary index) and the logits, so a resumed trainer
+ *   reproduces them exactly by passing the same offset.
+ *
+ * Normative sampler definition (draft proposal z~ and target correction z')
+ * ------------------------------------------------------------------------
+ *   The paper draws z~ ~ q and z' ~ p (Alg. 1) without naming a sampler; this
+ *   library fixes one so that the sampled tokens are unique and reproducible
+ *   bit for bit by any implementation of this definition.  Every operation
+ *   below is one IEEE-754 binary32 operation rounded to nearest-even (no fused
+ *   multiply-add, correctly rounded division); integers are unsigned 32-bit.
+ *
+ *   S1 Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
+ *      as easy as 1, 2, 3", SC'11).  Key (k0,k1) = (low 32 bits of seed,
+ *      high 32 bits of seed).  Ten rounds; round j uses the key
+ *      (k0 + j*0x9E3779B9, k1 + j*0xBB67AE85) mod 2^32, j = 0..9.  A round
+ *      maps (c0,c1,c2,c3) to
+ *        (hi(0xCD9E8D57*c2) ^ c1 ^ k0', lo(0xCD9E8D57*c2),
+ *         hi(0xD2511F53*c0) ^ c3 ^ k1', lo(0xD2511F53*c0))
+ *      where hi/lo are the upper/lower 32 bits of the 64-bit product.
+ *   S2 For vocabulary index v of row r and family f (0 = z~, 1 = z'), the
+ *      counter is (v >> 2, r, f, offset) and the word used is output word
+ *      (v & 3).  (For a mapped target row, v is the draft index.)
+ *   S3 u = float(2*(w >> 9) + 1) * 2^-24, exactly representable, in (0,1).
+ *   S4 Lambda(x), the normative log of a positive normal float x:
+ *        e = ((bits(x) >> 23) & 0xFF) - 127;
+ *        m = float with bits (bits(x) & 0x7FFFFF) | 0x3F800000;   (m in [1,2))
+ *        if m > 1.41421354f (0x3FB504F3): m = m * 0.5f; e = e + 1;
+ *        f = m - 1;   s = f / (2 + f);   z = s * s;
+ *        p = 1/9;  p = 1/7 + z*p;  p = 1/5 + z*p;  p = 1/3 + z*p;
+ *            (each constant c is float(c): 0x3DE38E39, 0x3E124925,
+ *             0x3E4CCCCD, 0x3EAAAAAB; every * and + rounds separately)
+ *        t2 = s + s;   lm = t2 + t2 * (z * p);
+ *        ef = float(e);
+ *        Lambda = ef * 0.693145751953125f (0x3F317200)
+ *                 + (lm + ef * 1.42860677e-06f (0x35BFBE8E)).
+ *      (The series is 2*atanh(s) = log(m); the constant split is exact for
+ *      the ef*hi product.)
+ *   S5 G = -Lambda(-Lambda(u))  (a Gumbel(0,1) variate).
+ *   S6 key_v = float(logit_v * invT) + G, with invT = float(1/T) and
+ *      logit_v = X[r][v] (z~, T = temp_draft) or Y[r][d2t[v]] (z',
+ *      T = temp_target).  The token is the v in [0, v_draft) with the largest
+ *      key; among equal keys the smallest v.
+ *   S7 The greedy reference z-bar is the v in [0, v_draft) maximising the raw
+ *      target logit Y[r][d2t[v]]; among equal logits the smallest v
+ *      (Alg. 2, greedy target policy).
+ *   Logits must be finite.
+ */
+#ifndef VSD_H
+#define VSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VSD_ABI_VERSION 1
+
+typedef enum vsd_status {
+  VSD_OK = 0,
+  VSD_ERR_NULL_POINTER = 1,  /* a required pointer is NULL */
+  VSD_ERR_INVALID_SHAPE = 2, /* B,T,N,L,v,ld or hidden_dim out of range */
+  VSD_ERR_INVALID_VALUE = 3, /* temperature, w_base, tau, mode ... invalid */
+  VSD_ERR_MISALIGNED = 4,    /* base pointer or row stride not 16-B aligned */
+  VSD_ERR_MAP_REQUIRED = 5,  /* v_draft != v_target and d2t == NULL */
+  VSD_ERR_UNSUPPORTED = 6,   /* combination this build does not implement */
+  VSD_ERR_WORKSPACE = 7,     /* workspace NULL or smaller than required */
+  VSD_ERR_HIP = 8            /* a HIP runtime call failed */
+} vsd_status;
+
+/* Codes written to *device_error by the kernels. */
+enum {
+  VSD_DEVERR_NONE = 0,
+  VSD_DEVERR_TOKEN_RANGE = 1, /* token outside [-1, v_draft) or -1 on a live slot */
+  VSD_DEVERR_MAP_RANGE = 2,   /* d2t entry outside [0, v_target) */
+  VSD_DEVERR_DEPTH_RANGE = 3  /* valid_depth entry outside [1, L] */
+};
+
+typedef enum vsd_dtype { VSD_F32 = 0, VSD_BF16 = 1 } vsd_dtype;
+
+/* Which M-step estimator the coefficients implement (Alg. 1, M-step). */
+typedef enum vsd_grad_mode {
+  VSD_GRAD_BASIC = 0,  /* Eq. basic: c = 0 */
+  VSD_GRAD_ARW = 1,    /* Eq. advance with zeta = 1: c = beta */
+  VSD_GRAD_ARW_CAR = 2 /* Eq. advance: c = beta * zeta (default) */
+} vsd_grad_mode;
+
+/* What CAR's softmax is taken over (Eq. zeta_update). */
+typedef enum vsd_car_input {
+  VSD_CAR_PROB = 0,   /* exp(Q/tau), Q = draft path probability (as printed) */
+  VSD_CAR_LOGPROB = 1 /* exp(log Q / tau), an alternative reading */
+} vsd_car_input;
+
+typedef struct vsd_dims {
+  int32_t B, T, N, L;  /* 1 <= B,T; 1 <= N <= 1024; 1 <= L <= 64 */
+  int32_t v_draft;     /* draft vocabulary size, >= 1 */
+  int32_t v_target;    /* target vocabulary size, >= v_draft */
+  int32_t dtype;       /* vsd_dtype of the logit (or hidden/weight) arrays */
+  int32_t hidden_dim;  /* fused LM-head variant only: H; 0 otherwise */
+  int64_t ld_draft;    /* row stride of the draft logit array, elements */
+  int64_t ld_target;   /* row stride of the target logit array, elements */
+} vsd_dims;
+
+typedef struct vsd_params {
+  float temp_draft;    /* T_q > 0: q = softmax(X / T_q) */
+  float temp_target;   /* T_p > 0: p = softmax(Y / T_p) */
+  float w_base;        /* > 0; oracle length weight w(l) = w_base^l (1.05) */
+  float car_tau;       /* > 0; CAR temperature tau (0.2) */
+  int32_t mode;        /* vsd_grad_mode */
+  int32_t car_input;   /* vsd_car_input */
+  float loss_scale;    /* multiplies the summed loss and the gradient */
+} vsd_params;
+
+/* Source of one model's logits.  Materialised: `logits` != NULL, an [R, ld]
+ * array of dims->dtype.  Fused LM head: `logits` == NULL, logits are
+ * hidden[R, H] @ weight[V, H]^T computed on the fly (bf16 only). */
+typedef struct vsd_src {
+  const void* logits;
+  const void* hidden;
+  const void* weight;
+} vsd_src;
+
+typedef struct vsd_score_out {
+  float* lse_draft;       /* [R]   required: log-sum-exp of X_r / T_q */
+  float* lse_target;      /* [R]   optional: log-sum-exp of Y_r / T_p */
+  float* log_alpha;       /* [R,3] optional: min(0, log p - log q) per family */
+  float* log_q_tok;       /* [R,3] optional: log q(token) per family */
+  float* survival;        /* [R]   optional: S_i of z~ (prefix product) */
+  float* exp_accept_len;  /* [P*N] optional: sum_{k<=d_s} S_k of z~ */
+  uint8_t* accept_flag;   /* [R]   optional: I~ = oracle accepts z~ at level */
+  uint8_t* valid_flag;    /* [R]   optional: I' = oracle accepts the used path */
+  float* o_prime;         /* [R]   optional: o' = w(l) * I' */
+  float* beta;            /* [R]   optional: ARW coefficient */
+  float* zeta;            /* [R]   optional: CAR weight */
+  float* coef_a;          /* [R]   required: coefficient of -log q(z~) */
+  float* coef_b;          /* [R]   required: coefficient of -log q(z') */
+  float* loss_pos;        /* [P]   optional: L_x (unscaled) */
+  float* loss_total;      /* [1]   optional: loss_scale * sum_x L_x */
+  int32_t* device_error;  /* [1]   required */
+} vsd_score_out;
+
+typedef struct vsd_grad {
+  void* grad_logits;      /* materialised: [R, ld_draft], dtype of X */
+  void* grad_hidden;      /* fused: [R, H] bf16 */
+  float* grad_weight;     /* fused, optional: [v_draft, H] fp32 */
+} vsd_grad;
+
+/* E-step sampling (Alg. 1: z~ ~ q and z' ~ p; Alg. 2: z-bar greedy).
+ * Writes tok_draft, tok_target, tok_greedy ([R] int32 each, draft-index
+ * space, -1 on masked rows) following the normative sampler definition above.
+ * Reads X (draft) over [0, v_draft) and Y (target) at d2t[v] for every v. */
+vsd_status vsd_sample_paths(const vsd_dims* dims, const vsd_src* draft,
+                            const vsd_src* target, const int32_t* d2t,
+                            const int32_t* valid_depth, float temp_draft,
+                            float temp_target, uint64_t seed, uint32_t offset,
+                            int32_t* tok_draft, int32_t* tok_target,
+                            int32_t* tok_greedy, int32_t* device_error,
+                            void* hip_stream);
+
+/* Path scoring and M-step weights for given tokens (any tokens the caller
+ * supplies, not only those of vsd_sample_paths).  Per row: q and p log-sum-exp
+ * over the full draft / target vocabularies, log alpha and log q of the three
+ * families.  Per position: prefix sums over depth, oracle flags (equality
+ * accepts), o', beta (leave-one-out over paths alive at the level; 0 when the
+ * denominator is 0), zeta (softmax over paths alive at the level), W = sum o',
+ * L_x (0 when W = 0), and
+ *   a_{s,i} = (1/W) sum_{l=i..d_s} o'_{l,s} (I~_{l,s} - c_{l,s})
+ *   b_{s,i} = (1/W) sum_{l=i..d_s} o'_{l,s} (1 - I~_{l,s}).
+ * `workspace` must hold vsd_score_workspace_bytes() bytes (16-B aligned). */
+vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params,
+                           const vsd_src* draft, const vsd_src* target,
+                           const int32_t* d2t, const int32_t* valid_depth,
+                           const int32_t* tok_draft, const int32_t* tok_target,
+                           const int32_t* tok_greedy, const vsd_score_out* out,
+                           void* workspace, size_t workspace_bytes,
+                           void* hip_stream);
+
+/* Gradient of loss_scale * sum_x L_x with respect to the draft logits (the
+ * derivative of Eq. advance, with o', beta, zeta and the tokens held fixed):
+ *   g[r][v] = loss_scale / T_q * ((a+b) q_r(v) - a [v = z~] - b [v = z'])
+ * with q_r(v) = exp(X[r][v] / T_q - lse_draft[r]).  Columns [0, v_draft) of
+ * every row are written; rows with a = b = 0 (masked rows among them) are
+ * written as zeros without reading X; padding columns [v_draft, ld) are not
+ * touched.  grad_logits has the layout of X (stride ld_draft) and its dtype
+ * (bf16 rounded to nearest-even). */
+vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
+                                 const vsd_src* draft, const float* lse_draft,
+                                 const int32_t* tok_draft,
+                                 const int32_t* tok_target, const float* coef_a,
+                                 const float* coef_b, const vsd_grad* grad,
+                                 int32_t* device_error, void* hip_stream);
+
+/* Bytes of workspace vsd_score_paths needs for `dims` (host only). */
+vsd_status vsd_score_workspace_bytes(const vsd_dims* dims, size_t* bytes);
+
+const char* vsd_status_string(vsd_status status); /* static string */
+const char* vsd_last_error(void);                 /* thread-local detail */
+int32_t vsd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VSD_H */

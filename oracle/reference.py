@@ -1,0 +1,85 @@
+"""Whole-step oracle over a set of positions (test infrastructure).
+
+Runs the three stages of one VSD EM step for every listed position, in the
+paper's order: E-step draws (Alg. 1 and the greedy baseline of Alg. 2), path
+scoring and M-step weights, then the gradient with respect to the draft logits.
+Inputs are plain numpy arrays holding the exact logit values (float32 holds
+every bf16 value exactly).
+"""
+import numpy as np
+
+from . import paths, sampler
+
+
+def sample_position(Xp, Yp_mapped, depth, first_row, temp_draft, temp_target, seed, offset):
+    """Tokens [N, L] x 3 for one position; -1 on masked slots.
+
+    Xp [N, L, V_d]; Yp_mapped [N, L, V_d] = target logits at d2t[v];
+    first_row = global row index of slot (0, 1).
+    """
+    N, L, Vd = Xp.shape
+    rows = first_row + np.arange(N * L)
+    zd, zt, zg = sampler.sample_rows(Xp.reshape(N * L, Vd), Yp_mapped.reshape(N * L, Vd), rows,
+                                     temp_draft, temp_target, seed, offset)
+    toks = [z.reshape(N, L).copy() for z in (zd, zt, zg)]
+    live = np.arange(L)[None, :] < np.asarray(depth)[:, None]
+    for t in toks:
+        t[~live] = -1
+    return toks
+
+
+def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
+                  tokens=None, want_grad=True):
+    """Oracle outputs for the given positions.
+
+    X [len(positions)*N*L, V_d], Y [len(positions)*N*L, V_t]: rows of those
+    positions in row order; depth [len(positions), N] or None; tokens, if
+    given, is a tuple of three [len(positions)*N*L] arrays used instead of
+    sampling (scoring then follows the given tokens).
+    Returns a dict of per-row arrays [len(positions)*N*L] (or [.., V_d] for
+    grad, [.., 3] for log_alpha / log_q) and per-position arrays.
+    """
+    p = dict(paths.DEFAULT_PARAMS)
+    p.update(params or {})
+    Vd = X.shape[1]
+    Vt = Y.shape[1]
+    d2t_arr = np.arange(Vd) if d2t is None else np.asarray(d2t, dtype=np.int64)
+    npos = len(positions)
+    X = X.reshape(npos, N, L, Vd)
+    Y = Y.reshape(npos, N, L, Vt)
+    depth = np.full((npos, N), L, dtype=np.int64) if depth is None else np.asarray(depth).reshape(npos, N)
+    keys = ["lse_q", "lse_p", "log_alpha", "log_q", "survival", "accept_flag", "valid_flag",
+            "o_prime", "beta", "zeta", "coef_a", "coef_b"]
+    acc = {k: [] for k in keys}
+    out = {"tok_draft": [], "tok_target": [], "tok_greedy": [], "exp_accept_len": [],
+           "loss_pos": [], "W": [], "grad": []}
+    for k, pos in enumerate(positions):
+        if tokens is None:
+            toks = sample_position(X[k], Y[k][:, :, d2t_arr], depth[k], int(pos) * N * L,
+                                   p["temp_draft"], p["temp_target"], seed, offset)
+        else:
+            sl = slice(k * N * L, (k + 1) * N * L)
+            toks = [np.asarray(t[sl], dtype=np.int64).reshape(N, L) for t in tokens]
+        sc = paths.score_position(X[k], Y[k], None if d2t is None else d2t_arr, depth[k],
+                                  toks[0], toks[1], toks[2], p)
+        for key in keys:
+            acc[key].append(sc[key].reshape(N * L, *sc[key].shape[2:]))
+        out["tok_draft"].append(toks[0].reshape(-1))
+        out["tok_target"].append(toks[1].reshape(-1))
+        out["tok_greedy"].append(toks[2].reshape(-1))
+        out["exp_accept_len"].append(sc["exp_accept_len"])
+        out["loss_pos"].append(sc["loss"])
+        out["W"].append(sc["W"])
+        if want_grad:
+            g = paths.grad_position(X[k], sc["lse_q"], toks[0], toks[1], sc["coef_a"], sc["coef_b"],
+                                    p["temp_draft"], p["loss_scale"])
+            out["grad"].append(g.reshape(N * L, Vd))
+    res = {k: np.concatenate(v) for k, v in acc.items()}
+    for k in ("tok_draft", "tok_target", "tok_greedy", "exp_accept_len"):
+        res[k] = np.concatenate(out[k])
+    res["loss_pos"] = np.asarray(out["loss_pos"])
+    res["W"] = np.asarray(out["W"])
+    res["loss_total"] = p["loss_scale"] * res["loss_pos"].sum()
+    if want_grad:
+        res["grad"] = np.concatenate(out["grad"])
+    return res

@@ -1,0 +1,215 @@
+"""Planted mistakes in the oracle must be caught by its pins (CPU only).
+
+Each mutant is a copy of an oracle module with one plausible mistake (a
+dropped term, a flipped sign or comparison, a wrong index or family, a
+transposed operand).  The checks below are the same kinds of pins as the
+oracle's own tests (hand-derived examples, closed forms, finite differences,
+distribution tests, float64 log accuracy); every mutant must fail at least one.
+"""
+import inspect
+import json
+import math
+import os
+import types
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle.paths as paths_mod
+import oracle.sampler as sampler_mod
+
+GOLDEN = ["micro_example.json", "ragged_example.json", "car_example.json"]
+MODES = {"BASIC": 0, "ARW": 1, "ARW_CAR": 2, "ARW_CAR_LOGPROB": 2}
+
+
+def _mutant(module, old, new):
+    src = inspect.getsource(module)
+    assert src.count(old) == 1, f"mutation anchor not unique/found: {old!r}"
+    mod = types.ModuleType(module.__name__ + "_mutant")
+    mod.__package__ = "oracle"
+    exec(compile(src.replace(old, new), module.__file__, "exec"), mod.__dict__)
+    return mod
+
+
+# ---- checks (return True when the pin holds) --------------------------------
+
+def _check_golden(P, golden_dir):
+    for name in GOLDEN:
+        with open(os.path.join(golden_dir, name)) as f:
+            g = json.load(f)
+        N, L, V = g["N"], g["L"], g["V"]
+        X = np.asarray(g["X_rows"]) if "X_rows" in g else np.broadcast_to(np.asarray(g["X_row"]), (N, L, V)).copy()
+        Y = np.broadcast_to(np.asarray(g["Y_row"]), (N, L, V)).copy()
+        toks = [np.asarray(g[k]) for k in ("tok_draft", "tok_target", "tok_greedy")]
+        for mode_name, exp in g["expected"].items():
+            params = dict(g["params"], mode=MODES[mode_name], car_input=exp.get("car_input", 0))
+            out = P.score_position(X, Y, None, np.asarray(g["depth"]), *toks, params)
+            grad = P.grad_position(X, out["lse_q"], toks[0], toks[1], out["coef_a"], out["coef_b"],
+                                   params["temp_draft"], params["loss_scale"])
+            checks = [np.allclose(grad, np.asarray(exp["grad"]), atol=1e-12),
+                      math.isclose(out["loss"], exp["loss"], rel_tol=1e-12, abs_tol=1e-15)]
+            for key in ("o_prime", "beta", "zeta", "coef_a", "coef_b", "survival", "exp_accept_len",
+                        "accept_flag", "valid_flag"):
+                if key in exp:
+                    checks.append(np.allclose(np.asarray(out[key], dtype=float), np.asarray(exp[key]), atol=1e-12))
+            if "W" in exp:
+                checks.append(math.isclose(out["W"], exp["W"], rel_tol=1e-12))
+            if not all(checks):
+                return False
+    return True
+
+
+def _softmax(x):
+    e = np.exp(x - x.max())
+    return e / e.sum()
+
+
+def _check_closed_form(P):
+    import itertools
+    rng = np.random.default_rng(3)
+    V, L = 4, 3
+    q_rows = [rng.normal(0, 1.5, V) for _ in range(L)]
+    p_rows = [rng.normal(0, 1.5, V) for _ in range(L)]
+    closed, prod = 0.0, 1.0
+    for i in range(L):
+        prod *= np.minimum(_softmax(p_rows[i]), _softmax(q_rows[i])).sum()
+        closed += prod
+    enum = 0.0
+    for z in itertools.product(range(V), repeat=L):
+        X = np.stack(q_rows)[None]
+        Y = np.stack(p_rows)[None]
+        tok = np.asarray(z)[None]
+        out = P.score_position(X, Y, None, [L], tok, tok, tok)
+        qz = np.prod([_softmax(q_rows[i])[z[i]] for i in range(L)])
+        enum += qz * out["exp_accept_len"][0]
+        if np.any(out["log_alpha"] > 0) or np.any(np.diff(out["survival"][0]) > 1e-15):
+            return False
+    return math.isclose(enum, closed, rel_tol=1e-10)
+
+
+def _check_fd(P):
+    rng = np.random.default_rng(5)
+    N, L, V = 3, 2, 4
+    for mode, T in ((2, 0.5), (0, 1.0)):
+        X = rng.normal(0, 1, (N, L, V))
+        Y = rng.normal(0, 1, (N, L, V))
+        depth = np.array([2, 1, 2])
+        toks = [rng.integers(0, V, (N, L)) for _ in range(3)]
+        params = dict(mode=mode, temp_draft=T)
+        out = P.score_position(X, Y, None, depth, *toks, params)
+        g = P.grad_position(X, out["lse_q"], toks[0], toks[1], out["coef_a"], out["coef_b"], T, 1.0)
+        h = 1e-6
+        for idx in np.ndindex(X.shape):
+            Xp, Xm = X.copy(), X.copy()
+            Xp[idx] += h
+            Xm[idx] -= h
+            fd = (P.loss_from_logits(Xp, Y, None, depth, *toks, out, params)
+                  - P.loss_from_logits(Xm, Y, None, depth, *toks, out, params)) / (2 * h)
+            if abs(fd - g[idx]) > 1e-6:
+                return False
+    return True
+
+
+def _check_map(P):
+    rng = np.random.default_rng(13)
+    N, L, V = 2, 2, 5
+    X = rng.normal(0, 1, (N, L, V))
+    Ym = rng.normal(0, 1, (N, L, V))
+    Y = np.zeros((N, L, 2 * V))
+    d2t = np.arange(0, 2 * V, 2)
+    Y[..., d2t] = Ym
+    Y[..., d2t + 1] = Ym
+    toks = [rng.integers(0, V, (N, L)) for _ in range(3)]
+    a = P.score_position(X, Ym, None, [L] * N, *toks)
+    b = P.score_position(X, Y, d2t, [L] * N, *toks)
+    unclamped = a["log_alpha"] < -1e-12
+    return (np.allclose(b["lse_p"], a["lse_p"] + math.log(2), rtol=1e-12)
+            and np.allclose(b["log_alpha"][unclamped], a["log_alpha"][unclamped] - math.log(2), rtol=1e-12))
+
+
+def _check_sampler(S):
+    w = (np.arange(2 ** 23, dtype=np.uint64) << np.uint64(9)).astype(np.uint32)
+    ug = S.uniform_from_word(w)
+    if not (ug[0] == np.float32(2.0 ** -24) and np.all(ug + ug[::-1] == 1) and np.all(np.diff(ug) > 0)):
+        return False
+    grid = np.arange(2 ** 20, dtype=np.int64) * 8
+    u = ((2 * grid + 1).astype(np.float32) * np.float32(2.0 ** -24))
+    lu = S.spec_log(u).astype(np.float64)
+    ref = np.log(u.astype(np.float64))
+    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    if (np.abs(lu - ref) / ulp).max() > 2:
+        return False
+    logits = np.array([0.0, 1.0, -0.5, 2.0], dtype=np.float32)
+    n = 100_000
+    for T in (1.0, 0.5):
+        keys = S.gumbel_keys(np.broadcast_to(logits, (n, 4)), np.arange(n), 0, T, 7, 0)
+        counts = np.bincount(S.first_argmax(keys), minlength=4)
+        p = _softmax(logits.astype(np.float64) / T)
+        if stats.chisquare(counts, p * n)[1] < 1e-4:
+            return False
+    x = np.zeros((1, 3), dtype=np.float32)
+    if S.sample_rows(x, np.array([[0.0, 1.0, 1.0]], dtype=np.float32), [0], 1.0, 1.0, 0, 0)[2][0] != 1:
+        return False
+    return True
+
+
+PATH_MUTANTS = [
+    ("np.minimum(0.0, log_p - log_q)", "np.maximum(0.0, log_p - log_q)"),
+    ("np.minimum(0.0, log_p - log_q)", "np.minimum(0.0, log_q - log_p)"),
+    ("acc_flag[s, i] = LS[0, s, i] >= LS[2, s, i]", "acc_flag[s, i] = LS[0, s, i] > LS[2, s, i]"),
+    ("corrected_ok = LS[1, s, i] >= LS[2, s, i]", "corrected_ok = LS[1, s, i] >= LS[0, s, i]"),
+    ("val_flag[s, i] = acc_flag[s, i] or corrected_ok", "val_flag[s, i] = corrected_ok"),
+    ("for j in alive if j != s)\n            den", "for j in alive)\n            den"),
+    ("beta[s, i] = num / den if den > 0 else 0.0", "beta[s, i] = num / den if den > 0 else 1.0"),
+    ("length_weight(i + 1, p[\"w_base\"])", "length_weight(i, p[\"w_base\"])"),
+    ("/ float(p[\"car_tau\"])", "* float(p[\"car_tau\"])"),
+    ("conf = np.array([np.exp(LQ[0, s, i]) for s in alive])", "conf = np.array([np.exp(LQ[1, s, i]) for s in alive])"),
+    ("survival = np.where(live, np.exp(LS[0]), 0.0)", "survival = np.where(live, np.exp(LS[2]), 0.0)"),
+    ("acc = acc + log_alpha[:, s, i]\n            accq = accq + log_q[:, s, i]\n            LS[:, s, i] = acc",
+     "LS[:, s, i] = acc\n            acc = acc + log_alpha[:, s, i]\n            accq = accq + log_q[:, s, i]"),
+    ("lq_used = LQ[0, s, i] if acc_flag[s, i] else LQ[1, s, i]", "lq_used = LQ[1, s, i] if acc_flag[s, i] else LQ[0, s, i]"),
+    ("        loss = -total / W", "        loss = total / W"),
+    ("for lev in range(i, depth[s]):", "for lev in range(0, i + 1):"),
+    ("coef_b[s, i] += o_prime[s, lev] * (1.0 - acc_flag[s, lev])", "coef_b[s, i] += o_prime[s, lev] * (1.0 - val_flag[s, lev])"),
+    ("coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] - c[s, lev])", "coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] + c[s, lev])"),
+    ("g[s, i] = loss_scale / temp_draft * row", "g[s, i] = loss_scale * row"),
+    ("row[tok_t[s, i]] -= b", "row[tok_d[s, i]] -= b"),
+    ("log_p[f, s, i] = float(Y[s, i, d2t[z]]) / Tp - lse_p[s, i]", "log_p[f, s, i] = float(Y[s, i, z]) / Tp - lse_p[s, i]"),
+    ("lse_p[s, i] = log_softmax_normaliser(Y[s, i], Tp)", "lse_p[s, i] = log_softmax_normaliser(Y[s, i, d2t], Tp)"),
+    ("log_q[f, s, i] = float(X[s, i, z]) / Tq - lse_q[s, i]", "log_q[f, s, i] = float(X[s, i, z]) - lse_q[s, i]"),
+    ("c = beta * zeta", "c = beta + zeta - 1.0"),
+]
+
+SAMPLER_MUTANTS = [
+    ("return -spec_log(e)", "return spec_log(e)"),
+    ("inv_t = F32(1.0) / F32(temperature)", "inv_t = F32(temperature)"),
+    ("_C5 = F32(1.0 / 5.0)", "_C5 = F32(1.0 / 6.0)"),
+    ("big = m > _SQRT2", "big = m > F32(1.9)"),
+    ("out = ef * _LN2_HI + (lm + ef * _LN2_LO)", "out = ef * _LN2_HI + lm"),
+    ("return (2 * k + 1).astype(F32) * F32(2.0 ** -24)", "return (k + 1).astype(F32) * F32(2.0 ** -23)"),
+    ("first_argmax(np.asarray(target_rows_mapped, dtype=np.float64))",
+     "first_argmax(-np.asarray(target_rows_mapped, dtype=np.float64))"),
+]
+
+
+def test_unmutated_oracle_passes_every_check(golden_dir):
+    assert _check_golden(paths_mod, golden_dir)
+    assert _check_closed_form(paths_mod)
+    assert _check_fd(paths_mod)
+    assert _check_map(paths_mod)
+    assert _check_sampler(sampler_mod)
+
+
+@pytest.mark.parametrize("old,new", PATH_MUTANTS, ids=[f"paths{i}" for i in range(len(PATH_MUTANTS))])
+def test_path_mutant_is_caught(golden_dir, old, new):
+    P = _mutant(paths_mod, old, new)
+    caught = (not _check_golden(P, golden_dir)) or (not _check_closed_form(P)) \
+        or (not _check_fd(P)) or (not _check_map(P))
+    assert caught, f"no pin caught mutant {new!r}"
+
+
+@pytest.mark.parametrize("old,new", SAMPLER_MUTANTS, ids=[f"sampler{i}" for i in range(len(SAMPLER_MUTANTS))])
+def test_sampler_mutant_is_caught(old, new):
+    S = _mutant(sampler_mod, old, new)
+    assert not _check_sampler(S), f"no pin caught mutant {new!r}"
