@@ -1,0 +1,197 @@
+"""Benchmark of one VSD EM step (sample -> score -> backward) on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config C3] [--no-cpu-baseline]
+
+Workload (default): the LLaMA-3-8B / EAGLE-3-shaped batch, B=4 T=512 N=8 L=6,
+target vocabulary 128256, draft vocabulary 32000 with a draft->target map,
+bf16 logits already resident in HBM, synthetic and seeded.  One step = every
+row of the batch through vsd_sample_paths, vsd_score_paths and
+vsd_weighted_loss_bwd on one stream.  W untimed steps, then exactly K steps
+timed between stream synchronisations; per-call durations come from HIP
+events recorded on the stream the kernels run on.
+
+Prints one JSON line: value = path-tokens (live rows) per second of whole
+steps; roofline = the dominant kernel against its bound; cpu_baseline = the
+CPU oracle timed on a bounded sample of the same workload (computed before the
+GPU is touched, in worker processes).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+# Plain (non-packed) fp32 VALU lane-operations per second:
+# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
+VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
+
+METRIC = "path-tokens scored/sec (fwd+bwd) and achieved HBM GB/s at V=128256"
+
+
+_SAMPLE = None  # (X, Y, d2t, N, L) shared with forked workers
+
+
+def _oracle_position(k):
+    """Position k of the sample through the CPU oracle (worker process)."""
+    from oracle import reference
+    X, Y, d2t, N, L = _SAMPLE
+    per = N * L
+    t0 = time.perf_counter()
+    reference.run_positions(X[k * per:(k + 1) * per], Y[k * per:(k + 1) * per], d2t, None, [k], N, L, {},
+                            seed=0, offset=0)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(cfg, workers, per_worker=8):
+    """Time the oracle on workers*per_worker positions of the workload, the
+    positions spread over `workers` forked processes."""
+    global _SAMPLE
+    import multiprocessing as mp
+
+    from synth import make_inputs, scaled
+    # a CPU-generated sample of the same recipe (the GPU is not touched here)
+    npos = workers * per_worker
+    sample_cfg = scaled(cfg.name, name=cfg.name + "-cpu-sample", B=1, T=npos)
+    inp = make_inputs(sample_cfg, "cpu", chunk_rows=1024)
+    X = inp["X"][:, :cfg.v_draft].float().numpy()
+    Y = inp["Y"][:, :cfg.v_target].float().numpy()
+    d2t = None if inp["d2t"] is None else inp["d2t"].numpy()
+    del inp
+    _SAMPLE = (X, Y, d2t, cfg.N, cfg.L)
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(workers) as pool:
+        pool.map(_oracle_position, range(npos), chunksize=per_worker)
+    wall = time.perf_counter() - t0
+    _SAMPLE = None
+    rows = npos * cfg.N * cfg.L
+    return {"value": rows / wall, "unit": "path-tokens/s", "cores": workers, "kind": "oracle",
+            "sample": f"{npos} positions ({rows} path-tokens) of the {cfg.name} recipe, sample+score+grad, "
+                      f"{workers} worker processes, {wall:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="C3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-workers", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (positions shard "
+              "independently across GPUs; run one process per GPU).", file=sys.stderr)
+        sys.exit(2)
+
+    from synth import CONFIGS
+    cfg = CONFIGS[args.config]
+    if cfg.kind == "fused":
+        print("the fused LM-head workload is not benchmarked by this build", file=sys.stderr)
+        sys.exit(2)
+
+    base = None
+    if not args.no_cpu_baseline:
+        workers = args.cpu_workers or max(1, min(16, os.cpu_count() or 1))
+        base = cpu_baseline(cfg, workers)
+        print(f"[bench] cpu baseline: {base['value']:.1f} {base['unit']} on {base['cores']} cores", flush=True)
+
+    import torch
+
+    import paper_2602_05774_amd as vsd
+    from synth import make_inputs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.perf_counter()
+    inp = make_inputs(cfg, dev)
+    torch.cuda.synchronize()
+    print(f"[bench] inputs {cfg.name} generated in {time.perf_counter() - t0:.1f} s", flush=True)
+    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+    params = vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target)
+    X, Y, d2t, depth = inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"]
+    out = vsd.alloc_score_outputs(prob, dev)
+    ws = torch.empty(vsd.score_workspace_bytes(prob, X.dtype), dtype=torch.uint8, device=dev)
+    grad = torch.empty_like(X)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        s = vsd.sample_paths(prob, X, Y, d2t, depth, cfg.temp_draft, cfg.temp_target, cfg.philox_seed,
+                             cfg.philox_offset, device_error=err)
+        if ev:
+            ev[1].record()
+        vsd.score_paths(prob, params, X, Y, s.tok_draft, s.tok_target, s.tok_greedy, d2t, depth, out=out,
+                        workspace=ws)
+        if ev:
+            ev[2].record()
+        vsd.weighted_loss_bwd(prob, params, X, out.lse_draft, s.tok_draft, s.tok_target, out.coef_a, out.coef_b,
+                              grad=grad, device_error=err)
+        if ev:
+            ev[3].record()
+        return s
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        s = step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+        raise RuntimeError("device error reported during the benchmark")
+    t_sample = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    t_score = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    t_bwd = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    t_step = sum(e[0].elapsed_time(e[3]) for e in evs) / args.steps
+
+    live = prob.R if depth is None else int((s.tok_draft >= 0).sum().item())
+    nonzero = int(((out.coef_a != 0) | (out.coef_b != 0)).sum().item())
+    es = X.element_size()
+    # algorithmic bytes per launch
+    score_bytes = live * es * (cfg.v_draft + cfg.v_target)
+    bwd_bytes = nonzero * es * cfg.v_draft + prob.R * es * cfg.v_draft
+    sample_keys = live * 2 * cfg.v_draft
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    kernels = {
+        "sample": {"ms": t_sample, "keys_per_s": sample_keys / (t_sample * 1e-3)},
+        "score": {"ms": t_score, "bytes": score_bytes, "GB/s": gbs(score_bytes, t_score)},
+        "bwd": {"ms": t_bwd, "bytes": bwd_bytes, "GB/s": gbs(bwd_bytes, t_bwd)},
+    }
+    sb_ms = t_score + t_bwd
+    score_bwd = {"ms": sb_ms, "bytes": score_bytes + bwd_bytes, "GB/s": gbs(score_bytes + bwd_bytes, sb_ms),
+                 "frac_of_hbm_peak": gbs(score_bytes + bwd_bytes, sb_ms) / HBM_PEAK_GBS,
+                 "path_tokens_per_s": live / (sb_ms * 1e-3)}
+    dominant = max(("sample", t_sample), ("score", t_score), ("bwd", t_bwd), key=lambda kv: kv[1])[0]
+    if dominant == "sample":
+        roof = {"bound": "alu", "kernel": "k_sample", "achieved": None, "peak": VALU_PEAK_GOPS,
+                "unit": "Gop/s", "frac": None, "traffic": None,
+                "note": "VALU-bound sampler; achieved op rate is taken from rocprofv3 SQ_INSTS_VALU"}
+    else:
+        k = kernels[dominant]
+        roof = {"bound": "hbm", "kernel": "k_score_rows" if dominant == "score" else "k_bwd",
+                "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": k["GB/s"] / HBM_PEAK_GBS,
+                "traffic": None}
+    line = {
+        "metric": METRIC, "value": live / (t_step * 1e-3), "unit": "path-tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step, "wall_ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: B={cfg.B} T={cfg.T} N={cfg.N} L={cfg.L} "
+                               f"V_target={cfg.v_target} V_draft={cfg.v_draft} logits={cfg.dtype}",
+                   "path_tokens_per_step": live, "parallelism": "single GPU"},
+        "kernels": kernels, "score_bwd": score_bwd, "roofline": roof, "cpu_baseline": base,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

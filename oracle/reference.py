@@ -49,7 +49,7 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
     Y = Y.reshape(npos, N, L, Vt)
     depth = np.full((npos, N), L, dtype=np.int64) if depth is None else np.asarray(depth).reshape(npos, N)
     keys = ["lse_q", "lse_p", "log_alpha", "log_q", "survival", "accept_flag", "valid_flag",
-            "o_prime", "beta", "zeta", "coef_a", "coef_b"]
+            "o_prime", "beta", "zeta", "coef_a", "coef_b", "LS"]
     acc = {k: [] for k in keys}
     out = {"tok_draft": [], "tok_target": [], "tok_greedy": [], "exp_accept_len": [],
            "loss_pos": [], "W": [], "grad": []}

@@ -1,0 +1,93 @@
+// Gradient of the weighted-likelihood loss with respect to the draft logits
+// (vsd_weighted_loss_bwd): the derivative of Eq. advance with the E-step
+// quantities fixed,
+//   g[v] = loss_scale / T_q * ((a + b) q(v) - a [v = z~] - b [v = z']),
+// q(v) = exp(X[v] / T_q - lse_q).  One wavefront per row streams the draft
+// row once (128-bit loads) and writes the gradient row once (128-bit stores);
+// rows with a = b = 0 are written as zeros without reading X.
+#include "vsd_device.hpp"
+#include "vsd_kernels.hpp"
+
+namespace vsd {
+
+namespace {
+
+constexpr int kRowsPerBlock = 4;
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd(BwdArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  T* G = static_cast<T*>(a.G) + r * a.ld;
+  const float ca = a.coef_a[r];
+  const float cb = a.coef_b[r];
+  constexpr int step = 8 * kWave;
+  if (ca == 0.0f && cb == 0.0f) {
+    const float zero[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int base = lane * 8;
+    for (; base + 8 <= a.Vd; base += step) store8(G + base, zero);
+    for (int v = base; v < a.Vd && v < base + 8; ++v) store1(G + v, 0.0f);
+    return;
+  }
+  const T* X = static_cast<const T*>(a.X) + r * a.ld;
+  const float c = a.inv_tq * kLog2e;
+  const float lse2 = a.lse_q[r] * kLog2e;
+  const float k = a.scale * a.inv_tq;
+  const float kab = k * (ca + cb), ka = k * ca, kb = k * cb;
+  const int zd = a.tok_d[r], zt = a.tok_t[r];
+  int base = lane * 8;
+  constexpr int U = 2;
+  for (; base + (U - 1) * step + 8 <= a.Vd; base += U * step) {
+    float x[U][8];
+#pragma unroll
+    for (int u = 0; u < U; ++u) load8(X + base + u * step, x[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float g[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int v = base + u * step + j;
+        float t = kab * __builtin_amdgcn_exp2f(fmaf(x[u][j], c, -lse2));
+        t -= (v == zd) ? ka : 0.0f;
+        t -= (v == zt) ? kb : 0.0f;
+        g[j] = t;
+      }
+      store8(G + base + u * step, g);
+    }
+  }
+  for (; base + 8 <= a.Vd; base += step) {
+    float x[8], g[8];
+    load8(X + base, x);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int v = base + j;
+      float t = kab * __builtin_amdgcn_exp2f(fmaf(x[j], c, -lse2));
+      t -= (v == zd) ? ka : 0.0f;
+      t -= (v == zt) ? kb : 0.0f;
+      g[j] = t;
+    }
+    store8(G + base, g);
+  }
+  for (int v = base; v < a.Vd && v < base + 8; ++v) {
+    float t = kab * __builtin_amdgcn_exp2f(fmaf(load1(X + v), c, -lse2));
+    t -= (v == zd) ? ka : 0.0f;
+    t -= (v == zt) ? kb : 0.0f;
+    store1(G + v, t);
+  }
+}
+
+template <typename T>
+hipError_t launch_t(const BwdArgs& a, hipStream_t s) {
+  const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
+  hipLaunchKernelGGL((k_bwd<T>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_bwd(const BwdArgs& a, bool bf16, hipStream_t s) {
+  return bf16 ? launch_t<bf16_t>(a, s) : launch_t<float>(a, s);
+}
+
+}  // namespace vsd

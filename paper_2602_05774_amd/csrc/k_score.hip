@@ -1,0 +1,287 @@
+// Path scoring (vsd_score_paths).
+//
+// k_score_rows   one wavefront per row: online log-sum-exp of X/T_q over the
+//                draft vocabulary and of Y/T_p over the whole target
+//                vocabulary (128-bit loads, exp2 with folded scales, per-lane
+//                chunk max), then the token gathers giving log q, log p and
+//                log alpha = min(0, log p - log q) of the three families
+//                (Sec. "Preliminary", Eq. acc).
+// k_combine      one workgroup per position, one thread per path: prefix sums
+//                over depth (Eqs. kappa, survival_def, accepted_len_cond), the
+//                oracle gate and the correction (Alg. 2, Alg. 1), ARW beta
+//                (Eq. beta_update), CAR zeta (Eq. zeta_update), the loss of
+//                Eq. advance / Eq. basic and the per-row coefficients a, b.
+// k_loss_total   one workgroup: loss_scale * sum over positions, fixed order.
+#include "vsd_device.hpp"
+#include "vsd_kernels.hpp"
+
+namespace vsd {
+
+namespace {
+
+constexpr int kRowsPerBlock = 4;
+
+// Online log2-sum-exp2 of row[v] * c over v < V, reduced over the wavefront.
+// m = running max of row*c, s = sum of exp2(row*c - m).  c > 0.
+template <typename T>
+__device__ __forceinline__ void row_lse2(const T* row, int V, float c, int lane, float& m, float& s) {
+  m = kNegBig;
+  s = 0.0f;
+  constexpr int U = 4;          // chunks in flight per lane
+  constexpr int step = 8 * kWave;
+  int base = lane * 8;
+  for (; base + (U - 1) * step + 8 <= V; base += U * step) {
+    float x[U][8];
+#pragma unroll
+    for (int u = 0; u < U; ++u) load8(row + base + u * step, x[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float cm = fmaxf(fmaxf(fmaxf(x[u][0], x[u][1]), fmaxf(x[u][2], x[u][3])),
+                       fmaxf(fmaxf(x[u][4], x[u][5]), fmaxf(x[u][6], x[u][7])));
+      cm *= c;
+      if (cm > m) {
+        s *= __builtin_amdgcn_exp2f(m - cm);
+        m = cm;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[u][k], c, -m));
+    }
+  }
+  for (; base + 8 <= V; base += step) {
+    float x[8];
+    load8(row + base, x);
+    float cm = x[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
+    cm *= c;
+    if (cm > m) {
+      s *= __builtin_amdgcn_exp2f(m - cm);
+      m = cm;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -m));
+  }
+  if (base < V) {  // the one partial chunk of the row
+    for (int v = base; v < V; ++v) {
+      const float xv = load1(row + v) * c;
+      if (xv > m) {
+        s *= __builtin_amdgcn_exp2f(m - xv);
+        m = xv;
+      }
+      s += __builtin_amdgcn_exp2f(xv - m);
+    }
+  }
+  wave_lse2(m, s);
+}
+
+template <typename T, bool MAPPED>
+__global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const int i = (int)(r % a.L);
+  const int64_t path = r / a.L;
+  int d = a.L;
+  if (a.depth != nullptr) {
+    d = a.depth[path];
+    if (d < 1 || d > a.L) {
+      if (lane == 0) report_error(a.err, VSD_DEVERR_DEPTH_RANGE);
+      d = 0;
+    }
+  }
+  if (i >= d) {  // masked slot: nothing is read, every output is zero
+    if (lane < 3) {
+      a.la[r * 3 + lane] = 0.0f;
+      a.lq[r * 3 + lane] = 0.0f;
+    }
+    if (lane == 0) {
+      a.lse_q[r] = 0.0f;
+      if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
+    }
+    return;
+  }
+  const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
+  const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
+  float mq, sq, mp, sp;
+  row_lse2(X, a.Vd, a.inv_tq * kLog2e, lane, mq, sq);
+  row_lse2(Y, a.Vt, a.inv_tp * kLog2e, lane, mp, sp);
+  const float lse_q = (mq + log2f(sq)) * kLn2;
+  const float lse_p = (mp + log2f(sp)) * kLn2;
+  if (lane < 3) {  // lane f gathers family f
+    const int32_t z = a.tok[lane][r];
+    float lq = 0.0f, la = 0.0f;
+    if ((uint32_t)z >= (uint32_t)a.Vd) {
+      report_error(a.err, VSD_DEVERR_TOKEN_RANGE);
+    } else {
+      const int32_t zt = MAPPED ? a.d2t[z] : z;
+      if ((uint32_t)zt >= (uint32_t)a.Vt) {
+        report_error(a.err, VSD_DEVERR_MAP_RANGE);
+      } else {
+        lq = load1(X + z) * a.inv_tq - lse_q;
+        const float lp = load1(Y + zt) * a.inv_tp - lse_p;
+        la = fminf(0.0f, lp - lq);
+      }
+    }
+    a.la[r * 3 + lane] = la;
+    a.lq[r * 3 + lane] = lq;
+  }
+  if (lane == 0) {
+    a.lse_q[r] = lse_q;
+    if (a.lse_p != nullptr) a.lse_p[r] = lse_p;
+  }
+}
+
+// Deterministic block reductions: butterfly within each wavefront, then the
+// per-wavefront partials combined in wavefront order by every thread.
+__device__ __forceinline__ float block_sum(float v, float* smem) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) smem[w] = v;
+  __syncthreads();
+  float t = 0.0f;
+  for (int k = 0; k < nw; ++k) t += smem[k];
+  return t;
+}
+
+__device__ __forceinline__ float block_max(float v, float* smem) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_max(v);
+  __syncthreads();
+  if (lane == 0) smem[w] = v;
+  __syncthreads();
+  float t = kNegBig;
+  for (int k = 0; k < nw; ++k) t = fmaxf(t, smem[k]);
+  return t;
+}
+
+__device__ __forceinline__ int block_sum_int(int v, int* smem) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum_int(v);
+  __syncthreads();
+  if (lane == 0) smem[w] = v;
+  __syncthreads();
+  int t = 0;
+  for (int k = 0; k < nw; ++k) t += smem[k];
+  return t;
+}
+
+__global__ __launch_bounds__(1024) void k_combine(CombineArgs a) {
+  __shared__ float redf[16];
+  __shared__ int redi[16];
+  const int pos = blockIdx.x;
+  const int s = threadIdx.x;
+  const bool real = s < a.N;
+  int d = 0;
+  if (real) {
+    d = a.depth != nullptr ? a.depth[(int64_t)pos * a.N + s] : a.L;
+    if (d < 1 || d > a.L) {
+      report_error(a.err, VSD_DEVERR_DEPTH_RANGE);
+      d = 0;
+    }
+  }
+  const int64_t row0 = ((int64_t)pos * a.N + s) * a.L;
+  float LSd = 0.0f, LSt = 0.0f, LSg = 0.0f, LQd = 0.0f, LQt = 0.0f;
+  float ea = 0.0f, wsum = 0.0f, lsum = 0.0f;
+  for (int l = 0; l < a.L; ++l) {
+    const bool live = real && l < d;
+    const int64_t row = row0 + l;
+    if (live) {  // prefix sums of log alpha (log survival) and of log q
+      LSd += a.la[row * 3 + 0];
+      LSt += a.la[row * 3 + 1];
+      LSg += a.la[row * 3 + 2];
+      LQd += a.lq[row * 3 + 0];
+      LQt += a.lq[row * 3 + 1];
+    }
+    // Alg. 2 gate on z~; Alg. 1 substitutes z' when it fails.
+    const bool acc = live && (LSd >= LSg);
+    const bool val = live && (acc || LSt >= LSg);
+    // ARW: leave-one-out acceptance rate among live paths with o' > 0; all
+    // o' at one level share w(l), which cancels (acc implies val).
+    const int n_acc = block_sum_int(acc ? 1 : 0, redi);
+    const int n_val = block_sum_int(val ? 1 : 0, redi);
+    const int num = n_acc - (acc ? 1 : 0);
+    const int den = n_val - (val ? 1 : 0);
+    const float beta = (live && den > 0) ? (float)num / (float)den : 0.0f;
+    // CAR: softmax over live paths of confidence / tau.
+    const float conf = a.car_input == VSD_CAR_PROB ? expf(LQd) : LQd;
+    const float cmax = block_max(live ? conf : kNegBig, redf);
+    const float e = live ? expf((conf - cmax) * a.inv_tau) : 0.0f;
+    const float esum = block_sum(e, redf);
+    const float zeta = live ? e / esum : 0.0f;
+    const float c = a.mode == VSD_GRAD_ARW_CAR ? beta * zeta : a.mode == VSD_GRAD_ARW ? beta : 0.0f;
+    const float o = val ? a.w[l] : 0.0f;
+    const float surv = live ? expf(LSd) : 0.0f;
+    ea += surv;
+    wsum += o;
+    if (live) lsum += o * ((acc ? LQd : LQt) - c * LQd);
+    if (real) {
+      if (a.survival) a.survival[row] = surv;
+      if (a.acc_flag) a.acc_flag[row] = acc ? 1 : 0;
+      if (a.val_flag) a.val_flag[row] = val ? 1 : 0;
+      if (a.o_prime) a.o_prime[row] = o;
+      if (a.beta) a.beta[row] = beta;
+      if (a.zeta) a.zeta[row] = zeta;
+      // level-l terms of the coefficient suffix sums, finished below
+      a.coef_a[row] = o * ((acc ? 1.0f : 0.0f) - c);
+      a.coef_b[row] = o * (acc ? 0.0f : 1.0f);
+    }
+  }
+  const float W = block_sum(wsum, redf);
+  const float total = block_sum(lsum, redf);
+  if (real) {
+    // a_{s,i} = (1/W) sum_{l>=i} o'(I~ - c),  b_{s,i} = (1/W) sum_{l>=i} o'(1 - I~)
+    float acc_a = 0.0f, acc_b = 0.0f;
+    for (int l = a.L - 1; l >= 0; --l) {
+      const int64_t row = row0 + l;
+      if (l < d && W > 0.0f) {
+        acc_a += a.coef_a[row];
+        acc_b += a.coef_b[row];
+        a.coef_a[row] = acc_a / W;
+        a.coef_b[row] = acc_b / W;
+      } else {
+        a.coef_a[row] = 0.0f;
+        a.coef_b[row] = 0.0f;
+      }
+    }
+    if (a.ea) a.ea[(int64_t)pos * a.N + s] = ea;
+  }
+  if (threadIdx.x == 0) a.loss_pos[pos] = W > 0.0f ? -total / W : 0.0f;
+}
+
+__global__ __launch_bounds__(256) void k_loss_total(const float* loss_pos, int32_t P, float scale, float* out) {
+  __shared__ float red[16];
+  float t = 0.0f;
+  for (int p = threadIdx.x; p < P; p += blockDim.x) t += loss_pos[p];
+  t = block_sum(t, red);
+  if (threadIdx.x == 0) *out = scale * t;
+}
+
+template <typename T>
+hipError_t launch_rows_t(const ScoreRowArgs& a, hipStream_t s) {
+  const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
+  if (a.d2t != nullptr)
+    hipLaunchKernelGGL((k_score_rows<T, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_score_rows<T, false>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s) {
+  return bf16 ? launch_rows_t<bf16_t>(a, s) : launch_rows_t<float>(a, s);
+}
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
+  const int threads = ((a.N + kWave - 1) / kWave) * kWave;
+  hipLaunchKernelGGL(k_combine, dim3((unsigned)a.P), dim3(threads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_total(const float* loss_pos, int32_t P, float scale, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(256), 0, s, loss_pos, P, scale, out);
+  return hipGetLastError();
+}
+
+}  // namespace vsd

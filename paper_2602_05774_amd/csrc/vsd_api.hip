@@ -1,0 +1,300 @@
+// Host side of the C ABI declared in include/vsd.h: argument validation
+// (before any launch), workspace layout, launch geometry, error reporting.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "vsd_device.hpp"
+#include "vsd_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+vsd_status fail(vsd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+vsd_status ok() {
+  g_last_error.clear();
+  return VSD_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
+
+constexpr int64_t kMaxRows = (int64_t)1 << 31;
+
+size_t align_up(size_t n) { return (n + 255) & ~(size_t)255; }
+
+int64_t rows_of(const vsd_dims* d) { return (int64_t)d->B * d->T * d->N * d->L; }
+
+// Shape checks shared by every entry point.
+vsd_status check_dims(const vsd_dims* d) {
+  if (d == nullptr) return fail(VSD_ERR_NULL_POINTER, "dims is NULL");
+  if (d->B < 1 || d->T < 1) return fail(VSD_ERR_INVALID_SHAPE, "B=%d T=%d must be >= 1", d->B, d->T);
+  if (d->N < 1 || d->N > 1024) return fail(VSD_ERR_INVALID_SHAPE, "N=%d outside [1,1024]", d->N);
+  if (d->L < 1 || d->L > vsd::kMaxL) return fail(VSD_ERR_INVALID_SHAPE, "L=%d outside [1,64]", d->L);
+  if (d->v_draft < 1) return fail(VSD_ERR_INVALID_SHAPE, "v_draft=%d must be >= 1", d->v_draft);
+  if (d->v_target < d->v_draft)
+    return fail(VSD_ERR_INVALID_SHAPE, "v_target=%d < v_draft=%d (the map must be injective)", d->v_target,
+                d->v_draft);
+  if (d->dtype != VSD_F32 && d->dtype != VSD_BF16) return fail(VSD_ERR_INVALID_VALUE, "dtype=%d", d->dtype);
+  const int64_t R = rows_of(d);
+  if (R >= kMaxRows) return fail(VSD_ERR_INVALID_SHAPE, "R=B*T*N*L=%lld must be < 2^31", (long long)R);
+  return VSD_OK;
+}
+
+// Materialised-logit checks for one source.
+vsd_status check_logits(const vsd_dims* d, const vsd_src* src, const char* name, int64_t ld, int32_t v) {
+  if (src == nullptr) return fail(VSD_ERR_NULL_POINTER, "%s source is NULL", name);
+  if (src->logits == nullptr) {
+    if (src->hidden != nullptr || src->weight != nullptr)
+      return fail(VSD_ERR_UNSUPPORTED, "%s: the fused LM-head source is not available in this build", name);
+    return fail(VSD_ERR_NULL_POINTER, "%s logits are NULL", name);
+  }
+  const int64_t es = d->dtype == VSD_F32 ? 4 : 2;
+  if (ld < v) return fail(VSD_ERR_INVALID_SHAPE, "%s ld=%lld < v=%d", name, (long long)ld, v);
+  if ((ld * es) % 16 != 0)
+    return fail(VSD_ERR_MISALIGNED, "%s row stride %lld bytes is not a multiple of 16", name, (long long)(ld * es));
+  if (!aligned16(src->logits)) return fail(VSD_ERR_MISALIGNED, "%s logits pointer not 16-byte aligned", name);
+  return VSD_OK;
+}
+
+vsd_status check_map(const vsd_dims* d, const int32_t* d2t) {
+  if (d->v_draft != d->v_target && d2t == nullptr)
+    return fail(VSD_ERR_MAP_REQUIRED, "v_draft=%d != v_target=%d requires d2t", d->v_draft, d->v_target);
+  if (d2t != nullptr && !aligned16(d2t)) return fail(VSD_ERR_MISALIGNED, "d2t pointer not 16-byte aligned");
+  return VSD_OK;
+}
+
+vsd_status check_params(const vsd_params* p) {
+  if (p == nullptr) return fail(VSD_ERR_NULL_POINTER, "params is NULL");
+  if (!finite_pos(p->temp_draft) || !finite_pos(p->temp_target))
+    return fail(VSD_ERR_INVALID_VALUE, "temperatures must be finite and > 0");
+  if (!finite_pos(p->w_base)) return fail(VSD_ERR_INVALID_VALUE, "w_base must be finite and > 0");
+  if (!finite_pos(p->car_tau)) return fail(VSD_ERR_INVALID_VALUE, "car_tau must be finite and > 0");
+  if (p->mode < VSD_GRAD_BASIC || p->mode > VSD_GRAD_ARW_CAR) return fail(VSD_ERR_INVALID_VALUE, "mode=%d", p->mode);
+  if (p->car_input != VSD_CAR_PROB && p->car_input != VSD_CAR_LOGPROB)
+    return fail(VSD_ERR_INVALID_VALUE, "car_input=%d", p->car_input);
+  if (!std::isfinite(p->loss_scale)) return fail(VSD_ERR_INVALID_VALUE, "loss_scale must be finite");
+  return VSD_OK;
+}
+
+vsd_status hip_fail(hipError_t e, const char* what) {
+  return fail(VSD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct WorkspaceLayout {
+  size_t la, lq, loss, total;
+};
+
+WorkspaceLayout workspace_layout(const vsd_dims* d) {
+  const int64_t R = rows_of(d);
+  const int64_t P = (int64_t)d->B * d->T;
+  WorkspaceLayout w;
+  w.la = 0;
+  w.lq = w.la + align_up((size_t)R * 3 * sizeof(float));
+  w.loss = w.lq + align_up((size_t)R * 3 * sizeof(float));
+  w.total = w.loss + align_up((size_t)P * sizeof(float));
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t vsd_abi_version(void) { return VSD_ABI_VERSION; }
+
+const char* vsd_status_string(vsd_status s) {
+  switch (s) {
+    case VSD_OK: return "VSD_OK";
+    case VSD_ERR_NULL_POINTER: return "VSD_ERR_NULL_POINTER";
+    case VSD_ERR_INVALID_SHAPE: return "VSD_ERR_INVALID_SHAPE";
+    case VSD_ERR_INVALID_VALUE: return "VSD_ERR_INVALID_VALUE";
+    case VSD_ERR_MISALIGNED: return "VSD_ERR_MISALIGNED";
+    case VSD_ERR_MAP_REQUIRED: return "VSD_ERR_MAP_REQUIRED";
+    case VSD_ERR_UNSUPPORTED: return "VSD_ERR_UNSUPPORTED";
+    case VSD_ERR_WORKSPACE: return "VSD_ERR_WORKSPACE";
+    case VSD_ERR_HIP: return "VSD_ERR_HIP";
+  }
+  return "VSD_ERR_UNKNOWN";
+}
+
+const char* vsd_last_error(void) { return g_last_error.c_str(); }
+
+vsd_status vsd_score_workspace_bytes(const vsd_dims* dims, size_t* bytes) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if (bytes == nullptr) return fail(VSD_ERR_NULL_POINTER, "bytes is NULL");
+  *bytes = workspace_layout(dims).total;
+  return ok();
+}
+
+vsd_status vsd_sample_paths(const vsd_dims* dims, const vsd_src* draft, const vsd_src* target,
+                            const int32_t* d2t, const int32_t* valid_depth, float temp_draft,
+                            float temp_target, uint64_t seed, uint32_t offset, int32_t* tok_draft,
+                            int32_t* tok_target, int32_t* tok_greedy, int32_t* device_error,
+                            void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
+  if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (!finite_pos(temp_draft) || !finite_pos(temp_target))
+    return fail(VSD_ERR_INVALID_VALUE, "temperatures must be finite and > 0");
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
+  if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+
+  vsd::SampleArgs a{};
+  a.X = draft->logits;
+  a.Y = target->logits;
+  a.d2t = d2t;
+  a.depth = valid_depth;
+  a.tok_d = tok_draft;
+  a.tok_t = tok_target;
+  a.tok_g = tok_greedy;
+  a.err = device_error;
+  a.R = rows_of(dims);
+  a.ld_d = dims->ld_draft;
+  a.ld_t = dims->ld_target;
+  a.L = dims->L;
+  a.Vd = dims->v_draft;
+  a.Vt = dims->v_target;
+  a.inv_tq = 1.0f / temp_draft;
+  a.inv_tp = 1.0f / temp_target;
+  a.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(seed >> 32);
+  a.offset = offset;
+  hipError_t e = vsd::launch_sample(a, dims->dtype == VSD_BF16, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "k_sample launch");
+  return ok();
+}
+
+vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                           const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                           const int32_t* tok_draft, const int32_t* tok_target, const int32_t* tok_greedy,
+                           const vsd_score_out* out, void* workspace, size_t workspace_bytes,
+                           void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
+  if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
+  if (out == nullptr) return fail(VSD_ERR_NULL_POINTER, "out is NULL");
+  if (out->lse_draft == nullptr || out->coef_a == nullptr || out->coef_b == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "out->lse_draft, coef_a and coef_b are required");
+  if (out->device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "out->device_error is NULL");
+  const WorkspaceLayout wl = workspace_layout(dims);
+  if (workspace == nullptr || workspace_bytes < wl.total)
+    return fail(VSD_ERR_WORKSPACE, "workspace of %zu bytes required, %zu given", wl.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned16(workspace)) return fail(VSD_ERR_MISALIGNED, "workspace not 16-byte aligned");
+
+  char* ws = static_cast<char*>(workspace);
+  float* la = out->log_alpha != nullptr ? out->log_alpha : reinterpret_cast<float*>(ws + wl.la);
+  float* lq = out->log_q_tok != nullptr ? out->log_q_tok : reinterpret_cast<float*>(ws + wl.lq);
+  float* loss_pos = out->loss_pos != nullptr ? out->loss_pos : reinterpret_cast<float*>(ws + wl.loss);
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+  vsd::ScoreRowArgs ra{};
+  ra.X = draft->logits;
+  ra.Y = target->logits;
+  ra.d2t = d2t;
+  ra.depth = valid_depth;
+  ra.tok[0] = tok_draft;
+  ra.tok[1] = tok_target;
+  ra.tok[2] = tok_greedy;
+  ra.lse_q = out->lse_draft;
+  ra.lse_p = out->lse_target;
+  ra.la = la;
+  ra.lq = lq;
+  ra.err = out->device_error;
+  ra.R = rows_of(dims);
+  ra.ld_d = dims->ld_draft;
+  ra.ld_t = dims->ld_target;
+  ra.L = dims->L;
+  ra.Vd = dims->v_draft;
+  ra.Vt = dims->v_target;
+  ra.inv_tq = 1.0f / params->temp_draft;
+  ra.inv_tp = 1.0f / params->temp_target;
+  hipError_t e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
+  if (e != hipSuccess) return hip_fail(e, "k_score_rows launch");
+
+  vsd::CombineArgs ca{};
+  ca.la = la;
+  ca.lq = lq;
+  ca.depth = valid_depth;
+  ca.survival = out->survival;
+  ca.ea = out->exp_accept_len;
+  ca.acc_flag = out->accept_flag;
+  ca.val_flag = out->valid_flag;
+  ca.o_prime = out->o_prime;
+  ca.beta = out->beta;
+  ca.zeta = out->zeta;
+  ca.coef_a = out->coef_a;
+  ca.coef_b = out->coef_b;
+  ca.loss_pos = loss_pos;
+  ca.err = out->device_error;
+  ca.P = dims->B * dims->T;
+  ca.N = dims->N;
+  ca.L = dims->L;
+  ca.mode = params->mode;
+  ca.car_input = params->car_input;
+  ca.inv_tau = 1.0f / params->car_tau;
+  for (int l = 0; l < dims->L; ++l) ca.w[l] = (float)std::pow((double)params->w_base, (double)(l + 1));
+  e = vsd::launch_combine(ca, s);
+  if (e != hipSuccess) return hip_fail(e, "k_combine launch");
+  if (out->loss_total != nullptr) {
+    e = vsd::launch_loss_total(loss_pos, ca.P, params->loss_scale, out->loss_total, s);
+    if (e != hipSuccess) return hip_fail(e, "k_loss_total launch");
+  }
+  return ok();
+}
+
+vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                                 const float* lse_draft, const int32_t* tok_draft, const int32_t* tok_target,
+                                 const float* coef_a, const float* coef_b, const vsd_grad* grad,
+                                 int32_t* device_error, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
+  if (lse_draft == nullptr || tok_draft == nullptr || tok_target == nullptr || coef_a == nullptr ||
+      coef_b == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "lse_draft, tokens and coefficients are required");
+  if (grad == nullptr || grad->grad_logits == nullptr) return fail(VSD_ERR_NULL_POINTER, "grad->grad_logits is NULL");
+  if (!aligned16(grad->grad_logits)) return fail(VSD_ERR_MISALIGNED, "grad_logits not 16-byte aligned");
+  if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+
+  vsd::BwdArgs a{};
+  a.X = draft->logits;
+  a.G = grad->grad_logits;
+  a.lse_q = lse_draft;
+  a.tok_d = tok_draft;
+  a.tok_t = tok_target;
+  a.coef_a = coef_a;
+  a.coef_b = coef_b;
+  a.R = rows_of(dims);
+  a.ld = dims->ld_draft;
+  a.Vd = dims->v_draft;
+  a.inv_tq = 1.0f / params->temp_draft;
+  a.scale = params->loss_scale;
+  hipError_t e = vsd::launch_bwd(a, dims->dtype == VSD_BF16, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "k_bwd launch");
+  return ok();
+}
+
+}  // extern "C"

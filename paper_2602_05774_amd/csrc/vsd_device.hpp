@@ -1,0 +1,193 @@
+// Device-side helpers shared by the VSD kernels (gfx950, wave64).
+//
+//  * Philox4x32-10 (Salmon et al., SC'11) and the library's normative float32
+//    logarithm / Gumbel variate, exactly as the sampler definition in vsd.h
+//    states them: one IEEE binary32 operation per step, no contraction.
+//  * 128-bit loads of 8 logits (bf16 or fp32) and 128-bit bf16 stores.
+//  * Wavefront reductions (butterfly over all 64 lanes, so every lane ends
+//    with the same, order-independent result).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/vsd.h"
+
+namespace vsd {
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegBig = -3.402823466e+38f;  // -FLT_MAX: an "empty" max
+
+using bf16_t = uint16_t;  // bf16 storage
+
+// ---------------------------------------------------------------- Philox ---
+__device__ __forceinline__ void mulhilo32(uint32_t a, uint32_t b, uint32_t& hi, uint32_t& lo) {
+  const uint64_t p = (uint64_t)a * (uint64_t)b;  // v_mad_u64_u32
+  hi = (uint32_t)(p >> 32);
+  lo = (uint32_t)p;
+}
+
+// Ten Philox4x32 rounds on counter (c0,c1,c2,c3) with key (k0,k1).
+__device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                               uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int j = 0; j < 10; ++j) {
+    uint32_t hi0, lo0, hi1, lo1;
+    mulhilo32(0xD2511F53u, c0, hi0, lo0);
+    mulhilo32(0xCD9E8D57u, c2, hi1, lo1);
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return make_uint4(c0, c1, c2, c3);
+}
+
+// ------------------------------------------------- normative log / Gumbel ---
+// Natural log of a positive normal float: x = 2^e m, m in (sqrt(1/2), sqrt(2)],
+// log m = 2 atanh(f / (2 + f)) by its odd series through s^9, e ln2 split
+// hi/lo.  Every line is one correctly rounded binary32 operation.
+__device__ __forceinline__ float spec_log(float x) {
+#pragma clang fp contract(off)
+  const uint32_t b = __float_as_uint(x);
+  int e = (int)((b >> 23) & 0xFFu) - 127;
+  float m = __uint_as_float((b & 0x7FFFFFu) | 0x3F800000u);
+  if (m > __uint_as_float(0x3FB504F3u)) {
+    m = m * 0.5f;
+    e = e + 1;
+  }
+  const float f = m - 1.0f;
+  const float s = f / (2.0f + f);
+  const float z = s * s;
+  float p = __uint_as_float(0x3DE38E39u);        // 1/9
+  p = __uint_as_float(0x3E124925u) + z * p;      // 1/7
+  p = __uint_as_float(0x3E4CCCCDu) + z * p;      // 1/5
+  p = __uint_as_float(0x3EAAAAABu) + z * p;      // 1/3
+  const float t2 = s + s;
+  const float lm = t2 + t2 * (z * p);
+  const float ef = (float)e;
+  return ef * __uint_as_float(0x3F317200u) + (lm + ef * __uint_as_float(0x35BFBE8Eu));
+}
+
+// G = -log(-log u), u = (2 (w >> 9) + 1) 2^-24.
+__device__ __forceinline__ float gumbel_from_word(uint32_t w) {
+#pragma clang fp contract(off)
+  const float u = (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-8f;
+  const float e = -spec_log(u);
+  return -spec_log(e);
+}
+
+// key = float(logit * invT) + G   (two roundings, as the definition fixes).
+__device__ __forceinline__ float gumbel_key(float logit, float inv_t, uint32_t w) {
+#pragma clang fp contract(off)
+  const float xs = logit * inv_t;
+  return xs + gumbel_from_word(w);
+}
+
+// ----------------------------------------------------------- loads/stores ---
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+__device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
+  const uint4 a = *reinterpret_cast<const uint4*>(p);
+  v[0] = bf16_lo(a.x); v[1] = bf16_hi(a.x);
+  v[2] = bf16_lo(a.y); v[3] = bf16_hi(a.y);
+  v[4] = bf16_lo(a.z); v[5] = bf16_hi(a.z);
+  v[6] = bf16_lo(a.w); v[7] = bf16_hi(a.w);
+}
+
+__device__ __forceinline__ void load8(const int32_t* p, int32_t (&v)[8]) {
+  const int4 a = reinterpret_cast<const int4*>(p)[0];
+  const int4 b = reinterpret_cast<const int4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+__device__ __forceinline__ float load1(const float* p) { return *p; }
+__device__ __forceinline__ float load1(const bf16_t* p) { return __uint_as_float((uint32_t)(*p) << 16); }
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo;
+  const __bf16 b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+__device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
+  *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                            pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+}
+
+__device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store1(bf16_t* p, float v) {
+  *p = __builtin_bit_cast(uint16_t, (__bf16)v);
+}
+
+// ------------------------------------------------------ wave reductions ---
+// (key, index) maximum; equal keys resolve to the smaller index.
+__device__ __forceinline__ void wave_argmax(float& key, int& idx) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ok = __shfl_xor(key, off, kWave);
+    const int oi = __shfl_xor(idx, off, kWave);
+    if (ok > key || (ok == key && oi < idx)) {
+      key = ok;
+      idx = oi;
+    }
+  }
+}
+
+// Combine per-lane (max, sum of exp2(x - max)) pairs in the log2 domain.
+__device__ __forceinline__ void wave_lse2(float& m, float& s) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float om = __shfl_xor(m, off, kWave);
+    const float os = __shfl_xor(s, off, kWave);
+    const float nm = fmaxf(m, om);
+    s = s * __builtin_amdgcn_exp2f(m - nm) + os * __builtin_amdgcn_exp2f(om - nm);
+    m = nm;
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// First device-side data error wins; later ones are dropped.
+__device__ __forceinline__ void report_error(int32_t* err, int32_t code) {
+  atomicCAS(err, 0, code);
+}
+
+}  // namespace vsd

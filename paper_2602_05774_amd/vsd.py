@@ -1,0 +1,218 @@
+"""Python binding of the VSD C ABI over torch device tensors.
+
+Argument marshalling only: tensors are checked for device, dtype, shape and
+contiguity, outputs are allocated with torch (device memory), and every step
+of the computation runs in libvsd.so on the current HIP stream.
+
+Layout (see include/vsd.h): row r = ((b*T + t)*N + s)*L + (i-1); logits are
+[R, ld] with ld >= v and 16-byte rows; tokens, per-row outputs [R]; per-path
+outputs [B*T*N]; per-position outputs [B*T].
+"""
+import ctypes
+from dataclasses import dataclass
+from typing import NamedTuple, Optional
+
+import torch
+
+from . import _lib
+from ._lib import (VSD_BF16, VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_F32, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR,
+                   VSD_GRAD_BASIC, VsdError)
+
+__all__ = ["Problem", "Params", "SampleResult", "ScoreResult", "sample_paths", "score_paths",
+           "weighted_loss_bwd", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
+           "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]
+
+
+@dataclass(frozen=True)
+class Problem:
+    B: int
+    T: int
+    N: int
+    L: int
+    v_draft: int
+    v_target: int
+
+    @property
+    def R(self):
+        return self.B * self.T * self.N * self.L
+
+    @property
+    def P(self):
+        return self.B * self.T
+
+
+@dataclass(frozen=True)
+class Params:
+    temp_draft: float = 1.0
+    temp_target: float = 1.0
+    w_base: float = 1.05
+    car_tau: float = 0.2
+    mode: int = VSD_GRAD_ARW_CAR
+    car_input: int = VSD_CAR_PROB
+    loss_scale: float = 1.0
+
+    def c(self):
+        return _lib.VsdParams(self.temp_draft, self.temp_target, self.w_base, self.car_tau,
+                              self.mode, self.car_input, self.loss_scale)
+
+
+class SampleResult(NamedTuple):
+    tok_draft: torch.Tensor
+    tok_target: torch.Tensor
+    tok_greedy: torch.Tensor
+    device_error: torch.Tensor
+
+
+class ScoreResult(NamedTuple):
+    lse_draft: torch.Tensor
+    lse_target: torch.Tensor
+    log_alpha: torch.Tensor
+    log_q_tok: torch.Tensor
+    survival: torch.Tensor
+    exp_accept_len: torch.Tensor
+    accept_flag: torch.Tensor
+    valid_flag: torch.Tensor
+    o_prime: torch.Tensor
+    beta: torch.Tensor
+    zeta: torch.Tensor
+    coef_a: torch.Tensor
+    coef_b: torch.Tensor
+    loss_pos: torch.Tensor
+    loss_total: torch.Tensor
+    device_error: torch.Tensor
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return VSD_BF16
+    if t.dtype == torch.float32:
+        return VSD_F32
+    raise ValueError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def _check_logits(name, t, prob, v):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dim() != 2 or t.shape[0] != prob.R or t.shape[1] < v or t.stride(1) != 1:
+        raise ValueError(f"{name} must be [R={prob.R}, ld>={v}] with unit column stride, got {tuple(t.shape)}")
+
+
+def _check_i32(name, t, numel):
+    if t is None:
+        return
+    if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous() or t.numel() != numel:
+        raise ValueError(f"{name} must be a contiguous int32 device tensor of {numel} elements")
+
+
+def _dims(prob, X, Y):
+    dt = _dtype_code(X)
+    if Y is not None and Y.dtype != X.dtype:
+        raise ValueError("draft and target logits must share a dtype")
+    return _lib.VsdDims(prob.B, prob.T, prob.N, prob.L, prob.v_draft, prob.v_target, dt, 0,
+                        X.stride(0), Y.stride(0) if Y is not None else X.stride(0))
+
+
+def _src(t):
+    return _lib.VsdSrc(t.data_ptr(), None, None)
+
+
+def sample_paths(prob, X, Y, d2t=None, valid_depth=None, temp_draft=1.0, temp_target=1.0,
+                 seed=0, offset=0, device_error=None):
+    """E-step draws: tokens of the draft proposal, target correction and greedy
+    reference families ([R] int32 each, -1 on masked rows)."""
+    lib = _lib.load()
+    _check_logits("X", X, prob, prob.v_draft)
+    _check_logits("Y", Y, prob, prob.v_target)
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    dev = X.device
+    toks = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    if device_error is None:
+        device_error = torch.zeros(1, dtype=torch.int32, device=dev)
+    dims = _dims(prob, X, Y)
+    _lib.check(lib.vsd_sample_paths(ctypes.byref(dims), ctypes.byref(_src(X)), ctypes.byref(_src(Y)),
+                                    _ptr(d2t), _ptr(valid_depth), temp_draft, temp_target,
+                                    int(seed), int(offset), _ptr(toks[0]), _ptr(toks[1]), _ptr(toks[2]),
+                                    _ptr(device_error), _stream(dev)))
+    return SampleResult(toks[0], toks[1], toks[2], device_error)
+
+
+def score_workspace_bytes(prob, dtype=torch.bfloat16):
+    lib = _lib.load()
+    dims = _lib.VsdDims(prob.B, prob.T, prob.N, prob.L, prob.v_draft, prob.v_target,
+                        VSD_BF16 if dtype == torch.bfloat16 else VSD_F32, 0, prob.v_draft, prob.v_target)
+    n = ctypes.c_size_t(0)
+    _lib.check(lib.vsd_score_workspace_bytes(ctypes.byref(dims), ctypes.byref(n)))
+    return n.value
+
+
+def alloc_score_outputs(prob, device, full=True):
+    """Output tensors for score_paths (optional ones only when full=True)."""
+    R, P, PN = prob.R, prob.P, prob.P * prob.N
+    f = lambda n: torch.empty(n, dtype=torch.float32, device=device)
+    u8 = lambda n: torch.empty(n, dtype=torch.uint8, device=device)
+    return ScoreResult(
+        lse_draft=f(R), lse_target=f(R) if full else None,
+        log_alpha=f(R * 3) if full else None, log_q_tok=f(R * 3) if full else None,
+        survival=f(R) if full else None, exp_accept_len=f(PN) if full else None,
+        accept_flag=u8(R) if full else None, valid_flag=u8(R) if full else None,
+        o_prime=f(R) if full else None, beta=f(R) if full else None, zeta=f(R) if full else None,
+        coef_a=f(R), coef_b=f(R), loss_pos=f(P) if full else None, loss_total=f(1),
+        device_error=torch.zeros(1, dtype=torch.int32, device=device))
+
+
+def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None, valid_depth=None,
+                out: Optional[ScoreResult] = None, workspace=None):
+    """Path scoring, oracle gate, ARW/CAR weights, loss and per-row coefficients."""
+    lib = _lib.load()
+    _check_logits("X", X, prob, prob.v_draft)
+    _check_logits("Y", Y, prob, prob.v_target)
+    for name, t in (("tok_draft", tok_draft), ("tok_target", tok_target), ("tok_greedy", tok_greedy)):
+        _check_i32(name, t, prob.R)
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    dev = X.device
+    if out is None:
+        out = alloc_score_outputs(prob, dev)
+    nbytes = score_workspace_bytes(prob, X.dtype)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dims = _dims(prob, X, Y)
+    names = [f[0] for f in _lib.VsdScoreOut._fields_]
+    so = _lib.VsdScoreOut(*[None if getattr(out, k) is None else getattr(out, k).data_ptr() for k in names])
+    pr = params.c()
+    _lib.check(lib.vsd_score_paths(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
+                                   ctypes.byref(_src(Y)), _ptr(d2t), _ptr(valid_depth), _ptr(tok_draft),
+                                   _ptr(tok_target), _ptr(tok_greedy), ctypes.byref(so),
+                                   _ptr(workspace), workspace.numel(), _stream(dev)))
+    return out
+
+
+def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,
+                      grad=None, device_error=None):
+    """Gradient of loss_scale * sum_x L_x with respect to the draft logits
+    (same shape, stride and dtype as X)."""
+    lib = _lib.load()
+    _check_logits("X", X, prob, prob.v_draft)
+    dev = X.device
+    if grad is None:
+        grad = torch.empty_like(X)
+    if grad.shape != X.shape or grad.stride() != X.stride() or grad.dtype != X.dtype:
+        raise ValueError("grad must match X in shape, stride and dtype")
+    if device_error is None:
+        device_error = torch.zeros(1, dtype=torch.int32, device=dev)
+    dims = _dims(prob, X, None)
+    pr = params.c()
+    g = _lib.VsdGrad(grad.data_ptr(), None, None)
+    _lib.check(lib.vsd_weighted_loss_bwd(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
+                                         _ptr(lse_draft), _ptr(tok_draft), _ptr(tok_target), _ptr(coef_a),
+                                         _ptr(coef_b), ctypes.byref(g), _ptr(device_error), _stream(dev)))
+    return grad

@@ -69,7 +69,8 @@ def get_config(name):
     return CONFIGS[name]
 
 
-def scaled(name, **overrides):
+def scaled(base_name, **overrides):
     """A config of the same recipe with some fields replaced (smaller B, T ...)."""
-    base = CONFIGS[name]
-    return replace(base, name=overrides.pop("name", base.name + "-scaled"), **overrides)
+    base = CONFIGS[base_name]
+    overrides.setdefault("name", base.name + "-scaled")
+    return replace(base, **overrides)

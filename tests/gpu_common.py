@@ -1,0 +1,161 @@
+"""Shared helpers of the GPU parity tests: run one EM step through the C ABI,
+run the oracle on the same seeded inputs, and compare under the stated bars.
+
+Bars (floating point against the float64 oracle):
+  log-domain values (log alpha, log q, log-sum-exp)   |d| <= 1e-3 * max(1, |ref|)
+  linear values (survival, E[A], o', beta, zeta, a, b,
+                 per-position loss, total loss)       |d| <= 1e-3 * |ref| + 1e-6
+  gradients, fp32 output                              |d| <= 2e-3
+  gradients, bf16 output                              |d| <= 2e-3, or <= one bf16
+                                                      ulp of ref where |ref| >= 1
+Integers (tokens, oracle flags) are compared exactly.  A flag may differ only
+where the oracle's float64 margin between the compared log-survivals is below
+1e-4 * max(1, |LS of the greedy path|) (a near-tie that float32 accumulation can
+resolve either way); such positions are reported and left out of the float
+comparisons that follow from the flags.
+"""
+import sys
+
+import numpy as np
+import torch
+
+import paper_2602_05774_amd as vsd
+from oracle import reference
+from synth.gen import rows_to_host
+
+TIE_REL = 1e-4
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def problem_of(cfg):
+    return vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+
+
+def params_of(cfg, **kw):
+    return vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target, **kw)
+
+
+def run_step(cfg, inp, params=None, tokens=None):
+    """sample -> score -> backward on the GPU; returns device tensors."""
+    prob = problem_of(cfg)
+    params = params or params_of(cfg)
+    if tokens is None:
+        smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"], params.temp_draft,
+                               params.temp_target, cfg.philox_seed, cfg.philox_offset)
+        tokens = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
+        err_s = smp.device_error
+    else:
+        err_s = torch.zeros(1, dtype=torch.int32, device=inp["X"].device)
+    sc = vsd.score_paths(prob, params, inp["X"], inp["Y"], *tokens, inp["d2t"], inp["valid_depth"])
+    grad = vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a,
+                                 sc.coef_b)
+    torch.cuda.synchronize()
+    return dict(tokens=tokens, score=sc, grad=grad, err_sample=err_s)
+
+
+def oracle_positions(cfg, inp, positions, params=None, tokens=None, want_grad=True):
+    """Oracle outputs for a list of positions (inputs copied from the device)."""
+    params = params or params_of(cfg)
+    rows = (np.asarray(positions)[:, None] * cfg.N * cfg.L + np.arange(cfg.N * cfg.L)[None]).reshape(-1)
+    X = rows_to_host(inp["X"], rows, cfg.v_draft)
+    Y = rows_to_host(inp["Y"], rows, cfg.v_target)
+    d2t = None if inp["d2t"] is None else inp["d2t"].cpu().numpy()
+    depth = None
+    if inp["valid_depth"] is not None:
+        depth = inp["valid_depth"].reshape(-1, cfg.N).cpu().numpy()[np.asarray(positions)]
+    tok = None
+    if tokens is not None:
+        tok = tuple(t.cpu().numpy()[rows] for t in tokens)
+    p = dict(temp_draft=params.temp_draft, temp_target=params.temp_target, w_base=params.w_base,
+             car_tau=params.car_tau, mode=params.mode, car_input=params.car_input, loss_scale=params.loss_scale)
+    ora = reference.run_positions(X, Y, d2t, depth, list(positions), cfg.N, cfg.L, p, seed=cfg.philox_seed,
+                                  offset=cfg.philox_offset, tokens=tok, want_grad=want_grad)
+    return rows, ora
+
+
+def _lin_ok(got, ref):
+    return np.abs(got - ref) <= 1e-3 * np.abs(ref) + 1e-6
+
+
+def _log_ok(got, ref):
+    return np.abs(got - ref) <= 1e-3 * np.maximum(1.0, np.abs(ref))
+
+
+def _bf16_ulp(x):
+    e = np.floor(np.log2(np.maximum(np.abs(x), 1e-30)))
+    return np.exp2(e - 7)
+
+
+def compare(cfg, gpu, rows, ora, positions, check_grad=True, label=""):
+    """Assert GPU == oracle on the given rows/positions; returns a summary dict."""
+    N, L = cfg.N, cfg.L
+    npos = len(positions)
+    sc = gpu["score"]
+    host = lambda t, idx=rows: t.cpu().numpy()[idx]
+    # 1. tokens: bit-exact
+    for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), gpu["tokens"]):
+        got = host(t)
+        bad = np.nonzero(got != ora[name])[0]
+        assert bad.size == 0, f"{label} {name}: {bad.size} mismatches, first row {rows[bad[0]]}: gpu {got[bad[0]]} oracle {ora[name][bad[0]]}"
+    # 2. flags: exact except oracle near-ties
+    LS = ora["LS"]                                    # [rows, 3] float64 log survival
+    ref_ls = np.maximum(1.0, np.abs(LS[:, 2]))
+    tie_acc = np.abs(LS[:, 0] - LS[:, 2]) / ref_ls < TIE_REL
+    tie_cor = np.abs(LS[:, 1] - LS[:, 2]) / ref_ls < TIE_REL
+    acc_g, val_g = host(sc.accept_flag).astype(bool), host(sc.valid_flag).astype(bool)
+    acc_o, val_o = ora["accept_flag"], ora["valid_flag"]
+    tied_pos = set()
+    for k in np.nonzero(acc_g != acc_o)[0]:
+        assert tie_acc[k], f"{label} accept flag mismatch at row {rows[k]}: margin {abs(LS[k, 0] - LS[k, 2])}"
+        tied_pos.add(k // (N * L))
+    for k in np.nonzero(val_g != val_o)[0]:
+        assert tie_cor[k] or acc_g[k] != acc_o[k], f"{label} valid flag mismatch at row {rows[k]}"
+        tied_pos.add(k // (N * L))
+    keep_rows = np.array([k // (N * L) not in tied_pos for k in range(npos * N * L)])
+    keep_pos = np.array([p not in tied_pos for p in range(npos)])
+    keep_paths = np.repeat(keep_pos, N)
+    # 3. row floats
+    la = sc.log_alpha.view(-1, 3).cpu().numpy()[rows]
+    lq = sc.log_q_tok.view(-1, 3).cpu().numpy()[rows]
+    checks = {
+        "lse_draft": (_log_ok, host(sc.lse_draft), ora["lse_q"], keep_rows),
+        "lse_target": (_log_ok, host(sc.lse_target), ora["lse_p"], keep_rows),
+        "log_alpha": (_log_ok, la, ora["log_alpha"], keep_rows[:, None]),
+        "log_q": (_log_ok, lq, ora["log_q"], keep_rows[:, None]),
+        "survival": (_lin_ok, host(sc.survival), ora["survival"], keep_rows),
+        "o_prime": (_lin_ok, host(sc.o_prime), ora["o_prime"], keep_rows),
+        "beta": (_lin_ok, host(sc.beta), ora["beta"], keep_rows),
+        "zeta": (_lin_ok, host(sc.zeta), ora["zeta"], keep_rows),
+        "coef_a": (_lin_ok, host(sc.coef_a), ora["coef_a"], keep_rows),
+        "coef_b": (_lin_ok, host(sc.coef_b), ora["coef_b"], keep_rows),
+    }
+    path_idx = (np.asarray(positions)[:, None] * N + np.arange(N)[None]).reshape(-1)
+    checks["exp_accept_len"] = (_lin_ok, sc.exp_accept_len.cpu().numpy()[path_idx], ora["exp_accept_len"], keep_paths)
+    checks["loss_pos"] = (_lin_ok, sc.loss_pos.cpu().numpy()[np.asarray(positions)], ora["loss_pos"], keep_pos)
+    worst = {}
+    for name, (fn, got, ref, keep) in checks.items():
+        ok = fn(got, ref)
+        ok = ok | ~np.broadcast_to(keep, ok.shape)
+        bad = np.argwhere(~ok)
+        assert bad.size == 0, f"{label} {name}: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {got[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
+        worst[name] = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    # 4. gradient
+    if check_grad and "grad" in ora:
+        g = gpu["grad"].index_select(0, torch.as_tensor(rows, device=gpu["grad"].device))[:, :cfg.v_draft]
+        g = g.float().cpu().numpy()
+        ref = ora["grad"]
+        err = np.abs(g - ref)
+        if gpu["grad"].dtype == torch.bfloat16:
+            ok = (err <= 2e-3) | ((np.abs(ref) >= 1.0) & (err <= _bf16_ulp(ref)))
+        else:
+            ok = err <= 2e-3
+        ok |= ~keep_rows[:, None]
+        bad = np.argwhere(~ok)
+        assert bad.size == 0, f"{label} grad: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {g[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
+        worst["grad"] = float(err[keep_rows].max()) if keep_rows.any() else 0.0
+    return dict(worst=worst, near_tie_positions=sorted(tied_pos))
+

@@ -1,0 +1,144 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/vsd.h declares, and host-side validation rejects invalid arguments
+with the documented status before anything is launched.
+
+Every call here fails validation, so no kernel is ever launched (pointer
+values are never dereferenced on the host).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_05774_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vsd.h")
+
+FAKE = 0x10000  # a 16-byte aligned stand-in address; never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libvsd.so not built (run __graft_entry__.build())")
+    return _lib.load()
+
+
+def test_every_declared_function_is_exported(lib):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\**\s+\**(vsd_[a-z_0-9]+)\s*\(", text, re.M))
+    assert {"vsd_sample_paths", "vsd_score_paths", "vsd_weighted_loss_bwd"} <= declared
+    assert declared == set(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert lib.vsd_abi_version() == 1
+    for code, name in _lib.STATUS_NAMES.items():
+        assert lib.vsd_status_string(code).decode() == name
+    assert lib.vsd_status_string(99).decode() == "VSD_ERR_UNKNOWN"
+
+
+def _dims(**kw):
+    d = dict(B=1, T=2, N=4, L=3, v_draft=1000, v_target=1000, dtype=_lib.VSD_F32, hidden_dim=0,
+             ld_draft=1000, ld_target=1000)
+    d.update(kw)
+    return _lib.VsdDims(**d)
+
+
+def _params(**kw):
+    p = dict(temp_draft=1.0, temp_target=1.0, w_base=1.05, car_tau=0.2, mode=2, car_input=0, loss_scale=1.0)
+    p.update(kw)
+    return _lib.VsdParams(**p)
+
+
+def _sample(lib, dims, X=FAKE, Y=FAKE, d2t=None, temps=(1.0, 1.0), toks=(FAKE, FAKE, FAKE), err=FAKE,
+            xsrc=None):
+    sx = xsrc if xsrc is not None else _lib.VsdSrc(X, None, None)
+    sy = _lib.VsdSrc(Y, None, None)
+    return lib.vsd_sample_paths(ctypes.byref(dims) if dims is not None else None, ctypes.byref(sx),
+                                ctypes.byref(sy), d2t, None, temps[0], temps[1], 0, 0, *toks, err, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), 2), (dict(T=0), 2), (dict(N=0), 2), (dict(N=1025), 2), (dict(L=0), 2), (dict(L=65), 2),
+    (dict(v_draft=0), 2), (dict(v_target=10), 2), (dict(dtype=7), 3),
+    (dict(ld_draft=999), 2), (dict(ld_draft=1001), 4), (dict(B=1 << 20, T=1 << 10), 2),
+])
+def test_sample_rejects_bad_dims(lib, kw, code):
+    assert _sample(lib, _dims(**kw)) == code
+    assert lib.vsd_last_error().decode() != ""
+
+
+def test_sample_rejects_nulls_misalignment_and_missing_map(lib):
+    assert _sample(lib, None) == 1
+    assert _sample(lib, _dims(), X=None) == 1
+    assert _sample(lib, _dims(), X=FAKE + 4) == 4
+    assert _sample(lib, _dims(), toks=(FAKE, None, FAKE)) == 1
+    assert _sample(lib, _dims(), err=None) == 1
+    assert _sample(lib, _dims(v_target=2000, ld_target=2000)) == 5
+    assert _sample(lib, _dims(v_target=2000, ld_target=2000), d2t=FAKE + 8) == 4
+    for bad in ((0.0, 1.0), (1.0, -1.0), (float("inf"), 1.0), (float("nan"), 1.0)):
+        assert _sample(lib, _dims(), temps=bad) == 3
+    fused = _lib.VsdSrc(None, FAKE, FAKE)
+    assert _sample(lib, _dims(), xsrc=fused) == 6
+
+
+def _score(lib, dims=None, params=None, out=None, ws=FAKE, ws_bytes=1 << 30, toks=(FAKE, FAKE, FAKE)):
+    dims = dims or _dims()
+    params = params or _params()
+    if out is None:
+        out = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    src = _lib.VsdSrc(FAKE, None, None)
+    return lib.vsd_score_paths(ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src), ctypes.byref(src),
+                               None, None, *toks, ctypes.byref(out), ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw", [dict(temp_draft=0.0), dict(temp_target=float("nan")), dict(w_base=0.0),
+                                dict(car_tau=-0.2), dict(mode=3), dict(car_input=2),
+                                dict(loss_scale=float("inf"))])
+def test_score_rejects_bad_params(lib, kw):
+    assert _score(lib, params=_params(**kw)) == 3
+
+
+def test_score_rejects_missing_required_outputs_and_small_workspace(lib):
+    assert _score(lib, out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=None, coef_b=FAKE, device_error=FAKE)) == 1
+    assert _score(lib, out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=None)) == 1
+    assert _score(lib, toks=(FAKE, FAKE, None)) == 1
+    need = ctypes.c_size_t()
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), ctypes.byref(need)) == 0
+    assert need.value >= 24 * 24  # [R,3] log alpha + [R,3] log q, R = 24
+    assert _score(lib, ws_bytes=need.value - 1) == 7
+    assert _score(lib, ws=None) == 7
+    assert _score(lib, ws=FAKE + 4, ws_bytes=need.value) == 4
+
+
+def test_bwd_rejects_bad_arguments(lib):
+    src = _lib.VsdSrc(FAKE, None, None)
+    g = _lib.VsdGrad(FAKE, None, None)
+    call = lambda dims, params, grad, err=FAKE, lse=FAKE: lib.vsd_weighted_loss_bwd(
+        ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src), lse, FAKE, FAKE, FAKE, FAKE,
+        ctypes.byref(grad), err, None)
+    assert call(_dims(L=0), _params(), g) == 2
+    assert call(_dims(), _params(temp_draft=0.0), g) == 3
+    assert call(_dims(), _params(), _lib.VsdGrad(None, None, None)) == 1
+    assert call(_dims(), _params(), _lib.VsdGrad(FAKE + 2, None, None)) == 4
+    assert call(_dims(), _params(), g, err=None) == 1
+    assert call(_dims(), _params(), g, lse=None) == 1
+
+
+def test_workspace_query_scales_with_rows(lib):
+    small, big = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), ctypes.byref(small)) == 0
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims(B=4)), ctypes.byref(big)) == 0
+    assert big.value > small.value
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), None) == 1
+
+
+def test_python_layer_raises_vsd_error_with_detail(lib):
+    with pytest.raises(_lib.VsdError) as ei:
+        _lib.check(_sample(lib, _dims(N=0)))
+    assert ei.value.status == 2 and "N=0" in ei.value.message
