@@ -21,12 +21,24 @@ namespace {
 
 constexpr int kRowsPerBlock = 4;
 
-// Online log2-sum-exp2 of row[v] * c over v < V, reduced over the wavefront.
-// m = running max of row*c, s = sum of exp2(row*c - m).  c > 0.
+// Online log-sum-exp of row[v] / T over v < V, reduced over the wavefront.
+//
+// With c = float(log2(e) / T), each lane keeps mraw (its largest raw logit),
+// mc = float(mraw * c) and s = sum_v exp2(fma(x_v, c, -mc)); the fused
+// multiply-add forms x_v * c exactly, so s is exactly consistent with mc.
+// Because float(mraw * c) differs from mraw * c by delta = fma(mraw, c, -mc)
+// (exactly representable), log2 sum_v 2^((x_v - mraw) c) = log2(s) - delta.
+// Callers then form log q(z) = (x_z - mraw)/T - ln2 (log2 s - delta), which
+// keeps full float32 precision even when |x/T| is in the hundreds (the
+// shifted difference never rounds against a large log-sum-exp).
+struct RowLse {
+  float mraw;  // wavefront max of the raw logits
+  float tail;  // ln sum_v exp((x_v - mraw)/T)  (>= 0)
+};
+
 template <typename T>
-__device__ __forceinline__ void row_lse2(const T* row, int V, float c, int lane, float& m, float& s) {
-  m = kNegBig;
-  s = 0.0f;
+__device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane) {
+  float mraw = kNegBig, mc = kNegBig, s = 0.0f;
   constexpr int U = 4;          // chunks in flight per lane
   constexpr int step = 8 * kWave;
   int base = lane * 8;
@@ -36,15 +48,16 @@ __device__ __forceinline__ void row_lse2(const T* row, int V, float c, int lane,
     for (int u = 0; u < U; ++u) load8(row + base + u * step, x[u]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      float cm = fmaxf(fmaxf(fmaxf(x[u][0], x[u][1]), fmaxf(x[u][2], x[u][3])),
-                       fmaxf(fmaxf(x[u][4], x[u][5]), fmaxf(x[u][6], x[u][7])));
-      cm *= c;
-      if (cm > m) {
-        s *= __builtin_amdgcn_exp2f(m - cm);
-        m = cm;
+      const float cm = fmaxf(fmaxf(fmaxf(x[u][0], x[u][1]), fmaxf(x[u][2], x[u][3])),
+                             fmaxf(fmaxf(x[u][4], x[u][5]), fmaxf(x[u][6], x[u][7])));
+      if (cm > mraw) {
+        const float nmc = cm * c;
+        s *= __builtin_amdgcn_exp2f(mc - nmc);
+        mc = nmc;
+        mraw = cm;
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[u][k], c, -m));
+      for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[u][k], c, -mc));
     }
   }
   for (; base + 8 <= V; base += step) {
@@ -53,25 +66,31 @@ __device__ __forceinline__ void row_lse2(const T* row, int V, float c, int lane,
     float cm = x[0];
 #pragma unroll
     for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
-    cm *= c;
-    if (cm > m) {
-      s *= __builtin_amdgcn_exp2f(m - cm);
-      m = cm;
+    if (cm > mraw) {
+      const float nmc = cm * c;
+      s *= __builtin_amdgcn_exp2f(mc - nmc);
+      mc = nmc;
+      mraw = cm;
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -m));
+    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -mc));
   }
   if (base < V) {  // the one partial chunk of the row
     for (int v = base; v < V; ++v) {
-      const float xv = load1(row + v) * c;
-      if (xv > m) {
-        s *= __builtin_amdgcn_exp2f(m - xv);
-        m = xv;
+      const float xv = load1(row + v);
+      if (xv > mraw) {
+        const float nmc = xv * c;
+        s *= __builtin_amdgcn_exp2f(mc - nmc);
+        mc = nmc;
+        mraw = xv;
       }
-      s += __builtin_amdgcn_exp2f(xv - m);
+      s += __builtin_amdgcn_exp2f(fmaf(xv, c, -mc));
     }
   }
-  wave_lse2(m, s);
+  wave_lse2(mc, s);            // every lane's mc = float(its mraw * c): the max commutes
+  mraw = wave_max(mraw);
+  const float delta = fmaf(mraw, c, -mc);
+  return RowLse{mraw, (log2f(s) - delta) * kLn2};
 }
 
 template <typename T, bool MAPPED>
@@ -102,11 +121,10 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   }
   const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
   const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
-  float mq, sq, mp, sp;
-  row_lse2(X, a.Vd, a.inv_tq * kLog2e, lane, mq, sq);
-  row_lse2(Y, a.Vt, a.inv_tp * kLog2e, lane, mp, sp);
-  const float lse_q = (mq + log2f(sq)) * kLn2;
-  const float lse_p = (mp + log2f(sp)) * kLn2;
+  const RowLse q = row_lse(X, a.Vd, a.inv_tq * kLog2e, lane);
+  const RowLse p = row_lse(Y, a.Vt, a.inv_tp * kLog2e, lane);
+  const float lse_q = q.mraw * a.inv_tq + q.tail;
+  const float lse_p = p.mraw * a.inv_tp + p.tail;
   if (lane < 3) {  // lane f gathers family f
     const int32_t z = a.tok[lane][r];
     float lq = 0.0f, la = 0.0f;
@@ -117,8 +135,8 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
       if ((uint32_t)zt >= (uint32_t)a.Vt) {
         report_error(a.err, VSD_DEVERR_MAP_RANGE);
       } else {
-        lq = load1(X + z) * a.inv_tq - lse_q;
-        const float lp = load1(Y + zt) * a.inv_tp - lse_p;
+        lq = (load1(X + z) - q.mraw) * a.inv_tq - q.tail;
+        const float lp = (load1(Y + zt) - p.mraw) * a.inv_tp - p.tail;
         la = fminf(0.0f, lp - lq);
       }
     }

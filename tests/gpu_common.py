@@ -24,6 +24,7 @@ from oracle import reference
 from synth.gen import rows_to_host
 
 TIE_REL = 1e-4
+SENTINEL = -7.0   # pre-filled into gradient buffers: padding columns must keep it
 
 
 def log(msg):
@@ -51,8 +52,9 @@ def run_step(cfg, inp, params=None, tokens=None):
     else:
         err_s = torch.zeros(1, dtype=torch.int32, device=inp["X"].device)
     sc = vsd.score_paths(prob, params, inp["X"], inp["Y"], *tokens, inp["d2t"], inp["valid_depth"])
-    grad = vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a,
-                                 sc.coef_b)
+    grad = torch.full_like(inp["X"], SENTINEL)
+    vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a, sc.coef_b,
+                          grad=grad)
     torch.cuda.synchronize()
     return dict(tokens=tokens, score=sc, grad=grad, err_sample=err_s)
 

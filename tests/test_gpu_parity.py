@@ -21,7 +21,7 @@ import torch
 import paper_2602_05774_amd as vsd
 from synth import CONFIGS, make_inputs, make_inputs_numpy_c1, scaled
 from synth.gen import PAD_VALUE
-from tests.gpu_common import compare, log, oracle_positions, params_of, problem_of, run_step
+from tests.gpu_common import SENTINEL, compare, log, oracle_positions, params_of, problem_of, run_step
 
 pytestmark = pytest.mark.gpu
 
@@ -58,7 +58,8 @@ def test_golden_examples(golden_dir, fixture):
                             w_base=g["params"]["w_base"], car_tau=g["params"]["car_tau"],
                             mode=modes[mode_name], car_input=exp.get("car_input", 0))
         sc = vsd.score_paths(prob, params, Xd, Yd, *toks, None, depth)
-        grad = vsd.weighted_loss_bwd(prob, params, Xd, sc.lse_draft, toks[0], toks[1], sc.coef_a, sc.coef_b)
+        grad = torch.full_like(Xd, SENTINEL)
+        vsd.weighted_loss_bwd(prob, params, Xd, sc.lse_draft, toks[0], toks[1], sc.coef_a, sc.coef_b, grad=grad)
         torch.cuda.synchronize()
         assert int(sc.device_error.item()) == 0
         R = N * L
@@ -75,7 +76,7 @@ def test_golden_examples(golden_dir, fixture):
         assert float(sc.loss_total.item()) == pytest.approx(exp["loss"], rel=2e-6)
         np.testing.assert_allclose(grad[:, :V].cpu().numpy(), np.asarray(exp["grad"]).reshape(R, V),
                                    rtol=2e-6, atol=1e-7, err_msg=f"{mode_name} grad")
-        assert np.all(grad[:, V:].cpu().numpy() == PAD_VALUE), "padding columns must not be written"
+        assert np.all(grad[:, V:].cpu().numpy() == SENTINEL), "padding columns must not be written"
 
 
 # ------------------------------------------------------------ oracle parity
@@ -226,7 +227,7 @@ def test_edge_cases(name):
     compare(cfg, gpu, rows, ora, list(range(cfg.P)), label=name)
     ld = inp["X"].shape[1]
     if ld > cfg.v_draft:
-        assert torch.all(gpu["grad"][:, cfg.v_draft:].float() == PAD_VALUE)
+        assert torch.all(gpu["grad"][:, cfg.v_draft:].float() == SENTINEL), "padding columns must not be written"
     if spec.get("same"):
         live = gpu["tokens"][0] >= 0
         assert torch.all(gpu["score"].accept_flag.bool()[live])
