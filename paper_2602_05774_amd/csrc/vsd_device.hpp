@@ -29,7 +29,13 @@ __device__ __forceinline__ void mulhilo32(uint32_t a, uint32_t b, uint32_t& hi, 
   lo = (uint32_t)p;
 }
 
-// Ten Philox4x32 rounds on counter (c0,c1,c2,c3) with key (k0,k1).
+// a ^ b ^ c in one gfx950 instruction (v_bitop3_b32, truth table 0x96).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+// Ten Philox4x32 rounds on counter (c0,c1,c2,c3) with key (k0,k1): per round
+// two 32x32->64 multiplies (v_mad_u64_u32) and two three-way XORs.
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                                uint32_t k0, uint32_t k1) {
 #pragma unroll
@@ -37,8 +43,8 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
     uint32_t hi0, lo0, hi1, lo1;
     mulhilo32(0xD2511F53u, c0, hi0, lo0);
     mulhilo32(0xCD9E8D57u, c2, hi1, lo1);
-    const uint32_t n0 = hi1 ^ c1 ^ k0;
-    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    const uint32_t n0 = xor3(hi1, c1, k0);
+    const uint32_t n2 = xor3(hi0, c3, k1);
     c0 = n0;
     c1 = lo1;
     c2 = n2;
