@@ -1,20 +1,28 @@
 // E-step sampling (Alg. 1 proposal z~ ~ q and correction z' ~ p; Alg. 2
 // greedy reference z-bar), one wavefront per row.
 //
-// Each lane walks its 8-element chunks of the row (128-bit loads) and draws
-// the Philox word of every element of both families.  The normative key
+// Each lane owns 8 consecutive vocabulary indices of every 512-element chunk
+// (128-bit loads; the Philox counters of S2 cover 4 consecutive indices) and
+// draws the Philox word of every element of both families.  The normative key
 // float(x/T) + G costs two logarithms with a correctly rounded division each,
 // so it is evaluated only for elements that can still win: with d = 1 - u
 // (exact on the 2^-24 grid), G = -ln(-ln(1 - d)) <= -ln(d) because
-// -ln(1 - d) >= d, and -ln(d) = (24 - log2(2^24 d)) ln 2 needs one hardware
-// log2 of an exact integer.  An element whose bound x/T + (-ln d) + margin is
+// -ln(1 - d) >= d, and -ln(d) <= (24 - log2 j') ln 2 for the integer
+// j' = (~w) >> 8 <= 2^24 d.  An element whose bound x/T - ln(d) + margin is
 // below the running maximum (the lane's own, or the wavefront's, refreshed
 // whenever a lane improves on it) cannot be the argmax; every other element
-// gets its exact key.  The margin covers the hardware log2 error, the error of
-// the normative log against the true one and the final rounding, so the
+// gets its exact key.  The margin exceeds every rounding involved, so the
 // tokens are exactly those of the definition.  Lanes visit indices in
 // increasing order and keep the first of equal keys; a butterfly reduction
 // with the same tie rule yields the row's tokens, independent of geometry.
+//
+// Mapped target logits are gathered in lane-strided order (gather k of a
+// chunk loads indices chunk + 64k + lane: a few consecutive cache lines per
+// instruction) and transposed to the lane-contiguous layout through a
+// per-wavefront LDS tile.  Full chunks are software pipelined: the next
+// chunk's map entries and draft row are loaded while the current chunk is
+// drawn, and its target gathers are issued at the end of the current chunk
+// and consumed after the next chunk's draft-family work.
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
 
@@ -23,11 +31,7 @@ namespace vsd {
 namespace {
 
 constexpr int kRowsPerBlock = 4;  // 256 threads = 4 wavefronts = 4 rows
-
-struct Best {
-  float key;
-  int idx;
-};
+constexpr int kChunk = 8 * kWave;  // elements per wavefront step
 
 template <typename T>
 __device__ __forceinline__ T neg_inf();
@@ -40,107 +44,93 @@ __device__ __forceinline__ uint32_t word_of(const uint4& p, int k) {
   return k == 0 ? p.x : k == 1 ? p.y : k == 2 ? p.z : p.w;
 }
 
-// One 512-element chunk of a row: gather, draw, bound, and the exact keys of
-// the candidates.  FULL chunks have every element in range and run without
-// per-element guards; the row's last partial chunk runs with them.
+// Raw 8-element slice of a row as loaded (bf16: one 128-bit load).
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  uint4 v;
+  __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void unpack(float (&o)[8]) const {
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x);
+    o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z);
+    o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void unpack(float (&o)[8]) const {
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+};
+
+struct Best {
+  float key;
+  int idx;
+};
+
 template <typename T, bool MAPPED>
-struct Chunk {
+struct RowSampler {
   const T* X;
   const T* Y;
   const int32_t* d2t;
-  T* tile;
+  T* tile;  // this wavefront's LDS tile, kChunk elements
   int Vd, Vt;
   float inv_tq, inv_tp;
+  float cq2, cp2;  // log2(e) / T of each family
   uint32_t row, offset, k0, k1;
   int lane;
-  float cq2, cp2;  // log2(e) / T of each family
+  Best bd{-INFINITY, 0x7FFFFFFF}, bt{-INFINITY, 0x7FFFFFFF}, bg{-INFINITY, 0x7FFFFFFF};
+  float wave_d = -INFINITY, wave_t = -INFINITY;  // wavefront maxima known so far
+  bool map_bad = false;
 
-  template <bool FULL>
-  __device__ __forceinline__ void run(int chunk, Best& bd, Best& bt, Best& bg, float& wave_d, float& wave_t,
-                                      bool& map_bad) const {
-    const int base = chunk + lane * 8;
-    float x[8], y[8];
-    uint32_t wd[8], wt[8];
-    if (MAPPED) {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int v = chunk + k * kWave + lane;
-        const bool in = FULL || v < Vd;
-        const uint32_t t = (uint32_t)d2t[in ? v : 0];
-        const bool ok = t < (uint32_t)Vt;
-        map_bad |= in && !ok;
-        const T val = Y[ok ? t : 0u];
-        tile[k * kWave + lane] = (in && ok) ? val : neg_inf<T>();
-      }
-    }
-    int nvalid = 8;
-    if (FULL) {
-      load8(X + base, x);
-      if (MAPPED)
-        load8(tile + lane * 8, y);
-      else
-        load8(Y + base, y);
-    } else {
-      nvalid = min(8, max(0, Vd - base));
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const bool in = k < nvalid;
-        x[k] = in ? load1(X + base + k) : -INFINITY;
-        y[k] = in ? (MAPPED ? load1(tile + lane * 8 + k) : load1(Y + base + k)) : -INFINITY;
-      }
-    }
-    // Philox words: counter (v >> 2, row, family, offset), word v & 3.  A
-    // chunk-aligned base is a multiple of 8, so the lane's 8 elements use the
-    // four words of counters base/4 and base/4 + 1.
-    const uint32_t c0 = (uint32_t)base >> 2;
-    const uint4 d0 = philox4x32_10(c0, row, 0u, offset, k0, k1);
-    const uint4 d1 = philox4x32_10(c0 + 1, row, 0u, offset, k0, k1);
-    const uint4 t0 = philox4x32_10(c0, row, 1u, offset, k0, k1);
-    const uint4 t1 = philox4x32_10(c0 + 1, row, 1u, offset, k0, k1);
+  __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t fam) const {
+    return philox4x32_10(c0, row, fam, offset, k0, k1);
+  }
+
+  // Bound test of the 4 elements that share one Philox counter: bit k set
+  // where x * log2e/T + off >= log2(j'), off = 24 - (thr - margin) log2e.
+  __device__ __forceinline__ static uint32_t cand4(const uint4& w, const float* v, float c2, float off) {
+    uint32_t m = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      wd[k] = word_of(d0, k);
-      wd[k + 4] = word_of(d1, k);
-      wt[k] = word_of(t0, k);
-      wt[k + 4] = word_of(t1, k);
+      const bool c = fmaf(v[k], c2, off) >= __builtin_amdgcn_logf((float)((~word_of(w, k)) >> 8));
+      m |= c ? (1u << k) : 0u;
     }
-    // greedy reference: raw target maximum, first index wins
+    return m;
+  }
+
+  // (thr - margin) log2e folded into the bound's constant.  The margin
+  // 2e-3 + 2e-6 |thr| exceeds every rounding involved for elements with
+  // |x/T| <= |thr| + 100; an element with x/T < thr - 100 cannot reach thr
+  // because G < 16.7.
+  __device__ __forceinline__ static float bound_offset(float thr) {
+    return 24.0f - (thr - (2e-3f + 2e-6f * fabsf(thr))) * kLog2e;
+  }
+
+  // Exact keys of the candidates (rare); their Philox words are recomputed.
+  __device__ __forceinline__ void exact(int base, const float (&x)[8], const float (&y)[8], uint32_t cd,
+                                        uint32_t ct) {
+    if (__ballot((cd | ct) != 0u) == 0ull) return;
+    const uint32_t c0 = (uint32_t)base >> 2;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      const bool better = (FULL || k < nvalid) && y[k] > bg.key;
-      bg.key = better ? y[k] : bg.key;
-      bg.idx = better ? base + k : bg.idx;
-    }
-    // Candidates: elements whose key bound reaches the running maximum thr.
-    // In log2 units the bound test reads  x * (log2e / T) + 24 - log2(j') >=
-    // (thr - margin) log2e  with j' = (~w) >> 8 <= 2^24 (1 - u) (j' = 0 gives
-    // an infinite bound).  The margin 2e-3 + 2e-6 |thr| exceeds every rounding
-    // involved for elements with |x/T| <= |thr| + 100, and an element with
-    // x/T < thr - 100 cannot reach thr because G < 16.7.
-    const float thr_d = fmaxf(bd.key, wave_d), thr_t = fmaxf(bt.key, wave_t);
-    const float od = 24.0f - (thr_d - (2e-3f + 2e-6f * fabsf(thr_d))) * kLog2e;
-    const float ot = 24.0f - (thr_t - (2e-3f + 2e-6f * fabsf(thr_t))) * kLog2e;
-    bool cd[8], ct[8];
-    bool any = false;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const bool in = FULL || k < nvalid;
-      cd[k] = in && fmaf(x[k], cq2, od) >= __builtin_amdgcn_logf((float)((~wd[k]) >> 8));
-      ct[k] = in && fmaf(y[k], cp2, ot) >= __builtin_amdgcn_logf((float)((~wt[k]) >> 8));
-      any |= cd[k] | ct[k];
-    }
-    if (__ballot(any) == 0ull) return;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      if (cd[k]) {
-        const float kd = gumbel_key(x[k], inv_tq, wd[k]);
+      if (cd & (1u << k)) {
+        const float kd = gumbel_key(x[k], inv_tq, word_of(philox(c0 + (k >> 2), 0u), k & 3));
         if (kd > bd.key) {
           bd.key = kd;
           bd.idx = base + k;
         }
       }
-      if (ct[k]) {
-        const float kt = gumbel_key(y[k], inv_tp, wt[k]);
+      if (ct & (1u << k)) {
+        const float kt = gumbel_key(y[k], inv_tp, word_of(philox(c0 + (k >> 2), 1u), k & 3));
         if (kt > bt.key) {
           bt.key = kt;
           bt.idx = base + k;
@@ -152,10 +142,133 @@ struct Chunk {
       wave_t = wave_max(bt.key);
     }
   }
+
+  __device__ __forceinline__ void greedy(int base, const float (&y)[8], int nvalid) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const bool better = k < nvalid && y[k] > bg.key;
+      bg.key = better ? y[k] : bg.key;
+      bg.idx = better ? base + k : bg.idx;
+    }
+  }
+
+  // Map entries of a full chunk in lane-strided order.
+  __device__ __forceinline__ void load_map(int chunk, uint32_t (&t)[8]) const {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t[k] = (uint32_t)d2t[chunk + k * kWave + lane];
+  }
+
+  // Gathers of the mapped target logits; an out-of-range map entry reads
+  // element 0 instead and is flagged in `bad`.
+  __device__ __forceinline__ void gather(const uint32_t (&t)[8], T (&g)[8], uint32_t& bad) const {
+    bad = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const bool ok = t[k] < (uint32_t)Vt;
+      bad |= ok ? 0u : (1u << k);
+      g[k] = Y[ok ? t[k] : 0u];
+    }
+  }
+
+  // Transpose gathered values through the LDS tile into this lane's 8
+  // lane-contiguous target logits (flagged entries become -inf).  LDS
+  // operations of one wavefront execute in order: no barrier is needed.
+  __device__ __forceinline__ void transpose(const T (&g)[8], uint32_t bad, float (&y)[8]) {
+    map_bad |= bad != 0u;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) tile[k * kWave + lane] = (bad & (1u << k)) ? neg_inf<T>() : g[k];
+    load8(tile + lane * 8, y);
+  }
+
+  // Every chunk of the row whose 512 elements are all in range.
+  __device__ void full_chunks(int nfull) {
+    if (nfull == 0) return;
+    uint32_t t[8];
+    T g[8];
+    uint32_t bad = 0;
+    Raw8<T> xr, yr;
+    if (MAPPED) {
+      load_map(0, t);
+      gather(t, g, bad);
+    } else {
+      yr.load(Y + lane * 8);
+    }
+    xr.load(X + lane * 8);
+    for (int it = 0; it < nfull; ++it) {
+      const int chunk = it * kChunk;
+      const int base = chunk + lane * 8;
+      const bool next = it + 1 < nfull;
+      uint32_t tn[8];
+      Raw8<T> xn, yn;
+      if (next) {  // prefetch the next chunk's map entries and rows
+        if (MAPPED)
+          load_map(chunk + kChunk, tn);
+        else
+          yn.load(Y + base + kChunk);
+        xn.load(X + base + kChunk);
+      }
+      const uint32_t c0 = (uint32_t)base >> 2;
+      // draft family first: it does not wait for this chunk's gathers
+      float x[8];
+      xr.unpack(x);
+      const float od = bound_offset(fmaxf(bd.key, wave_d));
+      const uint32_t cd = cand4(philox(c0, 0u), x, cq2, od) | (cand4(philox(c0 + 1, 0u), x + 4, cq2, od) << 4);
+      float y[8];
+      if (MAPPED)
+        transpose(g, bad, y);
+      else
+        yr.unpack(y);
+      greedy(base, y, 8);
+      const float ot = bound_offset(fmaxf(bt.key, wave_t));
+      const uint32_t ct = cand4(philox(c0, 1u), y, cp2, ot) | (cand4(philox(c0 + 1, 1u), y + 4, cp2, ot) << 4);
+      exact(base, x, y, cd, ct);
+      if (next) {
+        if (MAPPED)
+          gather(tn, g, bad);
+        else
+          yr = yn;
+        xr = xn;
+      }
+    }
+  }
+
+  // The row's last, partial chunk (guarded element by element).
+  __device__ void tail_chunk(int chunk) {
+    const int base = chunk + lane * 8;
+    const int nvalid = min(8, max(0, Vd - base));
+    if (MAPPED) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int v = chunk + k * kWave + lane;
+        const bool in = v < Vd;
+        const uint32_t t = (uint32_t)d2t[in ? v : 0];
+        const bool ok = t < (uint32_t)Vt;
+        map_bad |= in && !ok;
+        const T val = Y[ok ? t : 0u];
+        tile[k * kWave + lane] = (in && ok) ? val : neg_inf<T>();
+      }
+    }
+    float x[8], y[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const bool in = k < nvalid;
+      x[k] = in ? load1(X + base + k) : -INFINITY;
+      y[k] = in ? (MAPPED ? load1(tile + lane * 8 + k) : load1(Y + base + k)) : -INFINITY;
+    }
+    greedy(base, y, nvalid);
+    const uint32_t c0 = (uint32_t)base >> 2;
+    const uint32_t valid = (1u << nvalid) - 1u;
+    const float od = bound_offset(fmaxf(bd.key, wave_d));
+    const float ot = bound_offset(fmaxf(bt.key, wave_t));
+    const uint32_t cd = (cand4(philox(c0, 0u), x, cq2, od) | (cand4(philox(c0 + 1, 0u), x + 4, cq2, od) << 4)) & valid;
+    const uint32_t ct = (cand4(philox(c0, 1u), y, cp2, ot) | (cand4(philox(c0 + 1, 1u), y + 4, cp2, ot) << 4)) & valid;
+    exact(base, x, y, cd, ct);
+  }
 };
 
 template <typename T, bool MAPPED>
 __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
+  __shared__ __align__(16) T ytile[kRowsPerBlock][kChunk];
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (r >= a.R) return;
@@ -177,36 +290,32 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     }
     return;
   }
-  const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
-  const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
-  const uint32_t row = (uint32_t)r;
-
-  Best bd{-INFINITY, 0x7FFFFFFF}, bt{-INFINITY, 0x7FFFFFFF}, bg{-INFINITY, 0x7FFFFFFF};
-  float wave_d = -INFINITY, wave_t = -INFINITY;  // wavefront maxima known so far
-  bool map_bad = false;
-
-  // Per-wavefront LDS tile: the mapped target logits of one 512-element chunk.
-  // Gathers run in lane-strided order (instruction k loads draft indices
-  // chunk + 64k + lane, which hit a few consecutive cache lines) and the tile
-  // is read back in lane-contiguous order (lane j owns chunk + 8j .. +7, the
-  // layout the Philox counters want).  LDS operations of one wavefront execute
-  // in order, so no barrier is needed between its writes and reads.
-  __shared__ __align__(16) T ytile[kRowsPerBlock][8 * kWave];
-  T* tile = ytile[threadIdx.x >> 6];
-
-  Chunk<T, MAPPED> c{X,     Y,        a.d2t, tile, a.Vd, a.Vt, a.inv_tq, a.inv_tp, row, a.offset, a.k0, a.k1,
-                     lane,  a.inv_tq * kLog2e, a.inv_tp * kLog2e};
-  int chunk = 0;
-  for (; chunk + 8 * kWave <= a.Vd; chunk += 8 * kWave) c.template run<true>(chunk, bd, bt, bg, wave_d, wave_t, map_bad);
-  if (chunk < a.Vd) c.template run<false>(chunk, bd, bt, bg, wave_d, wave_t, map_bad);
-  if (map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
-  wave_argmax(bd.key, bd.idx);
-  wave_argmax(bt.key, bt.idx);
-  wave_argmax(bg.key, bg.idx);
+  RowSampler<T, MAPPED> s{static_cast<const T*>(a.X) + r * a.ld_d,
+                          static_cast<const T*>(a.Y) + r * a.ld_t,
+                          a.d2t,
+                          ytile[threadIdx.x >> 6],
+                          a.Vd,
+                          a.Vt,
+                          a.inv_tq,
+                          a.inv_tp,
+                          a.inv_tq * kLog2e,
+                          a.inv_tp * kLog2e,
+                          (uint32_t)r,
+                          a.offset,
+                          a.k0,
+                          a.k1,
+                          lane};
+  const int nfull = a.Vd / kChunk;
+  s.full_chunks(nfull);
+  if (nfull * kChunk < a.Vd) s.tail_chunk(nfull * kChunk);
+  if (s.map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
+  wave_argmax(s.bd.key, s.bd.idx);
+  wave_argmax(s.bt.key, s.bt.idx);
+  wave_argmax(s.bg.key, s.bg.idx);
   if (lane == 0) {
-    a.tok_d[r] = bd.idx;
-    a.tok_t[r] = bt.idx;
-    a.tok_g[r] = bg.idx;
+    a.tok_d[r] = s.bd.idx;
+    a.tok_t[r] = s.bt.idx;
+    a.tok_g[r] = s.bg.idx;
   }
 }
 
