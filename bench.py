@@ -5,15 +5,19 @@
 Workload (default): the LLaMA-3-8B / EAGLE-3-shaped batch, B=4 T=512 N=8 L=6,
 target vocabulary 128256, draft vocabulary 32000 with a draft->target map,
 bf16 logits already resident in HBM, synthetic and seeded.  One step = every
-row of the batch through vsd_sample_paths, vsd_score_paths and
-vsd_weighted_loss_bwd on one stream.  W untimed steps, then exactly K steps
-timed between stream synchronisations; per-call durations come from HIP
-events recorded on the stream the kernels run on.
+row of the batch through vsd_sample_score_paths (E-step draws and path
+scoring in one pass over the logits) and vsd_weighted_loss_bwd on one stream.
+The same step through the three separate calls (vsd_sample_paths,
+vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it.
+W untimed steps, then exactly K steps timed between stream synchronisations;
+per-call durations come from HIP events recorded on the stream the kernels
+run on.
 
 Prints one JSON line: value = path-tokens (live rows) per second of whole
-steps; roofline = the dominant kernel against its bound; cpu_baseline = the
-CPU oracle timed on a bounded sample of the same workload (computed before the
-GPU is touched, in worker processes).
+steps; roofline = the dominant kernel against its bound (algorithmic bytes:
+each live row's draft and target logits read once); cpu_baseline = the CPU
+oracle timed on a bounded sample of the same workload (computed before the GPU
+is touched, in worker processes).
 """
 import argparse
 import json
@@ -26,9 +30,6 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
-# Plain (non-packed) fp32 VALU lane-operations per second:
-# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
-VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 
 METRIC = "path-tokens scored/sec (fwd+bwd) and achieved HBM GB/s at V=128256"
 
@@ -119,7 +120,23 @@ def main():
     grad = torch.empty_like(X)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
 
-    def step(ev=None):
+    tok = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+
+    def step_fused(ev=None):
+        """One EM step: one-pass sample + score, then the backward."""
+        if ev:
+            ev[0].record()
+        vsd.sample_score_paths(prob, params, X, Y, d2t, depth, cfg.philox_seed, cfg.philox_offset, out=out,
+                               workspace=ws, tokens=tok)
+        if ev:
+            ev[1].record()
+        vsd.weighted_loss_bwd(prob, params, X, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=grad,
+                              device_error=err)
+        if ev:
+            ev[2].record()
+
+    def step_three_calls(ev=None):
+        """The same step through the three separate calls."""
         if ev:
             ev[0].record()
         s = vsd.sample_paths(prob, X, Y, d2t, depth, cfg.temp_draft, cfg.temp_target, cfg.philox_seed,
@@ -134,52 +151,47 @@ def main():
                               grad=grad, device_error=err)
         if ev:
             ev[3].record()
-        return s
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        s = step(evs[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
+    def timed(fn, nev):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            fn(evs[k])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        seg = [sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j in range(nev - 1)]
+        total = sum(e[0].elapsed_time(e[nev - 1]) for e in evs) / args.steps
+        return seg, total, wall
+
+    (t_sample3, t_score3, t_bwd3), t_step3, _ = timed(step_three_calls, 4)
+    (t_ss, t_bwd), t_step, wall = timed(step_fused, 3)
     if int(err.item()) != 0 or int(out.device_error.item()) != 0:
         raise RuntimeError("device error reported during the benchmark")
-    t_sample = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-    t_score = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-    t_bwd = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
-    t_step = sum(e[0].elapsed_time(e[3]) for e in evs) / args.steps
 
-    live = prob.R if depth is None else int((s.tok_draft >= 0).sum().item())
+    live = prob.R if depth is None else int((tok[0] >= 0).sum().item())
     nonzero = int(((out.coef_a != 0) | (out.coef_b != 0)).sum().item())
     es = X.element_size()
-    # algorithmic bytes per launch
-    score_bytes = live * es * (cfg.v_draft + cfg.v_target)
+    # algorithmic bytes per launch: every live row's draft and target logits
+    # once (sample + score), the backward's read of rows with a or b != 0 and
+    # its write of every row
+    ss_bytes = live * es * (cfg.v_draft + cfg.v_target)
     bwd_bytes = nonzero * es * cfg.v_draft + prob.R * es * cfg.v_draft
-    sample_keys = live * 2 * cfg.v_draft
     gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
     kernels = {
-        "sample": {"ms": t_sample, "keys_per_s": sample_keys / (t_sample * 1e-3)},
-        "score": {"ms": t_score, "bytes": score_bytes, "GB/s": gbs(score_bytes, t_score)},
+        "sample_score": {"ms": t_ss, "bytes": ss_bytes, "GB/s": gbs(ss_bytes, t_ss)},
         "bwd": {"ms": t_bwd, "bytes": bwd_bytes, "GB/s": gbs(bwd_bytes, t_bwd)},
     }
-    sb_ms = t_score + t_bwd
-    score_bwd = {"ms": sb_ms, "bytes": score_bytes + bwd_bytes, "GB/s": gbs(score_bytes + bwd_bytes, sb_ms),
-                 "frac_of_hbm_peak": gbs(score_bytes + bwd_bytes, sb_ms) / HBM_PEAK_GBS,
-                 "path_tokens_per_s": live / (sb_ms * 1e-3)}
-    dominant = max(("sample", t_sample), ("score", t_score), ("bwd", t_bwd), key=lambda kv: kv[1])[0]
-    if dominant == "sample":
-        roof = {"bound": "alu", "kernel": "k_sample", "achieved": None, "peak": VALU_PEAK_GOPS,
-                "unit": "Gop/s", "frac": None, "traffic": None,
-                "note": "VALU-bound sampler; achieved op rate is taken from rocprofv3 SQ_INSTS_VALU"}
-    else:
-        k = kernels[dominant]
-        roof = {"bound": "hbm", "kernel": "k_score_rows" if dominant == "score" else "k_bwd",
-                "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": k["GB/s"] / HBM_PEAK_GBS,
-                "traffic": None}
+    three_calls = {"ms_per_step": t_step3, "sample_ms": t_sample3, "score_ms": t_score3, "bwd_ms": t_bwd3,
+                   "score_GB/s": gbs(ss_bytes, t_score3),
+                   "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score3 + t_bwd3) / HBM_PEAK_GBS}
+    dominant = "sample_score" if t_ss >= t_bwd else "bwd"
+    k = kernels[dominant]
+    roof = {"bound": "hbm", "kernel": "k_sample<bf16,mapped,fused>" if dominant == "sample_score" else "k_bwd",
+            "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": k["GB/s"] / HBM_PEAK_GBS,
+            "traffic": None}
     line = {
         "metric": METRIC, "value": live / (t_step * 1e-3), "unit": "path-tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step, "wall_ms_per_step": wall * 1e3 / args.steps,
@@ -188,7 +200,7 @@ def main():
         "config": {"workload": f"{cfg.name}: B={cfg.B} T={cfg.T} N={cfg.N} L={cfg.L} "
                                f"V_target={cfg.v_target} V_draft={cfg.v_draft} logits={cfg.dtype}",
                    "path_tokens_per_step": live, "parallelism": "single GPU"},
-        "kernels": kernels, "score_bwd": score_bwd, "roofline": roof, "cpu_baseline": base,
+        "kernels": kernels, "three_calls": three_calls, "roofline": roof, "cpu_baseline": base,
     }
     print(json.dumps(line), flush=True)
 

@@ -251,6 +251,22 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params,
                            void* workspace, size_t workspace_bytes,
                            void* hip_stream);
 
+/* vsd_sample_paths followed by vsd_score_paths on the drawn tokens, in one
+ * pass over the logits: the sampling kernel also accumulates both
+ * log-sum-exps and gathers the drawn tokens' logits, so X and Y are read from
+ * memory once instead of twice.  Temperatures come from `params`.  Tokens are
+ * identical to vsd_sample_paths'; the float outputs agree with
+ * vsd_score_paths' up to float32 summation order.  Same workspace as
+ * vsd_score_paths. */
+vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params,
+                                  const vsd_src* draft, const vsd_src* target,
+                                  const int32_t* d2t, const int32_t* valid_depth,
+                                  uint64_t seed, uint32_t offset,
+                                  int32_t* tok_draft, int32_t* tok_target,
+                                  int32_t* tok_greedy, const vsd_score_out* out,
+                                  void* workspace, size_t workspace_bytes,
+                                  void* hip_stream);
+
 /* Gradient of loss_scale * sum_x L_x with respect to the draft logits (the
  * derivative of Eq. advance, with o', beta, zeta and the tokens held fixed):
  *   g[r][v] = loss_scale / T_q * ((a+b) q_r(v) - a [v = z~] - b [v = z'])

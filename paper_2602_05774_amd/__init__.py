@@ -9,8 +9,8 @@ torch binding (vsd.py).
 """
 from .vsd import (VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR, VSD_GRAD_BASIC, Params,
                   Problem, SampleResult, ScoreResult, VsdError, alloc_score_outputs, sample_paths,
-                  score_paths, score_workspace_bytes, weighted_loss_bwd)
+                  sample_score_paths, score_paths, score_workspace_bytes, weighted_loss_bwd)
 
 __all__ = ["Params", "Problem", "SampleResult", "ScoreResult", "VsdError", "alloc_score_outputs",
-           "sample_paths", "score_paths", "score_workspace_bytes", "weighted_loss_bwd",
+           "sample_paths", "sample_score_paths", "score_paths", "score_workspace_bytes", "weighted_loss_bwd",
            "VSD_GRAD_BASIC", "VSD_GRAD_ARW", "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]

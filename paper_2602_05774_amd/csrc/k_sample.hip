@@ -76,7 +76,38 @@ struct Best {
   int idx;
 };
 
-template <typename T, bool MAPPED>
+// Per-lane online log-sum-exp of v/T in the exactly consistent form of the
+// scorer: mraw = largest raw value, mc = float(mraw * c), s = sum of
+// exp2(fma(v, c, -mc)), c = log2(e)/T.  Elements equal to -inf add nothing.
+struct LaneLse {
+  float mraw = kNegBig, mc = kNegBig, s = 0.0f;
+
+  template <int K>
+  __device__ __forceinline__ void add(const float* v, float c) {
+    float cm = v[0];
+#pragma unroll
+    for (int k = 1; k < K; ++k) cm = fmaxf(cm, v[k]);
+    if (cm > mraw) {
+      const float nmc = cm * c;
+      s *= __builtin_amdgcn_exp2f(mc - nmc);
+      mc = nmc;
+      mraw = cm;
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) s += __builtin_amdgcn_exp2f(fmaf(v[k], c, -mc));
+  }
+
+  // Wavefront reduction; returns (max raw value, ln sum exp((v - max)/T)).
+  __device__ __forceinline__ void finish(float c, float& m_out, float& tail_out) {
+    float m = mc, t = s;
+    wave_lse2(m, t);
+    const float mr = wave_max(mraw);
+    m_out = mr;
+    tail_out = (log2f(t) - fmaf(mr, c, -m)) * kLn2;
+  }
+};
+
+template <typename T, bool MAPPED, bool FUSED>
 struct RowSampler {
   const T* X;
   const T* Y;
@@ -87,9 +118,27 @@ struct RowSampler {
   float cq2, cp2;  // log2(e) / T of each family
   uint32_t row, offset, k0, k1;
   int lane;
+  int tblock;      // FUSED && MAPPED: target elements streamed per chunk
   Best bd{-INFINITY, 0x7FFFFFFF}, bt{-INFINITY, 0x7FFFFFFF}, bg{-INFINITY, 0x7FFFFFFF};
   float wave_d = -INFINITY, wave_t = -INFINITY;  // wavefront maxima known so far
   bool map_bad = false;
+  LaneLse lq, lp;  // FUSED: draft and target log-sum-exp accumulators
+
+  // FUSED && MAPPED: log-sum-exp of the target elements [lo, hi) of the row
+  // (the target row is streamed in lock-step with the draft chunks, so the
+  // mapped gathers of the same chunk find its cache lines in L2).
+  __device__ __forceinline__ void stream_target(int lo, int hi) {
+    for (int g = lo + lane * 8; g - lane * 8 < hi; g += kChunk) {
+      float v[8];
+      if (g + 8 <= hi) {
+        load8(Y + g, v);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = (g + k < hi) ? load1(Y + g + k) : -INFINITY;
+      }
+      lp.template add<8>(v, cp2);
+    }
+  }
 
   __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t fam) const {
     return philox4x32_10(c0, row, fam, offset, k0, k1);
@@ -211,6 +260,7 @@ struct RowSampler {
       // draft family first: it does not wait for this chunk's gathers
       float x[8];
       xr.unpack(x);
+      if (FUSED) lq.template add<8>(x, cq2);
       const float od = bound_offset(fmaxf(bd.key, wave_d));
       const uint32_t cd = cand4(philox(c0, 0u), x, cq2, od) | (cand4(philox(c0 + 1, 0u), x + 4, cq2, od) << 4);
       float y[8];
@@ -218,6 +268,8 @@ struct RowSampler {
         transpose(g, bad, y);
       else
         yr.unpack(y);
+      if (FUSED && !MAPPED) lp.template add<8>(y, cp2);
+      if (FUSED && MAPPED) stream_target(it * tblock, min(Vt, (it + 1) * tblock));
       greedy(base, y, 8);
       const float ot = bound_offset(fmaxf(bt.key, wave_t));
       const uint32_t ct = cand4(philox(c0, 1u), y, cp2, ot) | (cand4(philox(c0 + 1, 1u), y + 4, cp2, ot) << 4);
@@ -234,6 +286,7 @@ struct RowSampler {
 
   // The row's last, partial chunk (guarded element by element).
   __device__ void tail_chunk(int chunk) {
+    if (FUSED && MAPPED) stream_target((chunk / kChunk) * tblock, min(Vt, (chunk / kChunk + 1) * tblock));
     const int base = chunk + lane * 8;
     const int nvalid = min(8, max(0, Vd - base));
     if (MAPPED) {
@@ -255,6 +308,10 @@ struct RowSampler {
       x[k] = in ? load1(X + base + k) : -INFINITY;
       y[k] = in ? (MAPPED ? load1(tile + lane * 8 + k) : load1(Y + base + k)) : -INFINITY;
     }
+    if (FUSED) {
+      lq.template add<8>(x, cq2);
+      if (!MAPPED) lp.template add<8>(y, cp2);
+    }
     greedy(base, y, nvalid);
     const uint32_t c0 = (uint32_t)base >> 2;
     const uint32_t valid = (1u << nvalid) - 1u;
@@ -266,7 +323,7 @@ struct RowSampler {
   }
 };
 
-template <typename T, bool MAPPED>
+template <typename T, bool MAPPED, bool FUSED>
 __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   __shared__ __align__(16) T ytile[kRowsPerBlock][kChunk];
   const int lane = threadIdx.x & (kWave - 1);
@@ -282,36 +339,78 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
       d = 0;
     }
   }
-  if (i >= d) {
+  if (i >= d) {  // masked slot: tokens -1, score outputs 0, nothing read
     if (lane == 0) {
       a.tok_d[r] = -1;
       a.tok_t[r] = -1;
       a.tok_g[r] = -1;
     }
+    if (FUSED) {
+      if (lane < 3) {
+        a.la[r * 3 + lane] = 0.0f;
+        a.lq[r * 3 + lane] = 0.0f;
+      }
+      if (lane == 0) {
+        a.lse_q[r] = 0.0f;
+        if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
+      }
+    }
     return;
   }
-  RowSampler<T, MAPPED> s{static_cast<const T*>(a.X) + r * a.ld_d,
-                          static_cast<const T*>(a.Y) + r * a.ld_t,
-                          a.d2t,
-                          ytile[threadIdx.x >> 6],
-                          a.Vd,
-                          a.Vt,
-                          a.inv_tq,
-                          a.inv_tp,
-                          a.inv_tq * kLog2e,
-                          a.inv_tp * kLog2e,
-                          (uint32_t)r,
-                          a.offset,
-                          a.k0,
-                          a.k1,
-                          lane};
+  const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
+  const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
+  RowSampler<T, MAPPED, FUSED> s{X,
+                                 Y,
+                                 a.d2t,
+                                 ytile[threadIdx.x >> 6],
+                                 a.Vd,
+                                 a.Vt,
+                                 a.inv_tq,
+                                 a.inv_tp,
+                                 a.inv_tq * kLog2e,
+                                 a.inv_tp * kLog2e,
+                                 (uint32_t)r,
+                                 a.offset,
+                                 a.k0,
+                                 a.k1,
+                                 lane,
+                                 a.tblock};
   const int nfull = a.Vd / kChunk;
   s.full_chunks(nfull);
   if (nfull * kChunk < a.Vd) s.tail_chunk(nfull * kChunk);
+  if (FUSED && MAPPED) {  // target elements past the last chunk's block (none when tblock covers the row)
+    const int nchunks = (a.Vd + kChunk - 1) / kChunk;
+    s.stream_target(min(a.Vt, nchunks * a.tblock), a.Vt);
+  }
   if (s.map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
   wave_argmax(s.bd.key, s.bd.idx);
   wave_argmax(s.bt.key, s.bt.idx);
   wave_argmax(s.bg.key, s.bg.idx);
+  if (FUSED) {
+    // Row statistics of the scorer, in its exactly consistent shifted form,
+    // and log q / log alpha of the three drawn tokens.
+    float mq, tq, mp, tp;
+    s.lq.finish(s.cq2, mq, tq);
+    s.lp.finish(s.cp2, mp, tp);
+    if (lane < 3) {
+      const int z = lane == 0 ? s.bd.idx : lane == 1 ? s.bt.idx : s.bg.idx;
+      float lqv = 0.0f, lav = 0.0f;
+      if ((uint32_t)z < (uint32_t)a.Vd) {
+        const int32_t zt = MAPPED ? a.d2t[z] : z;
+        if ((uint32_t)zt < (uint32_t)a.Vt) {
+          lqv = (load1(X + z) - mq) * a.inv_tq - tq;
+          const float lp = (load1(Y + zt) - mp) * a.inv_tp - tp;
+          lav = fminf(0.0f, lp - lqv);
+        }
+      }
+      a.la[r * 3 + lane] = lav;
+      a.lq[r * 3 + lane] = lqv;
+    }
+    if (lane == 0) {
+      a.lse_q[r] = mq * a.inv_tq + tq;
+      if (a.lse_p != nullptr) a.lse_p[r] = mp * a.inv_tp + tp;
+    }
+  }
   if (lane == 0) {
     a.tok_d[r] = s.bd.idx;
     a.tok_t[r] = s.bt.idx;
@@ -319,20 +418,22 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   }
 }
 
-template <typename T>
+template <typename T, bool FUSED>
 hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
   if (a.d2t != nullptr)
-    hipLaunchKernelGGL((k_sample<T, true>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_sample<T, true, FUSED>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_sample<T, false>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_sample<T, false, FUSED>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s) {
-  return bf16 ? launch_t<bf16_t>(a, s) : launch_t<float>(a, s);
+  const bool fused = a.lse_q != nullptr;
+  if (bf16) return fused ? launch_t<bf16_t, true>(a, s) : launch_t<bf16_t, false>(a, s);
+  return fused ? launch_t<float, true>(a, s) : launch_t<float, false>(a, s);
 }
 
 }  // namespace vsd

@@ -108,6 +108,57 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   return w;
 }
 
+// Validation of the score outputs and workspace shared by the scoring calls.
+vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const void* workspace,
+                           size_t workspace_bytes) {
+  if (out == nullptr) return fail(VSD_ERR_NULL_POINTER, "out is NULL");
+  if (out->lse_draft == nullptr || out->coef_a == nullptr || out->coef_b == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "out->lse_draft, coef_a and coef_b are required");
+  if (out->device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "out->device_error is NULL");
+  const WorkspaceLayout wl = workspace_layout(dims);
+  if (workspace == nullptr || workspace_bytes < wl.total)
+    return fail(VSD_ERR_WORKSPACE, "workspace of %zu bytes required, %zu given", wl.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned16(workspace)) return fail(VSD_ERR_MISALIGNED, "workspace not 16-byte aligned");
+  return VSD_OK;
+}
+
+// The per-position combine (and the loss total) over row statistics already
+// in la / lq.
+vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* params, const int32_t* valid_depth,
+                                    const vsd_score_out* out, const float* la, const float* lq, float* loss_pos,
+                                    hipStream_t s) {
+  vsd::CombineArgs ca{};
+  ca.la = la;
+  ca.lq = lq;
+  ca.depth = valid_depth;
+  ca.survival = out->survival;
+  ca.ea = out->exp_accept_len;
+  ca.acc_flag = out->accept_flag;
+  ca.val_flag = out->valid_flag;
+  ca.o_prime = out->o_prime;
+  ca.beta = out->beta;
+  ca.zeta = out->zeta;
+  ca.coef_a = out->coef_a;
+  ca.coef_b = out->coef_b;
+  ca.loss_pos = loss_pos;
+  ca.err = out->device_error;
+  ca.P = dims->B * dims->T;
+  ca.N = dims->N;
+  ca.L = dims->L;
+  ca.mode = params->mode;
+  ca.car_input = params->car_input;
+  ca.inv_tau = 1.0f / params->car_tau;
+  for (int l = 0; l < dims->L; ++l) ca.w[l] = (float)std::pow((double)params->w_base, (double)(l + 1));
+  hipError_t e = vsd::launch_combine(ca, s);
+  if (e != hipSuccess) return hip_fail(e, "k_combine launch");
+  if (out->loss_total != nullptr) {
+    e = vsd::launch_loss_total(loss_pos, ca.P, params->loss_scale, out->loss_total, s);
+    if (e != hipSuccess) return hip_fail(e, "k_loss_total launch");
+  }
+  return VSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -193,15 +244,8 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   if ((st = check_map(dims, d2t)) != VSD_OK) return st;
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
-  if (out == nullptr) return fail(VSD_ERR_NULL_POINTER, "out is NULL");
-  if (out->lse_draft == nullptr || out->coef_a == nullptr || out->coef_b == nullptr)
-    return fail(VSD_ERR_NULL_POINTER, "out->lse_draft, coef_a and coef_b are required");
-  if (out->device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "out->device_error is NULL");
+  if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
   const WorkspaceLayout wl = workspace_layout(dims);
-  if (workspace == nullptr || workspace_bytes < wl.total)
-    return fail(VSD_ERR_WORKSPACE, "workspace of %zu bytes required, %zu given", wl.total,
-                workspace == nullptr ? (size_t)0 : workspace_bytes);
-  if (!aligned16(workspace)) return fail(VSD_ERR_MISALIGNED, "workspace not 16-byte aligned");
 
   char* ws = static_cast<char*>(workspace);
   float* la = out->log_alpha != nullptr ? out->log_alpha : reinterpret_cast<float*>(ws + wl.la);
@@ -233,34 +277,66 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   hipError_t e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
   if (e != hipSuccess) return hip_fail(e, "k_score_rows launch");
 
-  vsd::CombineArgs ca{};
-  ca.la = la;
-  ca.lq = lq;
-  ca.depth = valid_depth;
-  ca.survival = out->survival;
-  ca.ea = out->exp_accept_len;
-  ca.acc_flag = out->accept_flag;
-  ca.val_flag = out->valid_flag;
-  ca.o_prime = out->o_prime;
-  ca.beta = out->beta;
-  ca.zeta = out->zeta;
-  ca.coef_a = out->coef_a;
-  ca.coef_b = out->coef_b;
-  ca.loss_pos = loss_pos;
-  ca.err = out->device_error;
-  ca.P = dims->B * dims->T;
-  ca.N = dims->N;
-  ca.L = dims->L;
-  ca.mode = params->mode;
-  ca.car_input = params->car_input;
-  ca.inv_tau = 1.0f / params->car_tau;
-  for (int l = 0; l < dims->L; ++l) ca.w[l] = (float)std::pow((double)params->w_base, (double)(l + 1));
-  e = vsd::launch_combine(ca, s);
-  if (e != hipSuccess) return hip_fail(e, "k_combine launch");
-  if (out->loss_total != nullptr) {
-    e = vsd::launch_loss_total(loss_pos, ca.P, params->loss_scale, out->loss_total, s);
-    if (e != hipSuccess) return hip_fail(e, "k_loss_total launch");
-  }
+  vsd_status st2 = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s);
+  if (st2 != VSD_OK) return st2;
+  return ok();
+}
+
+vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                                  const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                                  uint64_t seed, uint32_t offset, int32_t* tok_draft, int32_t* tok_target,
+                                  int32_t* tok_greedy, const vsd_score_out* out, void* workspace,
+                                  size_t workspace_bytes, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
+  if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
+  if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
+
+  const WorkspaceLayout wl = workspace_layout(dims);
+  char* ws = static_cast<char*>(workspace);
+  float* la = out->log_alpha != nullptr ? out->log_alpha : reinterpret_cast<float*>(ws + wl.la);
+  float* lq = out->log_q_tok != nullptr ? out->log_q_tok : reinterpret_cast<float*>(ws + wl.lq);
+  float* loss_pos = out->loss_pos != nullptr ? out->loss_pos : reinterpret_cast<float*>(ws + wl.loss);
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+  vsd::SampleArgs a{};
+  a.X = draft->logits;
+  a.Y = target->logits;
+  a.d2t = d2t;
+  a.depth = valid_depth;
+  a.tok_d = tok_draft;
+  a.tok_t = tok_target;
+  a.tok_g = tok_greedy;
+  a.err = out->device_error;
+  a.R = rows_of(dims);
+  a.ld_d = dims->ld_draft;
+  a.ld_t = dims->ld_target;
+  a.L = dims->L;
+  a.Vd = dims->v_draft;
+  a.Vt = dims->v_target;
+  a.inv_tq = 1.0f / params->temp_draft;
+  a.inv_tp = 1.0f / params->temp_target;
+  a.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(seed >> 32);
+  a.offset = offset;
+  a.lse_q = out->lse_draft;
+  a.lse_p = out->lse_target;
+  a.la = la;
+  a.lq = lq;
+  // target elements streamed per draft chunk: the whole target row split
+  // into as many blocks as there are 512-element draft chunks, each block a
+  // multiple of 512 elements
+  const int64_t nchunks = ((int64_t)dims->v_draft + 511) / 512;
+  a.tblock = (int32_t)(512 * ((dims->v_target + 512 * nchunks - 1) / (512 * nchunks)));
+  hipError_t e = vsd::launch_sample(a, dims->dtype == VSD_BF16, s);
+  if (e != hipSuccess) return hip_fail(e, "k_sample (fused) launch");
+  st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s);
+  if (st != VSD_OK) return st;
   return ok();
 }
 

@@ -21,6 +21,12 @@ struct SampleArgs {
   int32_t L, Vd, Vt;
   float inv_tq, inv_tp;      // float(1/T)
   uint32_t k0, k1, offset;   // Philox key words and counter word 3
+  // Fused sample + row statistics (all null for plain sampling):
+  float* lse_q;              // [R]
+  float* lse_p;              // [R] optional
+  float* la;                 // [R,3]
+  float* lq;                 // [R,3]
+  int32_t tblock;            // mapped: target elements streamed per 512-element chunk
 };
 
 struct ScoreRowArgs {

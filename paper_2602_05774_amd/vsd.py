@@ -18,7 +18,7 @@ from . import _lib
 from ._lib import (VSD_BF16, VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_F32, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR,
                    VSD_GRAD_BASIC, VsdError)
 
-__all__ = ["Problem", "Params", "SampleResult", "ScoreResult", "sample_paths", "score_paths",
+__all__ = ["Problem", "Params", "SampleResult", "ScoreResult", "sample_paths", "score_paths", "sample_score_paths",
            "weighted_loss_bwd", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
            "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]
 
@@ -194,6 +194,37 @@ def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None,
                                    _ptr(tok_target), _ptr(tok_greedy), ctypes.byref(so),
                                    _ptr(workspace), workspace.numel(), _stream(dev)))
     return out
+
+
+def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, offset=0,
+                       out: Optional[ScoreResult] = None, workspace=None, tokens=None):
+    """sample_paths then score_paths in one pass over the logits (the
+    sampling kernel also forms the row statistics).  Returns (SampleResult,
+    ScoreResult); the sample's device_error is the score's."""
+    lib = _lib.load()
+    _check_logits("X", X, prob, prob.v_draft)
+    _check_logits("Y", Y, prob, prob.v_target)
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    dev = X.device
+    if out is None:
+        out = alloc_score_outputs(prob, dev)
+    if tokens is None:
+        tokens = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), tokens):
+        _check_i32(name, t, prob.R)
+    nbytes = score_workspace_bytes(prob, X.dtype)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dims = _dims(prob, X, Y)
+    names = [f[0] for f in _lib.VsdScoreOut._fields_]
+    so = _lib.VsdScoreOut(*[None if getattr(out, k) is None else getattr(out, k).data_ptr() for k in names])
+    pr = params.c()
+    _lib.check(lib.vsd_sample_score_paths(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
+                                          ctypes.byref(_src(Y)), _ptr(d2t), _ptr(valid_depth), int(seed),
+                                          int(offset), _ptr(tokens[0]), _ptr(tokens[1]), _ptr(tokens[2]),
+                                          ctypes.byref(so), _ptr(workspace), workspace.numel(), _stream(dev)))
+    return SampleResult(tokens[0], tokens[1], tokens[2], out.device_error), out
 
 
 def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,

@@ -40,10 +40,20 @@ def params_of(cfg, **kw):
     return vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target, **kw)
 
 
-def run_step(cfg, inp, params=None, tokens=None):
-    """sample -> score -> backward on the GPU; returns device tensors."""
+def run_step(cfg, inp, params=None, tokens=None, fused=False):
+    """sample -> score -> backward on the GPU (fused: the one-pass
+    sample-and-score call); returns device tensors."""
     prob = problem_of(cfg)
     params = params or params_of(cfg)
+    if fused:
+        smp, sc = vsd.sample_score_paths(prob, params, inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"],
+                                         cfg.philox_seed, cfg.philox_offset)
+        tokens = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
+        grad = torch.full_like(inp["X"], SENTINEL)
+        vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a, sc.coef_b,
+                              grad=grad)
+        torch.cuda.synchronize()
+        return dict(tokens=tokens, score=sc, grad=grad, err_sample=sc.device_error)
     if tokens is None:
         smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"], params.temp_draft,
                                params.temp_target, cfg.philox_seed, cfg.philox_offset)

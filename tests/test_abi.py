@@ -142,3 +142,20 @@ def test_python_layer_raises_vsd_error_with_detail(lib):
     with pytest.raises(_lib.VsdError) as ei:
         _lib.check(_sample(lib, _dims(N=0)))
     assert ei.value.status == 2 and "N=0" in ei.value.message
+
+
+def test_fused_sample_score_rejects_bad_arguments(lib):
+    src = _lib.VsdSrc(FAKE, None, None)
+    out = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    def call(dims=None, params=None, toks=(FAKE, FAKE, FAKE), out=out, ws=FAKE, ws_bytes=1 << 30, d2t=None):
+        dims = dims or _dims()
+        params = params or _params()
+        return lib.vsd_sample_score_paths(ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src),
+                                          ctypes.byref(src), d2t, None, 0, 0, *toks, ctypes.byref(out), ws,
+                                          ws_bytes, None)
+    assert call(dims=_dims(N=0)) == 2
+    assert call(params=_params(car_tau=0.0)) == 3
+    assert call(toks=(FAKE, None, FAKE)) == 1
+    assert call(dims=_dims(v_target=2000, ld_target=2000)) == 5
+    assert call(ws_bytes=16) == 7
+    assert call(out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=None, device_error=FAKE)) == 1

@@ -276,3 +276,63 @@ def test_device_errors_are_reported_without_faults():
     s4 = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], depth, 1.0, 1.0, 0, 0)
     torch.cuda.synchronize()
     assert int(s4.device_error.item()) == 3
+
+
+# ------------------------------------------------------------ fused sample + score
+FUSED_CASES = {
+    "C1": (CONFIGS["C1"], None),
+    "C2s": (SMALL["C2s"], None),
+    "C3s": (SMALL["C3s"], None),
+    "C4s": (SMALL["C4s"], None),
+    "C4m_logprob": (scaled("C4", name="C4m", B=1, T=3), dict(car_input=1, loss_scale=0.5)),
+}
+
+
+@pytest.mark.parametrize("name", list(FUSED_CASES))
+def test_fused_sample_score_every_position(name):
+    cfg, extra = FUSED_CASES[name]
+    log(f"[fused] {name} R={cfg.R}")
+    inp = _to_device_c1(cfg) if cfg.name == "C1" else make_inputs(cfg, DEV)
+    params = params_of(cfg, **(extra or {}))
+    gpu = run_step(cfg, inp, params, fused=True)
+    assert int(gpu["score"].device_error.item()) == 0
+    rows, ora = oracle_positions(cfg, inp, list(range(cfg.P)), params)
+    res = compare(cfg, gpu, rows, ora, list(range(cfg.P)), label=f"fused {name}")
+    log(f"[fused] {name} worst {res['worst']}")
+    ref = run_step(cfg, inp, params)
+    for a, b in zip(gpu["tokens"], ref["tokens"]):
+        assert torch.equal(a, b), "fused and three-call tokens differ"
+
+
+@pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models"])
+def test_fused_edge_cases(name):
+    spec = dict(EDGES[name])
+    log(f"[fused-edge] {name}")
+    cfg, inp = _custom(**spec)
+    gpu = run_step(cfg, inp, fused=True)
+    assert int(gpu["score"].device_error.item()) == 0
+    rows, ora = oracle_positions(cfg, inp, list(range(cfg.P)))
+    compare(cfg, gpu, rows, ora, list(range(cfg.P)), label=f"fused {name}")
+
+
+@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
+def test_fused_full_size_sampled_positions(name):
+    cfg = CONFIGS[name]
+    log(f"[fused] {name} full size R={cfg.R}")
+    inp = make_inputs(cfg, DEV)
+    gpu = run_step(cfg, inp, fused=True)
+    assert int(gpu["score"].device_error.item()) == 0
+    _batch_properties(cfg, inp, gpu)
+    prob = problem_of(cfg)
+    smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"], cfg.temp_draft,
+                           cfg.temp_target, cfg.philox_seed, cfg.philox_offset)
+    torch.cuda.synchronize()
+    for a, b in zip(gpu["tokens"], smp[:3]):
+        assert torch.equal(a, b), "fused and three-call tokens differ"
+    rng = np.random.default_rng(321)
+    positions = sorted(set([0, cfg.P - 1] + list(rng.choice(cfg.P, 6, replace=False))))
+    rows, ora = oracle_positions(cfg, inp, positions)
+    res = compare(cfg, gpu, rows, ora, positions, label=f"fused {name}")
+    log(f"[fused] {name} positions {positions} worst {res['worst']}")
+    del inp, gpu
+    torch.cuda.empty_cache()
