@@ -75,6 +75,35 @@ def cpu_baseline(cfg, workers, per_worker=8):
                       f"{workers} worker processes, {wall:.1f} s wall"}
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
+KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_device.hpp"], "bwd": ["k_bwd.hip", "vsd_device.hpp"]}
+
+
+def source_hash(kernel):
+    """Hash of the sources a kernel is built from (traffic figures go stale when it changes)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2602_05774_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the PMC summary in profiles/, or None when no
+    figure exists for this workload and kernel or the kernel changed since."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    for line in open(TRAFFIC_FILE):
+        if line.startswith("traffic:"):
+            rec = json.loads(line[len("traffic:"):])
+            if rec.get("workload") == workload and rec.get("kernel") == kernel:
+                if rec.get("source_hash") != source_hash(kernel):
+                    return None
+                return rec.get("bytes_per_launch")
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -83,6 +112,8 @@ def main():
     ap.add_argument("--config", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-workers", type=int, default=0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device copy of this size first (calibrates PMC byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (positions shard "
@@ -121,6 +152,14 @@ def main():
     err = torch.zeros(1, dtype=torch.int32, device=dev)
 
     tok = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src_buf = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst_buf = torch.empty_like(src_buf)
+        torch.cuda.synchronize()
+        dst_buf.copy_(src_buf)
+        torch.cuda.synchronize()
+        del src_buf, dst_buf
 
     def step_fused(ev=None):
         """One EM step: one-pass sample + score, then the backward."""
@@ -189,9 +228,9 @@ def main():
                    "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score3 + t_bwd3) / HBM_PEAK_GBS}
     dominant = "sample_score" if t_ss >= t_bwd else "bwd"
     k = kernels[dominant]
-    roof = {"bound": "hbm", "kernel": "k_sample<bf16,mapped,fused>" if dominant == "sample_score" else "k_bwd",
+    roof = {"bound": "hbm", "kernel": "k_sample (fused, mapped, bf16)" if dominant == "sample_score" else "k_bwd",
             "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": k["GB/s"] / HBM_PEAK_GBS,
-            "traffic": None}
+            "traffic": measured_traffic(cfg.name, dominant)}
     line = {
         "metric": METRIC, "value": live / (t_step * 1e-3), "unit": "path-tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step, "wall_ms_per_step": wall * 1e3 / args.steps,

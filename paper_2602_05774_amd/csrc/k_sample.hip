@@ -1,13 +1,22 @@
 // E-step sampling (Alg. 1 proposal z~ ~ q and correction z' ~ p; Alg. 2
-// greedy reference z-bar), one wavefront per row.
+// greedy reference z-bar), optionally fused with the row statistics of path
+// scoring (log-sum-exps and the drawn tokens' log q / log alpha).
+//
+// Two wavefronts per row: the draft wavefront draws z~ from X (and, fused,
+// accumulates the draft log-sum-exp); the target wavefront draws z' and z-bar
+// from the mapped target logits.  Fused with a map, the target row is streamed
+// for its log-sum-exp in lock-step with the draft chunks (2048 target
+// elements per 512-element chunk, half by each wavefront), so the mapped
+// gathers of a chunk find its cache lines in L2 and every logit is read from
+// memory once.  The two wavefronts meet at one barrier at the end of the row.
 //
 // Each lane owns 8 consecutive vocabulary indices of every 512-element chunk
-// (128-bit loads; the Philox counters of S2 cover 4 consecutive indices) and
-// draws the Philox word of every element of both families.  The normative key
-// float(x/T) + G costs two logarithms with a correctly rounded division each,
-// so it is evaluated only for elements that can still win: with d = 1 - u
-// (exact on the 2^-24 grid), G = -ln(-ln(1 - d)) <= -ln(d) because
-// -ln(1 - d) >= d, and -ln(d) <= (24 - log2 j') ln 2 for the integer
+// (128-bit loads; the Philox counters of the sampler definition cover 4
+// consecutive indices) and draws the Philox word of every element.  The
+// normative key float(x/T) + G costs two logarithms with a correctly rounded
+// division each, so it is evaluated only for elements that can still win:
+// with d = 1 - u (exact on the 2^-24 grid), G = -ln(-ln(1 - d)) <= -ln(d)
+// because -ln(1 - d) >= d, and -ln(d) <= (24 - log2 j') ln 2 for the integer
 // j' = (~w) >> 8 <= 2^24 d.  An element whose bound x/T - ln(d) + margin is
 // below the running maximum (the lane's own, or the wavefront's, refreshed
 // whenever a lane improves on it) cannot be the argmax; every other element
@@ -19,10 +28,9 @@
 // Mapped target logits are gathered in lane-strided order (gather k of a
 // chunk loads indices chunk + 64k + lane: a few consecutive cache lines per
 // instruction) and transposed to the lane-contiguous layout through a
-// per-wavefront LDS tile.  Full chunks are software pipelined: the next
-// chunk's map entries and draft row are loaded while the current chunk is
-// drawn, and its target gathers are issued at the end of the current chunk
-// and consumed after the next chunk's draft-family work.
+// per-row LDS tile.  Chunks are software pipelined: the next chunk's map
+// entries and rows are loaded while the current chunk is drawn, and the target
+// gathers of the next chunk are issued at the end of the current one.
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
 
@@ -30,8 +38,9 @@ namespace vsd {
 
 namespace {
 
-constexpr int kRowsPerBlock = 4;  // 256 threads = 4 wavefronts = 4 rows
-constexpr int kChunk = 8 * kWave;  // elements per wavefront step
+constexpr int kRowsPerBlock = 2;   // 256 threads = 2 rows x 2 wavefronts
+constexpr int kChunk = 8 * kWave;  // draft elements per wavefront step
+constexpr int kStream = 2 * kChunk;  // target elements each wavefront streams per chunk (fused, mapped)
 
 template <typename T>
 __device__ __forceinline__ T neg_inf();
@@ -71,22 +80,14 @@ struct Raw8<float> {
   }
 };
 
-struct Best {
-  float key;
-  int idx;
-};
-
-// Per-lane online log-sum-exp of v/T in the exactly consistent form of the
-// scorer: mraw = largest raw value, mc = float(mraw * c), s = sum of
+// Per-lane online log-sum-exp of v/T in the scorer's exactly consistent form:
+// mraw = largest raw value, mc = float(mraw * c), s = sum of
 // exp2(fma(v, c, -mc)), c = log2(e)/T.  Elements equal to -inf add nothing.
 struct LaneLse {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
 
-  template <int K>
-  __device__ __forceinline__ void add(const float* v, float c) {
-    float cm = v[0];
-#pragma unroll
-    for (int k = 1; k < K; ++k) cm = fmaxf(cm, v[k]);
+  __device__ __forceinline__ void add8(const float (&v)[8], float c) {
+    const float cm = fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])), fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7])));
     if (cm > mraw) {
       const float nmc = cm * c;
       s *= __builtin_amdgcn_exp2f(mc - nmc);
@@ -94,58 +95,48 @@ struct LaneLse {
       mraw = cm;
     }
 #pragma unroll
-    for (int k = 0; k < K; ++k) s += __builtin_amdgcn_exp2f(fmaf(v[k], c, -mc));
+    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(v[k], c, -mc));
   }
 
-  // Wavefront reduction; returns (max raw value, ln sum exp((v - max)/T)).
-  __device__ __forceinline__ void finish(float c, float& m_out, float& tail_out) {
-    float m = mc, t = s;
-    wave_lse2(m, t);
-    const float mr = wave_max(mraw);
-    m_out = mr;
-    tail_out = (log2f(t) - fmaf(mr, c, -m)) * kLn2;
+  // Wavefront reduction (every lane ends with the row's values).
+  __device__ __forceinline__ void reduce() {
+    wave_lse2(mc, s);
+    mraw = wave_max(mraw);
   }
 };
 
-template <typename T, bool MAPPED, bool FUSED>
-struct RowSampler {
-  const T* X;
-  const T* Y;
-  const int32_t* d2t;
-  T* tile;  // this wavefront's LDS tile, kChunk elements
-  int Vd, Vt;
-  float inv_tq, inv_tp;
-  float cq2, cp2;  // log2(e) / T of each family
-  uint32_t row, offset, k0, k1;
-  int lane;
-  int tblock;      // FUSED && MAPPED: target elements streamed per chunk
-  Best bd{-INFINITY, 0x7FFFFFFF}, bt{-INFINITY, 0x7FFFFFFF}, bg{-INFINITY, 0x7FFFFFFF};
-  float wave_d = -INFINITY, wave_t = -INFINITY;  // wavefront maxima known so far
-  bool map_bad = false;
-  LaneLse lq, lp;  // FUSED: draft and target log-sum-exp accumulators
+struct Best {
+  float key;
+  int idx;
+};
 
-  // FUSED && MAPPED: log-sum-exp of the target elements [lo, hi) of the row
-  // (the target row is streamed in lock-step with the draft chunks, so the
-  // mapped gathers of the same chunk find its cache lines in L2).
-  __device__ __forceinline__ void stream_target(int lo, int hi) {
-    for (int g = lo + lane * 8; g - lane * 8 < hi; g += kChunk) {
-      float v[8];
-      if (g + 8 <= hi) {
-        load8(Y + g, v);
-      } else {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = (g + k < hi) ? load1(Y + g + k) : -INFINITY;
-      }
-      lp.template add<8>(v, cp2);
-    }
-  }
+// What the two wavefronts of a row hand to the epilogue.
+struct RowShared {
+  Best d, t, g;
+  float q_mraw, q_mc, q_s;   // draft log-sum-exp (reduced)
+  float p_mraw[2], p_mc[2], p_s[2];  // target log-sum-exp partials of the two wavefronts
+};
 
-  __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t fam) const {
-    return philox4x32_10(c0, row, fam, offset, k0, k1);
+// State and steps common to both wavefronts of a row: the Philox draws and
+// the exact filter of one family.
+struct FamilyDraw {
+  uint32_t row, fam, offset, k0, k1;
+  float inv_t, c2;  // 1/T and log2(e)/T
+  Best best{-INFINITY, 0x7FFFFFFF};
+  float wave_best = -INFINITY;  // wavefront maximum known so far
+
+  __device__ __forceinline__ uint4 philox(uint32_t c0) const { return philox4x32_10(c0, row, fam, offset, k0, k1); }
+
+  // (thr - margin) log2e folded into the bound's constant.  The margin
+  // 2e-3 + 2e-6 |thr| exceeds every rounding involved for elements with
+  // |x/T| <= |thr| + 100; an element with x/T < thr - 100 cannot reach thr
+  // because G < 16.7.
+  __device__ __forceinline__ static float bound_offset(float thr) {
+    return 24.0f - (thr - (2e-3f + 2e-6f * fabsf(thr))) * kLog2e;
   }
 
   // Bound test of the 4 elements that share one Philox counter: bit k set
-  // where x * log2e/T + off >= log2(j'), off = 24 - (thr - margin) log2e.
+  // where v * log2e/T + off >= log2(j').
   __device__ __forceinline__ static uint32_t cand4(const uint4& w, const float* v, float c2, float off) {
     uint32_t m = 0;
 #pragma unroll
@@ -156,139 +147,170 @@ struct RowSampler {
     return m;
   }
 
-  // (thr - margin) log2e folded into the bound's constant.  The margin
-  // 2e-3 + 2e-6 |thr| exceeds every rounding involved for elements with
-  // |x/T| <= |thr| + 100; an element with x/T < thr - 100 cannot reach thr
-  // because G < 16.7.
-  __device__ __forceinline__ static float bound_offset(float thr) {
-    return 24.0f - (thr - (2e-3f + 2e-6f * fabsf(thr))) * kLog2e;
-  }
-
-  // Exact keys of the candidates (rare); their Philox words are recomputed.
-  __device__ __forceinline__ void exact(int base, const float (&x)[8], const float (&y)[8], uint32_t cd,
-                                        uint32_t ct) {
-    if (__ballot((cd | ct) != 0u) == 0ull) return;
+  // Draw the lane's 8 elements at `base` (values v, the first nvalid valid).
+  __device__ __forceinline__ void draw(int base, const float (&v)[8], int nvalid) {
     const uint32_t c0 = (uint32_t)base >> 2;
+    const float off = bound_offset(fmaxf(best.key, wave_best));
+    uint32_t cand = cand4(philox(c0), v, c2, off) | (cand4(philox(c0 + 1), v + 4, c2, off) << 4);
+    cand &= (1u << nvalid) - 1u;
+    if (__ballot(cand != 0u) == 0ull) return;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      if (cd & (1u << k)) {
-        const float kd = gumbel_key(x[k], inv_tq, word_of(philox(c0 + (k >> 2), 0u), k & 3));
-        if (kd > bd.key) {
-          bd.key = kd;
-          bd.idx = base + k;
-        }
-      }
-      if (ct & (1u << k)) {
-        const float kt = gumbel_key(y[k], inv_tp, word_of(philox(c0 + (k >> 2), 1u), k & 3));
-        if (kt > bt.key) {
-          bt.key = kt;
-          bt.idx = base + k;
+      if (cand & (1u << k)) {  // rare: the exact key, Philox word recomputed
+        const float key = gumbel_key(v[k], inv_t, word_of(philox(c0 + (k >> 2)), k & 3));
+        if (key > best.key) {
+          best.key = key;
+          best.idx = base + k;
         }
       }
     }
-    if (__ballot(bd.key > wave_d || bt.key > wave_t) != 0ull) {
-      wave_d = wave_max(bd.key);
-      wave_t = wave_max(bt.key);
+    if (__ballot(best.key > wave_best) != 0ull) wave_best = wave_max(best.key);
+  }
+};
+
+// Log-sum-exp of target elements [lo, hi) of a row (guarded at both ends).
+template <typename T>
+__device__ __forceinline__ void stream_lse(const T* Y, int lo, int hi, int lane, float c2, LaneLse& acc) {
+  for (int g = lo + lane * 8; g - lane * 8 < hi; g += kChunk) {
+    float v[8];
+    if (g + 8 <= hi) {
+      load8(Y + g, v);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = (g + k < hi) ? load1(Y + g + k) : -INFINITY;
+    }
+    acc.add8(v, c2);
+  }
+}
+
+// The draft wavefront of a row: z~ and, fused, the draft log-sum-exp and one
+// half of the target stream.
+template <typename T, bool MAPPED, bool FUSED>
+__device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f, LaneLse& lq, LaneLse& lp,
+                           float cp2, int lane) {
+  const int nfull = Vd / kChunk;
+  if (nfull > 0) {
+    Raw8<T> xr;
+    xr.load(X + lane * 8);
+    for (int it = 0; it < nfull; ++it) {
+      const int base = it * kChunk + lane * 8;
+      Raw8<T> xn;
+      if (it + 1 < nfull) xn.load(X + base + kChunk);
+      float x[8];
+      xr.unpack(x);
+      if (FUSED) lq.add8(x, f.c2);
+      f.draw(base, x, 8);
+      if (FUSED && MAPPED) {
+        const int lo = it * 2 * kStream;
+        stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
+      }
+      xr = xn;
     }
   }
+  if (nfull * kChunk < Vd) {  // the partial last chunk
+    const int base = nfull * kChunk + lane * 8;
+    const int nvalid = min(8, max(0, Vd - base));
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = k < nvalid ? load1(X + base + k) : -INFINITY;
+    if (FUSED) lq.add8(x, f.c2);
+    f.draw(base, x, nvalid);
+    if (FUSED && MAPPED) {
+      const int lo = nfull * 2 * kStream;
+      stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
+    }
+  }
+  if (FUSED && MAPPED) {  // target elements past the last chunk's block: even half-blocks
+    const int nchunks = (Vd + kChunk - 1) / kChunk;
+    for (int lo = nchunks * 2 * kStream; lo < Vt; lo += 2 * kStream)
+      stream_lse(Y, lo, min(lo + kStream, Vt), lane, cp2, lp);
+  }
+}
 
-  __device__ __forceinline__ void greedy(int base, const float (&y)[8], int nvalid) {
+// The target wavefront of a row: z' and z-bar and, fused, the target
+// log-sum-exp (unmapped) or the other half of the target stream (mapped).
+template <typename T, bool MAPPED, bool FUSED>
+__device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int Vt, FamilyDraw& f, Best& bg,
+                            LaneLse& lp, bool& map_bad, int lane) {
+  const int nfull = Vd / kChunk;
+  auto greedy = [&](int base, const float (&y)[8], int nvalid) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const bool better = k < nvalid && y[k] > bg.key;
       bg.key = better ? y[k] : bg.key;
       bg.idx = better ? base + k : bg.idx;
     }
-  }
-
-  // Map entries of a full chunk in lane-strided order.
-  __device__ __forceinline__ void load_map(int chunk, uint32_t (&t)[8]) const {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) t[k] = (uint32_t)d2t[chunk + k * kWave + lane];
-  }
-
-  // Gathers of the mapped target logits; an out-of-range map entry reads
-  // element 0 instead and is flagged in `bad`.
-  __device__ __forceinline__ void gather(const uint32_t (&t)[8], T (&g)[8], uint32_t& bad) const {
-    bad = 0;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const bool ok = t[k] < (uint32_t)Vt;
-      bad |= ok ? 0u : (1u << k);
-      g[k] = Y[ok ? t[k] : 0u];
-    }
-  }
-
-  // Transpose gathered values through the LDS tile into this lane's 8
-  // lane-contiguous target logits (flagged entries become -inf).  LDS
-  // operations of one wavefront execute in order: no barrier is needed.
-  __device__ __forceinline__ void transpose(const T (&g)[8], uint32_t bad, float (&y)[8]) {
-    map_bad |= bad != 0u;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) tile[k * kWave + lane] = (bad & (1u << k)) ? neg_inf<T>() : g[k];
-    load8(tile + lane * 8, y);
-  }
-
-  // Every chunk of the row whose 512 elements are all in range.
-  __device__ void full_chunks(int nfull) {
-    if (nfull == 0) return;
+  };
+  if (nfull > 0) {
     uint32_t t[8];
     T g[8];
     uint32_t bad = 0;
-    Raw8<T> xr, yr;
+    Raw8<T> yr;
+    auto load_map = [&](int chunk, uint32_t (&tt)[8]) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) tt[k] = (uint32_t)d2t[chunk + k * kWave + lane];
+    };
+    auto gather = [&](const uint32_t (&tt)[8]) {  // out-of-range entries read element 0, flagged
+      bad = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const bool ok = tt[k] < (uint32_t)Vt;
+        bad |= ok ? 0u : (1u << k);
+        g[k] = Y[ok ? tt[k] : 0u];
+      }
+    };
     if (MAPPED) {
       load_map(0, t);
-      gather(t, g, bad);
+      gather(t);
     } else {
       yr.load(Y + lane * 8);
     }
-    xr.load(X + lane * 8);
     for (int it = 0; it < nfull; ++it) {
       const int chunk = it * kChunk;
       const int base = chunk + lane * 8;
       const bool next = it + 1 < nfull;
       uint32_t tn[8];
-      Raw8<T> xn, yn;
-      if (next) {  // prefetch the next chunk's map entries and rows
+      Raw8<T> yn;
+      if (next) {
         if (MAPPED)
           load_map(chunk + kChunk, tn);
         else
           yn.load(Y + base + kChunk);
-        xn.load(X + base + kChunk);
       }
-      const uint32_t c0 = (uint32_t)base >> 2;
-      // draft family first: it does not wait for this chunk's gathers
-      float x[8];
-      xr.unpack(x);
-      if (FUSED) lq.template add<8>(x, cq2);
-      const float od = bound_offset(fmaxf(bd.key, wave_d));
-      const uint32_t cd = cand4(philox(c0, 0u), x, cq2, od) | (cand4(philox(c0 + 1, 0u), x + 4, cq2, od) << 4);
+      if (FUSED && MAPPED) {  // this chunk's target block, second half
+        const int lo = it * 2 * kStream + kStream;
+        stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
+      }
       float y[8];
-      if (MAPPED)
-        transpose(g, bad, y);
-      else
+      if (MAPPED) {
+        // transpose the gathered values through the LDS tile; LDS operations
+        // of one wavefront execute in order, so no barrier is needed
+        map_bad |= bad != 0u;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) tile[k * kWave + lane] = (bad & (1u << k)) ? neg_inf<T>() : g[k];
+        load8(tile + lane * 8, y);
+      } else {
         yr.unpack(y);
-      if (FUSED && !MAPPED) lp.template add<8>(y, cp2);
-      if (FUSED && MAPPED) stream_target(it * tblock, min(Vt, (it + 1) * tblock));
+        if (FUSED) lp.add8(y, f.c2);
+      }
       greedy(base, y, 8);
-      const float ot = bound_offset(fmaxf(bt.key, wave_t));
-      const uint32_t ct = cand4(philox(c0, 1u), y, cp2, ot) | (cand4(philox(c0 + 1, 1u), y + 4, cp2, ot) << 4);
-      exact(base, x, y, cd, ct);
+      f.draw(base, y, 8);
       if (next) {
         if (MAPPED)
-          gather(tn, g, bad);
+          gather(tn);
         else
           yr = yn;
-        xr = xn;
       }
     }
   }
-
-  // The row's last, partial chunk (guarded element by element).
-  __device__ void tail_chunk(int chunk) {
-    if (FUSED && MAPPED) stream_target((chunk / kChunk) * tblock, min(Vt, (chunk / kChunk + 1) * tblock));
+  if (nfull * kChunk < Vd) {  // the partial last chunk
+    const int chunk = nfull * kChunk;
     const int base = chunk + lane * 8;
     const int nvalid = min(8, max(0, Vd - base));
+    if (FUSED && MAPPED) {
+      const int lo = nfull * 2 * kStream + kStream;
+      stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
+    }
     if (MAPPED) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -301,45 +323,90 @@ struct RowSampler {
         tile[k * kWave + lane] = (in && ok) ? val : neg_inf<T>();
       }
     }
-    float x[8], y[8];
+    float y[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const bool in = k < nvalid;
-      x[k] = in ? load1(X + base + k) : -INFINITY;
       y[k] = in ? (MAPPED ? load1(tile + lane * 8 + k) : load1(Y + base + k)) : -INFINITY;
     }
-    if (FUSED) {
-      lq.template add<8>(x, cq2);
-      if (!MAPPED) lp.template add<8>(y, cp2);
-    }
+    if (FUSED && !MAPPED) lp.add8(y, f.c2);
     greedy(base, y, nvalid);
-    const uint32_t c0 = (uint32_t)base >> 2;
-    const uint32_t valid = (1u << nvalid) - 1u;
-    const float od = bound_offset(fmaxf(bd.key, wave_d));
-    const float ot = bound_offset(fmaxf(bt.key, wave_t));
-    const uint32_t cd = (cand4(philox(c0, 0u), x, cq2, od) | (cand4(philox(c0 + 1, 0u), x + 4, cq2, od) << 4)) & valid;
-    const uint32_t ct = (cand4(philox(c0, 1u), y, cp2, ot) | (cand4(philox(c0 + 1, 1u), y + 4, cp2, ot) << 4)) & valid;
-    exact(base, x, y, cd, ct);
+    f.draw(base, y, nvalid);
   }
-};
+  if (FUSED && MAPPED) {  // target elements past the last chunk's block: odd half-blocks
+    const int nchunks = (Vd + kChunk - 1) / kChunk;
+    for (int lo = nchunks * 2 * kStream + kStream; lo < Vt; lo += 2 * kStream)
+      stream_lse(Y, lo, min(lo + kStream, Vt), lane, f.c2, lp);
+  }
+}
 
 template <typename T, bool MAPPED, bool FUSED>
 __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   __shared__ __align__(16) T ytile[kRowsPerBlock][kChunk];
+  __shared__ RowShared sh[kRowsPerBlock];
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-  if (r >= a.R) return;
-  const int i = (int)(r % a.L);
-  const int64_t path = r / a.L;  // (b*T + t)*N + s
-  int d = a.L;
-  if (a.depth != nullptr) {
-    d = a.depth[path];
-    if (d < 1 || d > a.L) {
-      if (lane == 0) report_error(a.err, VSD_DEVERR_DEPTH_RANGE);
-      d = 0;
+  const int wave = threadIdx.x >> 6;
+  const int slot = wave >> 1;       // row within the block
+  const bool draft_role = (wave & 1) == 0;
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + slot;
+  const bool active = r < a.R;
+  bool live = false;
+  if (active) {
+    const int i = (int)(r % a.L);
+    int d = a.L;
+    if (a.depth != nullptr) {
+      d = a.depth[r / a.L];
+      if (d < 1 || d > a.L) {
+        if (lane == 0 && draft_role) report_error(a.err, VSD_DEVERR_DEPTH_RANGE);
+        d = 0;
+      }
+    }
+    live = i < d;
+  }
+  const T* X = static_cast<const T*>(a.X) + (active ? r : 0) * a.ld_d;
+  const T* Y = static_cast<const T*>(a.Y) + (active ? r : 0) * a.ld_t;
+  const float cq2 = a.inv_tq * kLog2e, cp2 = a.inv_tp * kLog2e;
+  LaneLse lq, lp;
+  if (live) {
+    if (draft_role) {
+      FamilyDraw f{(uint32_t)r, 0u, a.offset, a.k0, a.k1, a.inv_tq, cq2};
+      draft_wave<T, MAPPED, FUSED>(X, Y, a.Vd, a.Vt, f, lq, lp, cp2, lane);
+      wave_argmax(f.best.key, f.best.idx);
+      if (FUSED) {
+        lq.reduce();
+        lp.reduce();
+      }
+      if (lane == 0) {
+        sh[slot].d = f.best;
+        sh[slot].q_mraw = lq.mraw;
+        sh[slot].q_mc = lq.mc;
+        sh[slot].q_s = lq.s;
+        sh[slot].p_mraw[0] = lp.mraw;
+        sh[slot].p_mc[0] = lp.mc;
+        sh[slot].p_s[0] = lp.s;
+      }
+    } else {
+      FamilyDraw f{(uint32_t)r, 1u, a.offset, a.k0, a.k1, a.inv_tp, cp2};
+      Best bg{-INFINITY, 0x7FFFFFFF};
+      bool map_bad = false;
+      target_wave<T, MAPPED, FUSED>(Y, a.d2t, ytile[slot], a.Vd, a.Vt, f, bg, lp, map_bad, lane);
+      if (map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
+      wave_argmax(f.best.key, f.best.idx);
+      wave_argmax(bg.key, bg.idx);
+      if (FUSED) lp.reduce();
+      if (lane == 0) {
+        sh[slot].t = f.best;
+        sh[slot].g = bg;
+        sh[slot].p_mraw[1] = lp.mraw;
+        sh[slot].p_mc[1] = lp.mc;
+        sh[slot].p_s[1] = lp.s;
+      }
     }
   }
-  if (i >= d) {  // masked slot: tokens -1, score outputs 0, nothing read
+  __syncthreads();
+  if (!active || draft_role) return;
+  // epilogue, by the target wavefront's first three lanes
+  if (!live) {  // masked slot: tokens -1, score outputs 0, nothing read
     if (lane == 0) {
       a.tok_d[r] = -1;
       a.tok_t[r] = -1;
@@ -357,64 +424,37 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     }
     return;
   }
-  const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
-  const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
-  RowSampler<T, MAPPED, FUSED> s{X,
-                                 Y,
-                                 a.d2t,
-                                 ytile[threadIdx.x >> 6],
-                                 a.Vd,
-                                 a.Vt,
-                                 a.inv_tq,
-                                 a.inv_tp,
-                                 a.inv_tq * kLog2e,
-                                 a.inv_tp * kLog2e,
-                                 (uint32_t)r,
-                                 a.offset,
-                                 a.k0,
-                                 a.k1,
-                                 lane,
-                                 a.tblock};
-  const int nfull = a.Vd / kChunk;
-  s.full_chunks(nfull);
-  if (nfull * kChunk < a.Vd) s.tail_chunk(nfull * kChunk);
-  if (FUSED && MAPPED) {  // target elements past the last chunk's block (none when tblock covers the row)
-    const int nchunks = (a.Vd + kChunk - 1) / kChunk;
-    s.stream_target(min(a.Vt, nchunks * a.tblock), a.Vt);
-  }
-  if (s.map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
-  wave_argmax(s.bd.key, s.bd.idx);
-  wave_argmax(s.bt.key, s.bt.idx);
-  wave_argmax(s.bg.key, s.bg.idx);
-  if (FUSED) {
-    // Row statistics of the scorer, in its exactly consistent shifted form,
-    // and log q / log alpha of the three drawn tokens.
-    float mq, tq, mp, tp;
-    s.lq.finish(s.cq2, mq, tq);
-    s.lp.finish(s.cp2, mp, tp);
-    if (lane < 3) {
-      const int z = lane == 0 ? s.bd.idx : lane == 1 ? s.bt.idx : s.bg.idx;
-      float lqv = 0.0f, lav = 0.0f;
-      if ((uint32_t)z < (uint32_t)a.Vd) {
-        const int32_t zt = MAPPED ? a.d2t[z] : z;
-        if ((uint32_t)zt < (uint32_t)a.Vt) {
-          lqv = (load1(X + z) - mq) * a.inv_tq - tq;
-          const float lp = (load1(Y + zt) - mp) * a.inv_tp - tp;
-          lav = fminf(0.0f, lp - lqv);
-        }
-      }
-      a.la[r * 3 + lane] = lav;
-      a.lq[r * 3 + lane] = lqv;
-    }
-    if (lane == 0) {
-      a.lse_q[r] = mq * a.inv_tq + tq;
-      if (a.lse_p != nullptr) a.lse_p[r] = mp * a.inv_tp + tp;
-    }
-  }
+  const RowShared& s = sh[slot];
   if (lane == 0) {
-    a.tok_d[r] = s.bd.idx;
-    a.tok_t[r] = s.bt.idx;
-    a.tok_g[r] = s.bg.idx;
+    a.tok_d[r] = s.d.idx;
+    a.tok_t[r] = s.t.idx;
+    a.tok_g[r] = s.g.idx;
+  }
+  if (FUSED && lane < 3) {
+    // row statistics in the scorer's shifted form: log q(z) = (x_z - max)/T
+    // - ln sum exp((x - max)/T), the scaled maximum's rounding corrected
+    const float qt = (log2f(s.q_s) - fmaf(s.q_mraw, cq2, -s.q_mc)) * kLn2;
+    const float pmc = fmaxf(s.p_mc[0], s.p_mc[1]);
+    const float ps = s.p_s[0] * __builtin_amdgcn_exp2f(s.p_mc[0] - pmc) +
+                     s.p_s[1] * __builtin_amdgcn_exp2f(s.p_mc[1] - pmc);
+    const float pmraw = fmaxf(s.p_mraw[0], s.p_mraw[1]);
+    const float pt = (log2f(ps) - fmaf(pmraw, cp2, -pmc)) * kLn2;
+    const int z = lane == 0 ? s.d.idx : lane == 1 ? s.t.idx : s.g.idx;
+    float lqv = 0.0f, lav = 0.0f;
+    if ((uint32_t)z < (uint32_t)a.Vd) {
+      const int32_t zt = MAPPED ? a.d2t[z] : z;
+      if ((uint32_t)zt < (uint32_t)a.Vt) {
+        lqv = (load1(X + z) - s.q_mraw) * a.inv_tq - qt;
+        const float lpv = (load1(Y + zt) - pmraw) * a.inv_tp - pt;
+        lav = fminf(0.0f, lpv - lqv);
+      }
+    }
+    a.la[r * 3 + lane] = lav;
+    a.lq[r * 3 + lane] = lqv;
+    if (lane == 0) {
+      a.lse_q[r] = s.q_mraw * a.inv_tq + qt;
+      if (a.lse_p != nullptr) a.lse_p[r] = pmraw * a.inv_tp + pt;
+    }
   }
 }
 
