@@ -21,6 +21,11 @@
  *   vsd_weighted_loss_bwd Gradient of that loss with respect to the draft
  *                         logits (derivative of Eq. advance).
  *
+ * Every call takes the logits either materialised ([R, ld] arrays) or, in
+ * the fused LM-head variant (dims->hidden_dim > 0), as hidden states and an
+ * LM-head weight: logits = hidden @ weight^T, computed tile by tile on the
+ * matrix cores and never stored (see "Fused LM head" below).
+ *
  * Terminology and layout
  * ----------------------
  *   position x = (b, t), b < B, t < T;  P = B*T positions.
@@ -119,6 +124,27 @@
  *      target logit Y[r][d2t[v]]; among equal logits the smallest v
  *      (Alg. 2, greedy target policy).
  *   Logits must be finite.
+ *
+ * Fused LM head (dims->hidden_dim = H > 0)
+ * ----------------------------------------
+ *   Both sources give `hidden` [R, H] and `weight` [V, H] (bf16, rows
+ *   contiguous, 16-byte aligned; `logits` NULL; dims->dtype = VSD_BF16;
+ *   H a multiple of 64).  X_r = hidden_d[r] . weight_d^T and Y_r likewise,
+ *   accumulated in fp32; every definition above applies to these values.
+ *   The fp32 sum's order is the library's (not fixed by this header), so
+ *   tokens are reproducible run to run but a different implementation
+ *   agrees with them only where the top two keys (or greedy values) of a row
+ *   are further apart than the products' rounding.
+ *   vsd_sample_paths does not accept fused sources (it has no workspace);
+ *   vsd_sample_score_paths draws and scores, vsd_score_paths scores given
+ *   tokens.  The map d2t, when given, must be injective (it is inverted on
+ *   the device).  The workspace (vsd_score_workspace_bytes with the same
+ *   dims) then also holds per-slice partial row statistics.
+ *   Backward: grad->grad_logits (bf16, row stride dims->ld_draft, a multiple
+ *   of 8 >= v_draft) receives g as defined at vsd_weighted_loss_bwd, and
+ *   grad->grad_hidden [R, H] (bf16) receives g . weight_d.
+ *   grad->grad_weight must be NULL (the weight gradient is not computed).
+ *   dims->ld_target is unused.
  */
 #ifndef VSD_H
 #define VSD_H
@@ -172,8 +198,9 @@ typedef struct vsd_dims {
   int32_t v_draft;     /* draft vocabulary size, >= 1 */
   int32_t v_target;    /* target vocabulary size, >= v_draft */
   int32_t dtype;       /* vsd_dtype of the logit (or hidden/weight) arrays */
-  int32_t hidden_dim;  /* fused LM-head variant only: H; 0 otherwise */
-  int64_t ld_draft;    /* row stride of the draft logit array, elements */
+  int32_t hidden_dim;  /* fused LM-head variant: H (multiple of 64); 0 otherwise */
+  int64_t ld_draft;    /* row stride of the draft logit array (fused: of the
+                          bf16 logit-gradient buffer), elements */
   int64_t ld_target;   /* row stride of the target logit array, elements */
 } vsd_dims;
 
@@ -187,9 +214,10 @@ typedef struct vsd_params {
   float loss_scale;    /* multiplies the summed loss and the gradient */
 } vsd_params;
 
-/* Source of one model's logits.  Materialised: `logits` != NULL, an [R, ld]
- * array of dims->dtype.  Fused LM head: `logits` == NULL, logits are
- * hidden[R, H] @ weight[V, H]^T computed on the fly (bf16 only). */
+/* Source of one model's logits.  Materialised (dims->hidden_dim == 0):
+ * `logits` != NULL, an [R, ld] array of dims->dtype.  Fused LM head
+ * (dims->hidden_dim > 0): `logits` == NULL, logits are hidden[R, H] @
+ * weight[V, H]^T computed on the fly (bf16 only). */
 typedef struct vsd_src {
   const void* logits;
   const void* hidden;
@@ -216,15 +244,16 @@ typedef struct vsd_score_out {
 } vsd_score_out;
 
 typedef struct vsd_grad {
-  void* grad_logits;      /* materialised: [R, ld_draft], dtype of X */
-  void* grad_hidden;      /* fused: [R, H] bf16 */
-  float* grad_weight;     /* fused, optional: [v_draft, H] fp32 */
+  void* grad_logits;      /* [R, ld_draft]: dtype of X; fused: bf16 */
+  void* grad_hidden;      /* fused: [R, H] bf16, required */
+  float* grad_weight;     /* fused: must be NULL (not computed) */
 } vsd_grad;
 
 /* E-step sampling (Alg. 1: z~ ~ q and z' ~ p; Alg. 2: z-bar greedy).
  * Writes tok_draft, tok_target, tok_greedy ([R] int32 each, draft-index
  * space, -1 on masked rows) following the normative sampler definition above.
- * Reads X (draft) over [0, v_draft) and Y (target) at d2t[v] for every v. */
+ * Reads X (draft) over [0, v_draft) and Y (target) at d2t[v] for every v.
+ * Materialised logits only (fused sources: VSD_ERR_UNSUPPORTED). */
 vsd_status vsd_sample_paths(const vsd_dims* dims, const vsd_src* draft,
                             const vsd_src* target, const int32_t* d2t,
                             const int32_t* valid_depth, float temp_draft,
@@ -274,7 +303,9 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
  * every row are written; rows with a = b = 0 (masked rows among them) are
  * written as zeros without reading X; padding columns [v_draft, ld) are not
  * touched.  grad_logits has the layout of X (stride ld_draft) and its dtype
- * (bf16 rounded to nearest-even). */
+ * (bf16 rounded to nearest-even).  Fused LM head: X is recomputed from the
+ * draft hidden states, g is written to grad_logits in bf16, and grad_hidden
+ * = g . weight_d (fp32 accumulation of the bf16 g, bf16 result). */
 vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
                                  const vsd_src* draft, const float* lse_draft,
                                  const int32_t* tok_draft,

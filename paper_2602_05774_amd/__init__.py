@@ -3,14 +3,16 @@
 The data-parallel hot path of Variational Speculative Decoding's EM draft
 training, as hand-written HIP kernels behind a C ABI (include/vsd.h):
 E-step sampling, path scoring with the oracle gate, ARW and CAR weights, the
-weighted-likelihood loss and its gradient with respect to the draft logits.
+weighted-likelihood loss and its gradient with respect to the draft logits,
+from materialised logits or through a fused LM head (MFMA GEMM tiles consumed
+in place).
 This package holds the kernels (csrc/), their build (build.py) and a thin
 torch binding (vsd.py).
 """
-from .vsd import (VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR, VSD_GRAD_BASIC, Params,
-                  Problem, SampleResult, ScoreResult, VsdError, alloc_score_outputs, sample_paths,
+from .vsd import (VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR, VSD_GRAD_BASIC, LmHead,
+                  LmHeadGrad, Params, Problem, SampleResult, ScoreResult, VsdError, alloc_score_outputs, sample_paths,
                   sample_score_paths, score_paths, score_workspace_bytes, weighted_loss_bwd)
 
-__all__ = ["Params", "Problem", "SampleResult", "ScoreResult", "VsdError", "alloc_score_outputs",
+__all__ = ["LmHead", "LmHeadGrad", "Params", "Problem", "SampleResult", "ScoreResult", "VsdError", "alloc_score_outputs",
            "sample_paths", "sample_score_paths", "score_paths", "score_workspace_bytes", "weighted_loss_bwd",
            "VSD_GRAD_BASIC", "VSD_GRAD_ARW", "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]

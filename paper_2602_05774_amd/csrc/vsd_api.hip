@@ -1,5 +1,6 @@
 // Host side of the C ABI declared in include/vsd.h: argument validation
 // (before any launch), workspace layout, launch geometry, error reporting.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -32,6 +33,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 
 constexpr int64_t kMaxRows = (int64_t)1 << 31;
+constexpr int32_t kMaxHidden = 65536;
 
 size_t align_up(size_t n) { return (n + 255) & ~(size_t)255; }
 
@@ -50,6 +52,34 @@ vsd_status check_dims(const vsd_dims* d) {
   if (d->dtype != VSD_F32 && d->dtype != VSD_BF16) return fail(VSD_ERR_INVALID_VALUE, "dtype=%d", d->dtype);
   const int64_t R = rows_of(d);
   if (R >= kMaxRows) return fail(VSD_ERR_INVALID_SHAPE, "R=B*T*N*L=%lld must be < 2^31", (long long)R);
+  if (d->hidden_dim < 0 || d->hidden_dim > kMaxHidden || d->hidden_dim % 64 != 0)
+    return fail(VSD_ERR_INVALID_SHAPE, "hidden_dim=%d must be 0 or a multiple of 64 up to %d", d->hidden_dim,
+                kMaxHidden);
+  if (d->hidden_dim > 0) {
+    if (d->dtype != VSD_BF16) return fail(VSD_ERR_UNSUPPORTED, "the fused LM head takes bf16 operands only");
+    // workgroup ids of the fused kernels are 32-bit: row tiles x vocabulary tiles
+    const int64_t nrt = (R + vsd::kLmTile - 1) / vsd::kLmTile;
+    const int64_t vt = std::max<int64_t>((d->v_draft + vsd::kLmTile - 1) / vsd::kLmTile,
+                                         vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
+    if (nrt * vt >= kMaxRows)
+      return fail(VSD_ERR_INVALID_SHAPE, "fused LM head: R=%lld rows x %lld vocabulary tiles too large",
+                  (long long)R, (long long)vt);
+  }
+  return VSD_OK;
+}
+
+bool is_fused(const vsd_dims* d) { return d->hidden_dim > 0; }
+
+// Fused LM-head checks for one source: hidden [R, H] and weight [V, H], bf16,
+// rows contiguous.
+vsd_status check_fused_src(const vsd_src* src, const char* name) {
+  if (src == nullptr) return fail(VSD_ERR_NULL_POINTER, "%s source is NULL", name);
+  if (src->logits != nullptr)
+    return fail(VSD_ERR_UNSUPPORTED, "%s: hidden_dim > 0 selects the fused LM head, but logits were given", name);
+  if (src->hidden == nullptr || src->weight == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "%s: the fused LM head needs hidden and weight", name);
+  if (!aligned16(src->hidden) || !aligned16(src->weight))
+    return fail(VSD_ERR_MISALIGNED, "%s hidden / weight pointer not 16-byte aligned", name);
   return VSD_OK;
 }
 
@@ -58,7 +88,8 @@ vsd_status check_logits(const vsd_dims* d, const vsd_src* src, const char* name,
   if (src == nullptr) return fail(VSD_ERR_NULL_POINTER, "%s source is NULL", name);
   if (src->logits == nullptr) {
     if (src->hidden != nullptr || src->weight != nullptr)
-      return fail(VSD_ERR_UNSUPPORTED, "%s: the fused LM-head source is not available in this build", name);
+      return fail(VSD_ERR_UNSUPPORTED, "%s: a fused LM-head source needs dims->hidden_dim > 0 (and is not "
+                  "accepted by vsd_sample_paths)", name);
     return fail(VSD_ERR_NULL_POINTER, "%s logits are NULL", name);
   }
   const int64_t es = d->dtype == VSD_F32 ? 4 : 2;
@@ -74,6 +105,18 @@ vsd_status check_map(const vsd_dims* d, const int32_t* d2t) {
     return fail(VSD_ERR_MAP_REQUIRED, "v_draft=%d != v_target=%d requires d2t", d->v_draft, d->v_target);
   if (d2t != nullptr && !aligned16(d2t)) return fail(VSD_ERR_MISALIGNED, "d2t pointer not 16-byte aligned");
   return VSD_OK;
+}
+
+// Both sources materialised (hidden_dim == 0) or both fused LM heads
+// (hidden_dim > 0).
+vsd_status check_sources(const vsd_dims* d, const vsd_src* draft, const vsd_src* target) {
+  vsd_status st;
+  if (d->hidden_dim > 0) {
+    if ((st = check_fused_src(draft, "draft")) != VSD_OK) return st;
+    return check_fused_src(target, "target");
+  }
+  if ((st = check_logits(d, draft, "draft", d->ld_draft, d->v_draft)) != VSD_OK) return st;
+  return check_logits(d, target, "target", d->ld_target, d->v_target);
 }
 
 vsd_status check_params(const vsd_params* p) {
@@ -94,9 +137,11 @@ vsd_status hip_fail(hipError_t e, const char* what) {
 }
 
 struct WorkspaceLayout {
-  size_t la, lq, loss, total;
+  size_t la, lq, loss, inv, part, total;
 };
 
+// la [R,3], lq [R,3], loss [P] fp32; fused LM head also: inv [v_target]
+// int32 and the slice partials [R, nslice_t + nslice_d].
 WorkspaceLayout workspace_layout(const vsd_dims* d) {
   const int64_t R = rows_of(d);
   const int64_t P = (int64_t)d->B * d->T;
@@ -104,7 +149,14 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   w.la = 0;
   w.lq = w.la + align_up((size_t)R * 3 * sizeof(float));
   w.loss = w.lq + align_up((size_t)R * 3 * sizeof(float));
-  w.total = w.loss + align_up((size_t)P * sizeof(float));
+  w.inv = w.loss + align_up((size_t)P * sizeof(float));
+  w.part = w.inv;
+  w.total = w.inv;
+  if (d->hidden_dim > 0) {
+    w.part = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
+    const size_t nsl = (size_t)(vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
+    w.total = w.part + align_up((size_t)R * nsl * sizeof(vsd::LmPartial));
+  }
   return w;
 }
 
@@ -159,6 +211,74 @@ vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* para
   return VSD_OK;
 }
 
+// Fused LM head: the forward GEMM pass over both vocabularies (sampling
+// or log-sum-exp only), then the slice combine into tokens and row
+// statistics.  tok_in != null scores the given tokens; otherwise draws.
+vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft, const vsd_src* target,
+                      const int32_t* d2t, const int32_t* valid_depth, uint64_t seed, uint32_t offset,
+                      const int32_t* const tok_in[3], int32_t* const tok_out[3], const vsd_score_out* out,
+                      char* ws, const WorkspaceLayout& wl, float* la, float* lq, hipStream_t s) {
+  const bool sampling = tok_in == nullptr;
+  int32_t* inv = nullptr;
+  hipError_t e;
+  if (sampling && d2t != nullptr) {
+    inv = reinterpret_cast<int32_t*>(ws + wl.inv);
+    e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
+    if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
+  }
+  vsd::LmPartial* part = reinterpret_cast<vsd::LmPartial*>(ws + wl.part);
+  vsd::LmFwdArgs f{};
+  f.Hd = draft->hidden;
+  f.Ht = target->hidden;
+  f.Wd = draft->weight;
+  f.Wt = target->weight;
+  f.inv = inv;
+  f.part = part;
+  f.R = rows_of(dims);
+  f.H = dims->hidden_dim;
+  f.Vd = dims->v_draft;
+  f.Vt = dims->v_target;
+  f.nslice_t = vsd::lm_nslice(dims->v_target);
+  f.nslice_d = vsd::lm_nslice(dims->v_draft);
+  f.sample = sampling ? 1 : 0;
+  f.inv_tq = 1.0f / params->temp_draft;
+  f.inv_tp = 1.0f / params->temp_target;
+  f.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  f.k1 = (uint32_t)(seed >> 32);
+  f.offset = offset;
+  e = vsd::launch_lm_fwd(f, s);
+  if (e != hipSuccess) return hip_fail(e, "k_lm_fwd launch");
+  vsd::LmCombineArgs c{};
+  c.part = part;
+  c.Hd = draft->hidden;
+  c.Ht = target->hidden;
+  c.Wd = draft->weight;
+  c.Wt = target->weight;
+  c.d2t = d2t;
+  c.depth = valid_depth;
+  for (int k = 0; k < 3; ++k) {
+    c.tok_in[k] = sampling ? nullptr : tok_in[k];
+    c.tok_out[k] = sampling ? tok_out[k] : nullptr;
+  }
+  c.lse_q = out->lse_draft;
+  c.lse_p = out->lse_target;
+  c.la = la;
+  c.lq = lq;
+  c.err = out->device_error;
+  c.R = f.R;
+  c.L = dims->L;
+  c.H = f.H;
+  c.Vd = f.Vd;
+  c.Vt = f.Vt;
+  c.nslice_t = f.nslice_t;
+  c.nslice_d = f.nslice_d;
+  c.inv_tq = f.inv_tq;
+  c.inv_tp = f.inv_tp;
+  e = vsd::launch_lm_combine(c, s);
+  if (e != hipSuccess) return hip_fail(e, "k_lm_combine launch");
+  return VSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -197,6 +317,8 @@ vsd_status vsd_sample_paths(const vsd_dims* dims, const vsd_src* draft, const vs
                             void* hip_stream) {
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
+  if (is_fused(dims))
+    return fail(VSD_ERR_UNSUPPORTED, "the fused LM head needs a workspace: use vsd_sample_score_paths");
   if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
   if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
   if ((st = check_map(dims, d2t)) != VSD_OK) return st;
@@ -239,8 +361,7 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
   if ((st = check_params(params)) != VSD_OK) return st;
-  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
-  if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
+  if ((st = check_sources(dims, draft, target)) != VSD_OK) return st;
   if ((st = check_map(dims, d2t)) != VSD_OK) return st;
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
@@ -252,6 +373,14 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   float* lq = out->log_q_tok != nullptr ? out->log_q_tok : reinterpret_cast<float*>(ws + wl.lq);
   float* loss_pos = out->loss_pos != nullptr ? out->loss_pos : reinterpret_cast<float*>(ws + wl.loss);
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+  if (is_fused(dims)) {
+    const int32_t* const tin[3] = {tok_draft, tok_target, tok_greedy};
+    st = lm_forward(dims, params, draft, target, d2t, valid_depth, 0, 0, tin, nullptr, out, ws, wl, la, lq, s);
+    if (st != VSD_OK) return st;
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s)) != VSD_OK) return st;
+    return ok();
+  }
 
   vsd::ScoreRowArgs ra{};
   ra.X = draft->logits;
@@ -290,8 +419,7 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
   if ((st = check_params(params)) != VSD_OK) return st;
-  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
-  if ((st = check_logits(dims, target, "target", dims->ld_target, dims->v_target)) != VSD_OK) return st;
+  if ((st = check_sources(dims, draft, target)) != VSD_OK) return st;
   if ((st = check_map(dims, d2t)) != VSD_OK) return st;
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
@@ -303,6 +431,15 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   float* lq = out->log_q_tok != nullptr ? out->log_q_tok : reinterpret_cast<float*>(ws + wl.lq);
   float* loss_pos = out->loss_pos != nullptr ? out->loss_pos : reinterpret_cast<float*>(ws + wl.loss);
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+  if (is_fused(dims)) {
+    int32_t* const tout[3] = {tok_draft, tok_target, tok_greedy};
+    st = lm_forward(dims, params, draft, target, d2t, valid_depth, seed, offset, nullptr, tout, out, ws, wl, la,
+                    lq, s);
+    if (st != VSD_OK) return st;
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s)) != VSD_OK) return st;
+    return ok();
+  }
 
   vsd::SampleArgs a{};
   a.X = draft->logits;
@@ -347,13 +484,47 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
   if ((st = check_params(params)) != VSD_OK) return st;
-  if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) return st;
+  if (is_fused(dims)) {
+    if ((st = check_fused_src(draft, "draft")) != VSD_OK) return st;
+  } else if ((st = check_logits(dims, draft, "draft", dims->ld_draft, dims->v_draft)) != VSD_OK) {
+    return st;
+  }
   if (lse_draft == nullptr || tok_draft == nullptr || tok_target == nullptr || coef_a == nullptr ||
       coef_b == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "lse_draft, tokens and coefficients are required");
   if (grad == nullptr || grad->grad_logits == nullptr) return fail(VSD_ERR_NULL_POINTER, "grad->grad_logits is NULL");
   if (!aligned16(grad->grad_logits)) return fail(VSD_ERR_MISALIGNED, "grad_logits not 16-byte aligned");
   if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+
+  if (is_fused(dims)) {
+    // grad_logits receives g (bf16, stride ld_draft), then dH = g W_d
+    if (dims->ld_draft < dims->v_draft || (dims->ld_draft * 2) % 16 != 0)
+      return fail(VSD_ERR_INVALID_SHAPE, "fused: ld_draft=%lld must be >= v_draft and a multiple of 8",
+                  (long long)dims->ld_draft);
+    if (grad->grad_hidden == nullptr) return fail(VSD_ERR_NULL_POINTER, "fused: grad->grad_hidden is NULL");
+    if (!aligned16(grad->grad_hidden)) return fail(VSD_ERR_MISALIGNED, "grad_hidden not 16-byte aligned");
+    if (grad->grad_weight != nullptr)
+      return fail(VSD_ERR_UNSUPPORTED, "fused: the weight gradient is not computed (pass grad_weight = NULL)");
+    vsd::LmBwdArgs b{};
+    b.Hd = draft->hidden;
+    b.Wd = draft->weight;
+    b.G = grad->grad_logits;
+    b.dH = grad->grad_hidden;
+    b.lse_q = lse_draft;
+    b.tok_d = tok_draft;
+    b.tok_t = tok_target;
+    b.coef_a = coef_a;
+    b.coef_b = coef_b;
+    b.R = rows_of(dims);
+    b.ldg = dims->ld_draft;
+    b.H = dims->hidden_dim;
+    b.Vd = dims->v_draft;
+    b.inv_tq = 1.0f / params->temp_draft;
+    b.scale = params->loss_scale;
+    hipError_t e = vsd::launch_lm_bwd(b, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "k_lm_bwd launch");
+    return ok();
+  }
 
   vsd::BwdArgs a{};
   a.X = draft->logits;

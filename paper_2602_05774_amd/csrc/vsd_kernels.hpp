@@ -79,6 +79,92 @@ struct BwdArgs {
   float inv_tq, scale;
 };
 
+// ------------------------------------------------ fused LM-head variant ---
+constexpr int kLmTile = 128;           // rows and vocabulary columns per logit tile
+constexpr int kLmTilesPerSlice = 32;   // vocabulary tiles one forward workgroup walks
+
+// Vocabulary slices of a V-column pass (a function of V only, so the float
+// outputs of a row do not depend on the batch size).
+inline int lm_nslice(int V) {
+  const int tiles = (V + kLmTile - 1) / kLmTile;
+  return (tiles + kLmTilesPerSlice - 1) / kLmTilesPerSlice;
+}
+
+// One slice's running state of one row (32 bytes).
+struct LmPartial {
+  float mraw, mc, s;   // log-sum-exp in shifted form
+  float key;           // best Gumbel key
+  int32_t idx;         // its draft index
+  float gval;          // greedy maximum (target pass)
+  int32_t gidx;
+  int32_t pad;
+};
+
+struct LmFwdArgs {
+  const void* Hd;            // [R, H] bf16
+  const void* Ht;            // [R, H] bf16
+  const void* Wd;            // [Vd, H] bf16
+  const void* Wt;            // [Vt, H] bf16
+  const int32_t* inv;        // [Vt] draft index of each target column (-1: none); null = identity
+  LmPartial* part;           // [R, nslice_t + nslice_d], target slices first
+  int64_t R;
+  int32_t H, Vd, Vt;
+  int32_t nslice_t, nslice_d;
+  int32_t sample;            // 0: log-sum-exp only (scoring given tokens)
+  float inv_tq, inv_tp;
+  uint32_t k0, k1, offset;
+};
+
+struct LmCombineArgs {
+  const LmPartial* part;
+  const void* Hd;
+  const void* Ht;
+  const void* Wd;
+  const void* Wt;
+  const int32_t* d2t;
+  const int32_t* depth;
+  const int32_t* tok_in[3];  // scoring: given tokens; sampling: null
+  int32_t* tok_out[3];       // sampling: drawn tokens
+  float* lse_q;
+  float* lse_p;              // optional
+  float* la;                 // [R,3]
+  float* lq;                 // [R,3]
+  int32_t* err;
+  int64_t R;
+  int32_t L, H, Vd, Vt;
+  int32_t nslice_t, nslice_d;
+  float inv_tq, inv_tp;
+};
+
+struct LmBwdArgs {
+  const void* Hd;
+  const void* Wd;
+  void* G;                   // [R, ldg] bf16: gradient w.r.t. the draft logits
+  void* dH;                  // [R, H] bf16
+  const float* lse_q;
+  const int32_t* tok_d;
+  const int32_t* tok_t;
+  const float* coef_a;
+  const float* coef_b;
+  int64_t R, ldg;
+  int32_t H, Vd;
+  float inv_tq, scale;
+};
+
+struct LmGemmNNArgs {
+  const void* A;             // [M, K] bf16
+  const void* B;             // [K, N] bf16
+  void* C;                   // [M, N] bf16
+  int64_t M, lda;
+  int64_t ldb, ldc;
+  int32_t N, K;
+};
+
+hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32_t* err, hipStream_t s);
+hipError_t launch_lm_fwd(const LmFwdArgs& a, hipStream_t s);
+hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s);
+hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
+
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);

@@ -7,6 +7,10 @@ of the computation runs in libvsd.so on the current HIP stream.
 Layout (see include/vsd.h): row r = ((b*T + t)*N + s)*L + (i-1); logits are
 [R, ld] with ld >= v and 16-byte rows; tokens, per-row outputs [R]; per-path
 outputs [B*T*N]; per-position outputs [B*T].
+
+Wherever a logit tensor is accepted, an LmHead(hidden [R, H], weight [V, H])
+may be given instead (both models alike): the fused LM-head variant, whose
+logits hidden @ weight.T are computed inside the kernels and never stored.
 """
 import ctypes
 from dataclasses import dataclass
@@ -18,8 +22,8 @@ from . import _lib
 from ._lib import (VSD_BF16, VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_F32, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR,
                    VSD_GRAD_BASIC, VsdError)
 
-__all__ = ["Problem", "Params", "SampleResult", "ScoreResult", "sample_paths", "score_paths", "sample_score_paths",
-           "weighted_loss_bwd", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
+__all__ = ["Problem", "Params", "LmHead", "LmHeadGrad", "SampleResult", "ScoreResult", "sample_paths",
+           "score_paths", "sample_score_paths", "weighted_loss_bwd", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
            "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]
 
 
@@ -54,6 +58,22 @@ class Params:
     def c(self):
         return _lib.VsdParams(self.temp_draft, self.temp_target, self.w_base, self.car_tau,
                               self.mode, self.car_input, self.loss_scale)
+
+
+@dataclass(frozen=True)
+class LmHead:
+    """A fused LM-head source: logits = hidden @ weight.T (bf16, contiguous)."""
+    hidden: torch.Tensor  # [R, H]
+    weight: torch.Tensor  # [V, H]
+
+    @property
+    def device(self):
+        return self.hidden.device
+
+
+class LmHeadGrad(NamedTuple):
+    grad_hidden: torch.Tensor  # [R, H] bf16
+    grad_logits: torch.Tensor  # [R, ld] bf16 (columns [0, v_draft) written)
 
 
 class SampleResult(NamedTuple):
@@ -105,6 +125,27 @@ def _check_logits(name, t, prob, v):
         raise ValueError(f"{name} must be [R={prob.R}, ld>={v}] with unit column stride, got {tuple(t.shape)}")
 
 
+def _check_head(name, src, prob, v):
+    h, w = src.hidden, src.weight
+    for nm, t in (("hidden", h), ("weight", w)):
+        if not t.is_cuda or t.dtype != torch.bfloat16 or not t.is_contiguous() or t.dim() != 2:
+            raise ValueError(f"{name}.{nm} must be a contiguous 2-D bfloat16 device tensor")
+    if h.shape[0] != prob.R or w.shape[0] != v or h.shape[1] != w.shape[1]:
+        raise ValueError(f"{name}: hidden must be [R={prob.R}, H] and weight [{v}, H], got "
+                         f"{tuple(h.shape)} and {tuple(w.shape)}")
+
+
+def _check_src(name, t, prob, v):
+    if isinstance(t, LmHead):
+        _check_head(name, t, prob, v)
+    else:
+        _check_logits(name, t, prob, v)
+
+
+def _ld8(v):
+    return (v + 7) // 8 * 8
+
+
 def _check_i32(name, t, numel):
     if t is None:
         return
@@ -112,7 +153,15 @@ def _check_i32(name, t, numel):
         raise ValueError(f"{name} must be a contiguous int32 device tensor of {numel} elements")
 
 
-def _dims(prob, X, Y):
+def _dims(prob, X, Y, ld_grad=None):
+    if isinstance(X, LmHead):
+        H = X.hidden.shape[1]
+        if Y is not None and (not isinstance(Y, LmHead) or Y.hidden.shape[1] != H):
+            raise ValueError("draft and target must both be LmHead sources with the same hidden size")
+        return _lib.VsdDims(prob.B, prob.T, prob.N, prob.L, prob.v_draft, prob.v_target, VSD_BF16, H,
+                            ld_grad if ld_grad is not None else _ld8(prob.v_draft), prob.v_target)
+    if isinstance(Y, LmHead):
+        raise ValueError("draft and target must both be logits or both be LmHead sources")
     dt = _dtype_code(X)
     if Y is not None and Y.dtype != X.dtype:
         raise ValueError("draft and target logits must share a dtype")
@@ -121,14 +170,19 @@ def _dims(prob, X, Y):
 
 
 def _src(t):
+    if isinstance(t, LmHead):
+        return _lib.VsdSrc(None, t.hidden.data_ptr(), t.weight.data_ptr())
     return _lib.VsdSrc(t.data_ptr(), None, None)
 
 
 def sample_paths(prob, X, Y, d2t=None, valid_depth=None, temp_draft=1.0, temp_target=1.0,
                  seed=0, offset=0, device_error=None):
     """E-step draws: tokens of the draft proposal, target correction and greedy
-    reference families ([R] int32 each, -1 on masked rows)."""
+    reference families ([R] int32 each, -1 on masked rows).  Materialised
+    logits only: the fused LM head draws through sample_score_paths."""
     lib = _lib.load()
+    if isinstance(X, LmHead) or isinstance(Y, LmHead):
+        raise ValueError("sample_paths takes logits; draw from LmHead sources with sample_score_paths")
     _check_logits("X", X, prob, prob.v_draft)
     _check_logits("Y", Y, prob, prob.v_target)
     _check_i32("d2t", d2t, prob.v_draft)
@@ -145,13 +199,21 @@ def sample_paths(prob, X, Y, d2t=None, valid_depth=None, temp_draft=1.0, temp_ta
     return SampleResult(toks[0], toks[1], toks[2], device_error)
 
 
-def score_workspace_bytes(prob, dtype=torch.bfloat16):
+def score_workspace_bytes(prob, dtype=torch.bfloat16, hidden_dim=0):
+    """Workspace bytes of score_paths / sample_score_paths (hidden_dim > 0:
+    the fused LM-head variant)."""
     lib = _lib.load()
     dims = _lib.VsdDims(prob.B, prob.T, prob.N, prob.L, prob.v_draft, prob.v_target,
-                        VSD_BF16 if dtype == torch.bfloat16 else VSD_F32, 0, prob.v_draft, prob.v_target)
+                        VSD_BF16 if dtype == torch.bfloat16 else VSD_F32, hidden_dim, prob.v_draft, prob.v_target)
     n = ctypes.c_size_t(0)
     _lib.check(lib.vsd_score_workspace_bytes(ctypes.byref(dims), ctypes.byref(n)))
     return n.value
+
+
+def _workspace_bytes(prob, X):
+    if isinstance(X, LmHead):
+        return score_workspace_bytes(prob, torch.bfloat16, X.hidden.shape[1])
+    return score_workspace_bytes(prob, X.dtype)
 
 
 def alloc_score_outputs(prob, device, full=True):
@@ -173,8 +235,8 @@ def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None,
                 out: Optional[ScoreResult] = None, workspace=None):
     """Path scoring, oracle gate, ARW/CAR weights, loss and per-row coefficients."""
     lib = _lib.load()
-    _check_logits("X", X, prob, prob.v_draft)
-    _check_logits("Y", Y, prob, prob.v_target)
+    _check_src("X", X, prob, prob.v_draft)
+    _check_src("Y", Y, prob, prob.v_target)
     for name, t in (("tok_draft", tok_draft), ("tok_target", tok_target), ("tok_greedy", tok_greedy)):
         _check_i32(name, t, prob.R)
     _check_i32("d2t", d2t, prob.v_draft)
@@ -182,7 +244,7 @@ def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None,
     dev = X.device
     if out is None:
         out = alloc_score_outputs(prob, dev)
-    nbytes = score_workspace_bytes(prob, X.dtype)
+    nbytes = _workspace_bytes(prob, X)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     dims = _dims(prob, X, Y)
@@ -202,8 +264,8 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
     sampling kernel also forms the row statistics).  Returns (SampleResult,
     ScoreResult); the sample's device_error is the score's."""
     lib = _lib.load()
-    _check_logits("X", X, prob, prob.v_draft)
-    _check_logits("Y", Y, prob, prob.v_target)
+    _check_src("X", X, prob, prob.v_draft)
+    _check_src("Y", Y, prob, prob.v_target)
     _check_i32("d2t", d2t, prob.v_draft)
     _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
     dev = X.device
@@ -213,7 +275,7 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
         tokens = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
     for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), tokens):
         _check_i32(name, t, prob.R)
-    nbytes = score_workspace_bytes(prob, X.dtype)
+    nbytes = _workspace_bytes(prob, X)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     dims = _dims(prob, X, Y)
@@ -230,19 +292,36 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
 def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,
                       grad=None, device_error=None):
     """Gradient of loss_scale * sum_x L_x with respect to the draft logits
-    (same shape, stride and dtype as X)."""
+    (same shape, stride and dtype as X).  For an LmHead source, returns
+    LmHeadGrad(grad_hidden [R, H], grad_logits [R, ld]): the logit gradient is
+    written in bf16 and then contracted with the weight; `grad`, if given, is
+    such a pair to fill."""
     lib = _lib.load()
-    _check_logits("X", X, prob, prob.v_draft)
+    _check_src("X", X, prob, prob.v_draft)
     dev = X.device
-    if grad is None:
-        grad = torch.empty_like(X)
-    if grad.shape != X.shape or grad.stride() != X.stride() or grad.dtype != X.dtype:
-        raise ValueError("grad must match X in shape, stride and dtype")
     if device_error is None:
         device_error = torch.zeros(1, dtype=torch.int32, device=dev)
-    dims = _dims(prob, X, None)
     pr = params.c()
-    g = _lib.VsdGrad(grad.data_ptr(), None, None)
+    if isinstance(X, LmHead):
+        H = X.hidden.shape[1]
+        if grad is None:
+            grad = LmHeadGrad(torch.empty(prob.R, H, dtype=torch.bfloat16, device=dev),
+                              torch.empty(prob.R, _ld8(prob.v_draft), dtype=torch.bfloat16, device=dev))
+        gh, gl = grad
+        if gh.shape != (prob.R, H) or gh.dtype != torch.bfloat16 or not gh.is_contiguous():
+            raise ValueError(f"grad_hidden must be a contiguous bfloat16 [{prob.R}, {H}] tensor")
+        if (gl.dim() != 2 or gl.shape[0] != prob.R or gl.shape[1] < prob.v_draft or gl.stride(1) != 1
+                or gl.dtype != torch.bfloat16):
+            raise ValueError(f"grad_logits must be a bfloat16 [{prob.R}, ld>={prob.v_draft}] tensor")
+        dims = _dims(prob, X, None, ld_grad=gl.stride(0))
+        g = _lib.VsdGrad(gl.data_ptr(), gh.data_ptr(), None)
+    else:
+        if grad is None:
+            grad = torch.empty_like(X)
+        if grad.shape != X.shape or grad.stride() != X.stride() or grad.dtype != X.dtype:
+            raise ValueError("grad must match X in shape, stride and dtype")
+        dims = _dims(prob, X, None)
+        g = _lib.VsdGrad(grad.data_ptr(), None, None)
     _lib.check(lib.vsd_weighted_loss_bwd(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
                                          _ptr(lse_draft), _ptr(tok_draft), _ptr(tok_target), _ptr(coef_a),
                                          _ptr(coef_b), ctypes.byref(g), _ptr(device_error), _stream(dev)))

@@ -32,6 +32,7 @@ class Config:
     mapped: bool = False
     ragged: bool = False
     hidden: int = 0
+    w_std: float = 0.02   # fused recipe: LM-head weight standard deviation
     seed: int = 0         # generator seed (inputs)
     philox_seed: int = 0  # sampler seed
     philox_offset: int = 0
@@ -70,7 +71,12 @@ def get_config(name):
 
 
 def scaled(base_name, **overrides):
-    """A config of the same recipe with some fields replaced (smaller B, T ...)."""
+    """A config of the same recipe with some fields replaced (smaller B, T ...).
+
+    For the fused recipe a smaller hidden size keeps the logit spread of the
+    full shape (std 0.02 * sqrt(4096) = 1.28) unless w_std is given."""
     base = CONFIGS[base_name]
     overrides.setdefault("name", base.name + "-scaled")
+    if base.kind == "fused" and "hidden" in overrides and "w_std" not in overrides:
+        overrides["w_std"] = base.w_std * (base.hidden / overrides["hidden"]) ** 0.5
     return replace(base, **overrides)

@@ -84,8 +84,8 @@ def make_inputs(cfg, device="cuda", chunk_rows=8192):
         bf = torch.bfloat16
         out["Hd"] = torch.randn(R, H, generator=gen, device=dev, dtype=torch.float32).to(bf)
         out["Ht"] = torch.randn(R, H, generator=gen, device=dev, dtype=torch.float32).to(bf)
-        out["Wd"] = (0.02 * torch.randn(Vd, H, generator=gen, device=dev)).to(bf)
-        out["Wt"] = (0.02 * torch.randn(Vt, H, generator=gen, device=dev)).to(bf)
+        out["Wd"] = (cfg.w_std * torch.randn(Vd, H, generator=gen, device=dev)).to(bf)
+        out["Wt"] = (cfg.w_std * torch.randn(Vt, H, generator=gen, device=dev)).to(bf)
         return out
 
     X = torch.empty(R, cfg.ld(Vd), dtype=_dtype(cfg), device=dev)

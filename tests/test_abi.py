@@ -159,3 +159,47 @@ def test_fused_sample_score_rejects_bad_arguments(lib):
     assert call(dims=_dims(v_target=2000, ld_target=2000)) == 5
     assert call(ws_bytes=16) == 7
     assert call(out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=None, device_error=FAKE)) == 1
+
+
+def test_fused_lm_head_validation(lib):
+    """hidden_dim > 0 selects the fused LM head: shape, dtype, source and
+    gradient-buffer checks, all before any launch."""
+    head = _lib.VsdSrc(None, FAKE, FAKE)
+    out = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    fdims = lambda **kw: _dims(**{**dict(dtype=_lib.VSD_BF16, hidden_dim=128, ld_draft=1000), **kw})
+
+    def score(dims, d=head, t=head, ws_bytes=1 << 30):
+        return lib.vsd_score_paths(ctypes.byref(dims), ctypes.byref(_params()), ctypes.byref(d), ctypes.byref(t),
+                                   None, None, FAKE, FAKE, FAKE, ctypes.byref(out), FAKE, ws_bytes, None)
+
+    def sample_score(dims, d=head, t=head):
+        return lib.vsd_sample_score_paths(ctypes.byref(dims), ctypes.byref(_params()), ctypes.byref(d),
+                                          ctypes.byref(t), None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(out),
+                                          FAKE, 1 << 30, None)
+
+    assert score(fdims(hidden_dim=100)) == 2          # not a multiple of 64
+    assert score(fdims(hidden_dim=-64)) == 2
+    assert score(fdims(dtype=_lib.VSD_F32)) == 6      # bf16 only
+    assert score(fdims(), d=_lib.VsdSrc(FAKE, None, None)) == 6   # logits with hidden_dim > 0
+    assert score(fdims(), t=_lib.VsdSrc(None, FAKE, None)) == 1   # weight missing
+    assert score(fdims(), d=_lib.VsdSrc(None, FAKE + 2, FAKE)) == 4
+    assert sample_score(fdims(), t=_lib.VsdSrc(None, None, FAKE)) == 1
+    assert sample_score(fdims(v_target=2000)) == 5    # map required
+    # vsd_sample_paths has no workspace: fused dims are refused
+    assert _sample(lib, fdims(), xsrc=head) == 6
+    # workspace: the fused layout adds the slice partials
+    plain, fused = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), ctypes.byref(plain)) == 0
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(fdims()), ctypes.byref(fused)) == 0
+    assert fused.value >= plain.value + 24 * 32 + 1000 * 4
+    assert score(fdims(), ws_bytes=fused.value - 1) == 7
+    # backward: grad_hidden required, grad_weight unsupported, ld_draft checked
+    def bwd(dims, grad):
+        return lib.vsd_weighted_loss_bwd(ctypes.byref(dims), ctypes.byref(_params()), ctypes.byref(head), FAKE,
+                                         FAKE, FAKE, FAKE, FAKE, ctypes.byref(grad), FAKE, None)
+    assert bwd(fdims(), _lib.VsdGrad(FAKE, None, None)) == 1
+    assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE + 8, None)) == 4
+    assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE, FAKE)) == 6
+    assert bwd(fdims(ld_draft=999), _lib.VsdGrad(FAKE, FAKE, None)) == 2
+    assert bwd(fdims(ld_draft=1004), _lib.VsdGrad(FAKE, FAKE, None)) == 2   # 2008 bytes: not 16-B rows
+    assert bwd(fdims(), _lib.VsdGrad(None, FAKE, None)) == 1

@@ -1,0 +1,231 @@
+"""GPU parity of the fused LM-head variant (hidden states and LM-head weights
+in, logits formed on the matrix cores and never stored) against the oracle's
+LM head (exact float64 logits handed to the per-position oracle).
+
+* Draws: the kernels' fp32 logits differ from the exact ones by the products'
+  rounding, so a token must equal the oracle's wherever the oracle's two best
+  keys (or greedy values) of the row are more than GAP apart; closer rows are
+  counted, and their token may differ.
+* Scoring and backward: run on the oracle's tokens (vsd_score_paths with
+  given tokens, then the backward) and compared under the materialised path's
+  bars; the hidden-state gradient to 1e-2 relative Frobenius error and 2e-3
+  absolute.  The one-pass draw-and-score outputs are also compared on every
+  position whose tokens all agree.
+* Sizes: a small batch checked on every position (two row tiles, the last
+  ragged; vocabularies that span several slices and end mid-tile), edge cases
+  (identity map, ragged depth, temperature, one k-step, odd vocabulary), and
+  the full 49 152 x 4096 shape on sampled positions.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_05774_amd as vsd
+from oracle import lmhead
+from synth import CONFIGS, make_inputs, scaled
+from tests.gpu_common import SENTINEL, compare, log, params_of, problem_of
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+GAP = 1e-4
+
+
+def _heads(inp):
+    return vsd.LmHead(inp["Hd"], inp["Wd"]), vsd.LmHead(inp["Ht"], inp["Wt"])
+
+
+def _bwd(prob, params, Xs, sc, toks):
+    gl = torch.full((prob.R, (prob.v_draft + 7) // 8 * 8), SENTINEL, dtype=torch.bfloat16, device=DEV)
+    gh = torch.empty(prob.R, Xs.hidden.shape[1], dtype=torch.bfloat16, device=DEV)
+    vsd.weighted_loss_bwd(prob, params, Xs, sc.lse_draft, toks[0], toks[1], sc.coef_a, sc.coef_b,
+                          grad=vsd.LmHeadGrad(gh, gl))
+    return gh, gl
+
+
+def _rows_of(cfg, positions):
+    return (np.asarray(positions)[:, None] * cfg.N * cfg.L + np.arange(cfg.N * cfg.L)[None]).reshape(-1)
+
+
+def _oracle(cfg, inp, positions, params, tokens=None):
+    rows = _rows_of(cfg, positions)
+    idx = torch.as_tensor(rows, device=DEV)
+    f32 = lambda t: t.float().cpu().numpy()
+    Hd, Ht = f32(inp["Hd"].index_select(0, idx)), f32(inp["Ht"].index_select(0, idx))
+    Wd, Wt = f32(inp["Wd"]), f32(inp["Wt"])
+    d2t = None if inp["d2t"] is None else inp["d2t"].cpu().numpy()
+    depth = None
+    if inp["valid_depth"] is not None:
+        depth = inp["valid_depth"].reshape(-1, cfg.N).cpu().numpy()[np.asarray(positions)]
+    p = dict(temp_draft=params.temp_draft, temp_target=params.temp_target, w_base=params.w_base,
+             car_tau=params.car_tau, mode=params.mode, car_input=params.car_input, loss_scale=params.loss_scale)
+    ora = lmhead.run_positions(Hd, Ht, Wd, Wt, d2t, depth, list(positions), cfg.N, cfg.L, p,
+                               seed=cfg.philox_seed, offset=cfg.philox_offset, tokens=tokens)
+    gaps = lmhead.key_gaps(ora["X"], ora["Y"], d2t, rows, params.temp_draft, params.temp_target,
+                           cfg.philox_seed, cfg.philox_offset)
+    return rows, ora, gaps
+
+
+def check_lmhead(cfg, inp, positions, params=None, label=""):
+    """Draw, score and backward on the GPU; compare with the oracle on
+    `positions`.  Returns a summary."""
+    prob = problem_of(cfg)
+    params = params or params_of(cfg)
+    Xs, Ys = _heads(inp)
+    log(f"[{label}] fused LM head: R={prob.R} H={cfg.hidden} Vd={cfg.v_draft} Vt={cfg.v_target}")
+    smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, inp["d2t"], inp["valid_depth"], cfg.philox_seed,
+                                     cfg.philox_offset)
+    toks = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 0
+    rows, ora, gaps = _oracle(cfg, inp, positions, params)
+    # 1. draws: equal wherever the oracle's top-two gap exceeds GAP
+    live = ora["tok_draft"] >= 0
+    near = {}
+    differs = np.zeros(len(rows), dtype=bool)
+    for name, t, gap in zip(("tok_draft", "tok_target", "tok_greedy"), toks, gaps):
+        got = t.cpu().numpy()[rows]
+        bad = got != ora[name]
+        sure = live & (gap > GAP)
+        assert not np.any(bad & sure), (f"{label} {name}: {int(np.sum(bad & sure))} decided mismatches, first row "
+                                        f"{rows[np.argmax(bad & sure)]}")
+        assert np.all(got[~live] == -1)
+        near[name] = (int(np.sum(live & ~sure)), int(np.sum(bad)))
+        differs |= bad
+    log(f"[{label}] near-tie rows / mismatches per family: {near}")
+    # 2. one-pass outputs on positions whose tokens all agree
+    per = cfg.N * cfg.L
+    agree = [p for k, p in enumerate(positions) if not differs[k * per:(k + 1) * per].any()]
+    gh, gl = _bwd(prob, params, Xs, sc, toks)
+    torch.cuda.synchronize()
+    if agree:
+        keep = np.concatenate([np.arange(k * per, (k + 1) * per) for k, p in enumerate(positions) if p in agree])
+        sub = {k: (v[keep] if isinstance(v, np.ndarray) and v.shape[:1] == (len(rows),) else v)
+               for k, v in ora.items()}
+        pk = np.array([k for k, p in enumerate(positions) if p in agree])
+        for k in ("loss_pos", "W"):
+            sub[k] = ora[k][pk]
+        paths_keep = np.concatenate([np.arange(k * cfg.N, (k + 1) * cfg.N) for k in pk])
+        sub["exp_accept_len"] = ora["exp_accept_len"][paths_keep]
+        compare(cfg, dict(tokens=toks, score=sc, grad=gl), rows[keep], sub, agree, label=label + " one-pass")
+    # 3. scoring and backward on the oracle's tokens
+    full_tok = [t.clone() for t in toks]
+    idx = torch.as_tensor(rows, device=DEV)
+    for t, name in zip(full_tok, ("tok_draft", "tok_target", "tok_greedy")):
+        t.index_copy_(0, idx, torch.as_tensor(ora[name].astype(np.int32), device=DEV))
+    sc2 = vsd.score_paths(prob, params, Xs, Ys, *full_tok, inp["d2t"], inp["valid_depth"])
+    gh2, gl2 = _bwd(prob, params, Xs, sc2, full_tok)
+    torch.cuda.synchronize()
+    assert int(sc2.device_error.item()) == 0
+    summary = compare(cfg, dict(tokens=full_tok, score=sc2, grad=gl2), rows, ora, positions, label=label)
+    # padding columns of the logit-gradient buffer are never written
+    pad = gl2[:, cfg.v_draft:]
+    assert pad.numel() == 0 or bool(torch.all(pad == SENTINEL))
+    # 4. hidden-state gradient
+    got = gh2.index_select(0, idx).float().cpu().numpy()
+    ref = ora["grad_hidden"]
+    err = np.abs(got - ref)
+    keep_rows = np.ones(len(rows), dtype=bool)
+    for p in summary["near_tie_positions"]:
+        keep_rows[p * per:(p + 1) * per] = False
+    assert np.all(err[keep_rows] <= 2e-3), f"{label} grad_hidden max abs err {err[keep_rows].max()}"
+    fro = np.linalg.norm((got - ref)[keep_rows]) / max(np.linalg.norm(ref[keep_rows]), 1e-30)
+    assert fro <= 1e-2, f"{label} grad_hidden relative Frobenius error {fro}"
+    summary["grad_hidden_fro"] = float(fro)
+    summary["near"] = near
+    log(f"[{label}] ok: worst {summary['worst']}, dH rel fro {fro:.2e}")
+    return summary
+
+
+SMALL = scaled("C5", B=2, T=8, N=4, L=3, v_draft=4500, v_target=9000, hidden=256)
+
+
+def test_small_batch_every_position():
+    cfg = SMALL
+    inp = make_inputs(cfg, DEV)
+    check_lmhead(cfg, inp, list(range(cfg.P)), label="C5s")
+
+
+@pytest.mark.parametrize("case", ["identity", "ragged_temp", "one_kstep_odd_vocab"])
+def test_edge_cases(case):
+    if case == "identity":
+        cfg = scaled("C5", B=1, T=4, N=4, L=2, v_draft=3000, v_target=3000, hidden=128, mapped=False)
+    elif case == "ragged_temp":
+        cfg = scaled("C5", B=2, T=4, N=8, L=4, v_draft=2000, v_target=7000, hidden=192, ragged=True,
+                     temp_draft=0.5, temp_target=1.3, seed=51)
+    else:
+        cfg = scaled("C5", B=1, T=3, N=3, L=3, v_draft=1001, v_target=2003, hidden=64, seed=52)
+    inp = make_inputs(cfg, DEV)
+    check_lmhead(cfg, inp, list(range(cfg.P)), label=f"C5 {case}")
+
+
+def test_modes_and_loss_scale():
+    cfg = scaled("C5", B=1, T=4, N=4, L=3, v_draft=1500, v_target=6000, hidden=128, seed=53)
+    inp = make_inputs(cfg, DEV)
+    for mode in (vsd.VSD_GRAD_BASIC, vsd.VSD_GRAD_ARW):
+        check_lmhead(cfg, inp, list(range(cfg.P)), params_of(cfg, mode=mode, loss_scale=0.25),
+                     label=f"C5 mode {mode}")
+
+
+def test_deterministic_and_matches_materialised_logits_path():
+    """Two runs agree bit for bit; the fused tokens equal the materialised
+    path's tokens on the kernels' own rounding-free cases: logits that are
+    exact in bf16 (hidden one-hot rows pick bf16 weight entries)."""
+    cfg = scaled("C5", B=1, T=2, N=4, L=2, v_draft=700, v_target=1300, hidden=64, seed=54)
+    inp = make_inputs(cfg, DEV)
+    prob, params = problem_of(cfg), params_of(cfg)
+    # one-hot hidden rows: logits = single weight entries, exact in fp32
+    k = torch.arange(prob.R, device=DEV) % cfg.hidden
+    for name in ("Hd", "Ht"):
+        h = torch.zeros(prob.R, cfg.hidden, dtype=torch.bfloat16, device=DEV)
+        h[torch.arange(prob.R, device=DEV), k] = 4.0
+        inp[name] = h
+    Xs, Ys = _heads(inp)
+    outs = []
+    for _ in range(2):
+        smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, inp["d2t"], None, 3, 9)
+        torch.cuda.synchronize()
+        outs.append((smp, sc))
+    for a, b in zip(outs[0][0][:3], outs[1][0][:3]):
+        assert torch.equal(a, b)
+    for name in ("lse_draft", "coef_a", "coef_b", "log_alpha"):
+        assert torch.equal(getattr(outs[0][1], name), getattr(outs[1][1], name))
+    X = (inp["Hd"].float() @ inp["Wd"].float().T).contiguous()
+    Y = (inp["Ht"].float() @ inp["Wt"].float().T)
+    Yp = torch.zeros(prob.R, (cfg.v_target + 3) // 4 * 4, device=DEV)
+    Yp[:, :cfg.v_target] = Y
+    Xp = torch.zeros(prob.R, (cfg.v_draft + 3) // 4 * 4, device=DEV)
+    Xp[:, :cfg.v_draft] = X
+    ref = vsd.sample_paths(prob, Xp, Yp, inp["d2t"], None, 1.0, 1.0, 3, 9)
+    torch.cuda.synchronize()
+    for a, b in zip(outs[0][0][:3], ref[:3]):
+        assert torch.equal(a, b)
+
+
+def test_device_errors_are_reported():
+    cfg = scaled("C5", B=1, T=2, N=2, L=2, v_draft=500, v_target=900, hidden=64, seed=55)
+    inp = make_inputs(cfg, DEV)
+    prob, params = problem_of(cfg), params_of(cfg)
+    Xs, Ys = _heads(inp)
+    toks = [torch.zeros(prob.R, dtype=torch.int32, device=DEV) for _ in range(3)]
+    toks[1][3] = cfg.v_draft  # out of range
+    sc = vsd.score_paths(prob, params, Xs, Ys, *toks, inp["d2t"], None)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 1
+    bad_map = inp["d2t"].clone()
+    bad_map[5] = cfg.v_target + 7
+    smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, bad_map, None, 0, 0)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 2
+    depth = torch.full((cfg.B, cfg.T, cfg.N), 1, dtype=torch.int32, device=DEV)
+    depth[0, 1, 1] = cfg.L + 1
+    smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, inp["d2t"], depth, 0, 0)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 3
+
+
+def test_full_size_sampled_positions():
+    cfg = CONFIGS["C5"]
+    inp = make_inputs(cfg, DEV)
+    positions = [0, 517, cfg.P - 1]
+    check_lmhead(cfg, inp, positions, label="C5 full")

@@ -1,0 +1,97 @@
+"""Pins of the oracle's fused LM-head variant (oracle/lmhead.py).
+
+  * Unit-vector weights: with W[v] = s_v e_{k_v} the logits are s_v h[k_v]
+    exactly, which fixes the product's operand order and indexing.
+  * Chain rule: central finite differences of the whole loss (Eq. advance with
+    the E-step quantities frozen) as a function of the hidden states equal
+    grad_hidden(g, W) with g the oracle's logit gradient.
+  * The LM-head driver equals the materialised driver on the same logits, and
+    its draws are the Gumbel-max draws of those logits.
+"""
+import numpy as np
+import pytest
+
+from oracle import lmhead, paths, reference, sampler
+
+
+def test_unit_vector_weights_select_hidden_entries():
+    rng = np.random.default_rng(0)
+    n, H, V = 5, 6, 9
+    h = rng.normal(size=(n, H))
+    k = rng.integers(0, H, V)
+    s = rng.normal(size=V)
+    W = np.zeros((V, H))
+    W[np.arange(V), k] = s
+    X = lmhead.logits(h, W)
+    assert X.shape == (n, V)
+    np.testing.assert_array_equal(X, h[:, k] * s[None, :])
+
+
+def test_logits_are_linear_in_each_operand():
+    rng = np.random.default_rng(1)
+    h1, h2 = rng.normal(size=(2, 3, 8))
+    W = rng.normal(size=(11, 8))
+    np.testing.assert_allclose(lmhead.logits(2.0 * h1 - h2, W),
+                               2.0 * lmhead.logits(h1, W) - lmhead.logits(h2, W), atol=1e-12)
+
+
+@pytest.mark.parametrize("mode", [paths.MODE_BASIC, paths.MODE_ARW_CAR])
+def test_hidden_gradient_matches_central_finite_differences(mode):
+    rng = np.random.default_rng(2)
+    N, L, H, V = 3, 2, 4, 6
+    hd = rng.normal(size=(N * L, H))
+    ht = rng.normal(size=(N * L, H))
+    Wd = rng.normal(size=(V, H))
+    Wt = rng.normal(size=(V, H))
+    depth = np.array([L, 1, L])
+    toks = [rng.integers(0, V, N * L) for _ in range(3)]
+    params = dict(mode=mode, temp_draft=0.7, loss_scale=1.5)
+    res = lmhead.run_positions(hd, ht, Wd, Wt, None, depth[None, :], [0], N, L, params, tokens=toks)
+    X = res["X"].reshape(N, L, V)
+    Y = res["Y"].reshape(N, L, V)
+    t3 = [t.reshape(N, L) for t in toks]
+    frozen = paths.score_position(X, Y, None, depth, *t3, params)
+
+    def loss_of(h):
+        Xh = lmhead.logits(h, Wd).reshape(N, L, V)
+        return params["loss_scale"] * paths.loss_from_logits(Xh, Y, None, depth, *t3, frozen, params)
+
+    eps = 1e-6
+    fd = np.zeros_like(hd)
+    for idx in np.ndindex(hd.shape):
+        hp, hm = hd.copy(), hd.copy()
+        hp[idx] += eps
+        hm[idx] -= eps
+        fd[idx] = (loss_of(hp) - loss_of(hm)) / (2 * eps)
+    np.testing.assert_allclose(res["grad_hidden"], fd, atol=1e-8, rtol=1e-6)
+    assert np.abs(fd).max() > 1e-3  # the case is not degenerate
+
+
+def test_driver_equals_materialised_driver_and_gumbel_max():
+    rng = np.random.default_rng(3)
+    N, L, H, Vd, Vt = 2, 3, 8, 10, 16
+    hd = rng.normal(size=(2 * N * L, H))
+    ht = rng.normal(size=(2 * N * L, H))
+    Wd = rng.normal(size=(Vd, H))
+    Wt = rng.normal(size=(Vt, H))
+    d2t = np.sort(rng.permutation(Vt)[:Vd])
+    res = lmhead.run_positions(hd, ht, Wd, Wt, d2t, None, [4, 7], N, L, {}, seed=11, offset=2)
+    ref = reference.run_positions(hd @ Wd.T, ht @ Wt.T, d2t, None, [4, 7], N, L, {}, seed=11, offset=2)
+    for k in ("tok_draft", "tok_target", "tok_greedy", "accept_flag"):
+        np.testing.assert_array_equal(res[k], ref[k])
+    for k in ("lse_q", "coef_a", "coef_b", "grad"):
+        np.testing.assert_allclose(res[k], ref[k], rtol=1e-12, atol=1e-12)
+    rows = 4 * N * L + np.arange(N * L)
+    keys = sampler.gumbel_keys(res["X"][: N * L], rows, 0, 1.0, 11, 2)
+    np.testing.assert_array_equal(res["tok_draft"][: N * L], np.argmax(keys, axis=1))
+
+
+def test_key_gaps_are_top_two_differences():
+    X = np.array([[0.0, 3.0, 1.0, 3.0]])
+    Y = np.array([[5.0, 1.0, 4.5, 2.0, 7.0]])
+    d2t = np.array([0, 1, 2, 3])
+    gd, gt, gg = lmhead.key_gaps(X, Y, d2t, [0], 1.0, 1.0, 0, 0)
+    assert gg[0] == pytest.approx(0.5)  # mapped target values 5, 1, 4.5, 2; the unmapped 7 is ignored
+    kd = np.sort(sampler.gumbel_keys(X, [0], 0, 1.0, 0, 0)[0].astype(np.float64))
+    assert gd[0] == pytest.approx(kd[-1] - kd[-2])
+    assert gt[0] > 0
