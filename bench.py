@@ -17,7 +17,10 @@ Prints one JSON line: value = path-tokens (live rows) per second of whole
 steps; roofline = the dominant kernel against its bound (algorithmic bytes:
 each live row's draft and target logits read once); cpu_baseline = the CPU
 oracle timed on a bounded sample of the same workload (computed before the GPU
-is touched, in worker processes).
+is touched, in worker processes).  The line also carries "fused_lm_head": the
+same step in the fused LM-head variant on its own workload (B=2 T=512 N=8 L=6,
+hidden 4096, LM-head weights 128256 x 4096 and 32000 x 4096 bf16), against the
+bf16 matrix-core peak.  --config C5 makes that workload the line's own.
 """
 import argparse
 import json
@@ -30,6 +33,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, TFLOP/s
 
 METRIC = "path-tokens scored/sec (fwd+bwd) and achieved HBM GB/s at V=128256"
 
@@ -75,6 +79,112 @@ def cpu_baseline(cfg, workers, per_worker=8):
                       f"{workers} worker processes, {wall:.1f} s wall"}
 
 
+def _oracle_lm_position(k):
+    """Position k of the LM-head sample through the CPU oracle (worker process)."""
+    from oracle import lmhead
+    Hd, Ht, Wd, Wt, d2t, N, L = _SAMPLE
+    per = N * L
+    t0 = time.perf_counter()
+    lmhead.run_positions(Hd[k * per:(k + 1) * per], Ht[k * per:(k + 1) * per], Wd, Wt, d2t, None, [k], N, L, {},
+                         seed=0, offset=0)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline_lm(cfg, workers, per_worker=1):
+    """The LM-head oracle (float64 logits, then the per-position oracle) on
+    workers*per_worker positions of the fused workload."""
+    global _SAMPLE
+    import multiprocessing as mp
+
+    from synth import make_inputs, scaled
+    npos = workers * per_worker
+    sample_cfg = scaled(cfg.name, name=cfg.name + "-cpu-sample", B=1, T=npos)
+    inp = make_inputs(sample_cfg, "cpu")
+    f32 = lambda t: t.float().numpy()
+    _SAMPLE = (f32(inp["Hd"]), f32(inp["Ht"]), f32(inp["Wd"]), f32(inp["Wt"]), inp["d2t"].numpy(), cfg.N, cfg.L)
+    del inp
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(workers) as pool:
+        pool.map(_oracle_lm_position, range(npos), chunksize=per_worker)
+    wall = time.perf_counter() - t0
+    _SAMPLE = None
+    rows = npos * cfg.N * cfg.L
+    return {"value": rows / wall, "unit": "path-tokens/s", "cores": workers, "kind": "oracle",
+            "sample": f"{npos} positions ({rows} path-tokens) of the {cfg.name} recipe, float64 LM-head logits + "
+                      f"sample+score+grad, {workers} worker processes, {wall:.1f} s wall"}
+
+
+def bench_lm_head(cfg, steps, warmup, dev):
+    """One EM step of the fused LM-head variant: vsd_sample_score_paths and
+    vsd_weighted_loss_bwd on LmHead sources.  Returns timings and the
+    matrix-core roofline of the forward (the dominant kernel)."""
+    import torch
+
+    import paper_2602_05774_amd as vsd
+    from synth import make_inputs
+    t0 = time.perf_counter()
+    inp = make_inputs(cfg, dev)
+    torch.cuda.synchronize()
+    print(f"[bench] inputs {cfg.name} generated in {time.perf_counter() - t0:.1f} s", flush=True)
+    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+    params = vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target)
+    Xs, Ys = vsd.LmHead(inp["Hd"], inp["Wd"]), vsd.LmHead(inp["Ht"], inp["Wt"])
+    out = vsd.alloc_score_outputs(prob, dev)
+    ws = torch.empty(vsd.score_workspace_bytes(prob, torch.bfloat16, cfg.hidden), dtype=torch.uint8, device=dev)
+    tok = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    grad = vsd.LmHeadGrad(torch.empty(prob.R, cfg.hidden, dtype=torch.bfloat16, device=dev),
+                          torch.empty(prob.R, (cfg.v_draft + 7) // 8 * 8, dtype=torch.bfloat16, device=dev))
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        vsd.sample_score_paths(prob, params, Xs, Ys, inp["d2t"], inp["valid_depth"], cfg.philox_seed,
+                               cfg.philox_offset, out=out, workspace=ws, tokens=tok)
+        if ev:
+            ev[1].record()
+        vsd.weighted_loss_bwd(prob, params, Xs, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=grad,
+                              device_error=err)
+        if ev:
+            ev[2].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_fwd = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
+    t_bwd = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+        raise RuntimeError("device error reported during the LM-head benchmark")
+    live = prob.R if inp["valid_depth"] is None else int((tok[0] >= 0).sum().item())
+    R, H = prob.R, cfg.hidden
+    # algorithmic flops: every row's draft and target logits once (forward);
+    # the draft logits again and g W_d (backward)
+    fwd_flop = 2.0 * R * H * (cfg.v_draft + cfg.v_target)
+    bwd_flop = 4.0 * R * H * cfg.v_draft
+    tf = lambda f, ms: f / (ms * 1e-3) / 1e12
+    res = {
+        "workload": f"{cfg.name}: B={cfg.B} T={cfg.T} N={cfg.N} L={cfg.L} hidden={H} V_target={cfg.v_target} "
+                    f"V_draft={cfg.v_draft} bf16 hidden states and LM-head weights",
+        "path_tokens_per_step": live, "ms_per_step": t_fwd + t_bwd, "wall_ms_per_step": wall * 1e3 / steps,
+        "value": live / ((t_fwd + t_bwd) * 1e-3), "unit": "path-tokens/s",
+        "kernels": {"sample_score": {"ms": t_fwd, "flop": fwd_flop, "TFLOP/s": tf(fwd_flop, t_fwd)},
+                    "bwd": {"ms": t_bwd, "flop": bwd_flop, "TFLOP/s": tf(bwd_flop, t_bwd)}},
+        "step_TFLOP/s": tf(fwd_flop + bwd_flop, t_fwd + t_bwd),
+        "roofline": {"bound": "mfma", "kernel": "k_lm_fwd (forward call: GEMM tiles + sampling epilogue)",
+                     "achieved": tf(fwd_flop, t_fwd), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tf(fwd_flop, t_fwd) / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
+    }
+    del inp, out, ws, grad
+    torch.cuda.empty_cache()
+    return res
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
 KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_device.hpp"], "bwd": ["k_bwd.hip", "vsd_device.hpp"]}
 
@@ -112,6 +222,8 @@ def main():
     ap.add_argument("--config", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-workers", type=int, default=0)
+    ap.add_argument("--no-lm-head", action="store_true", help="skip the fused LM-head measurement")
+    ap.add_argument("--lm-steps", type=int, default=3, help="timed steps of the fused LM-head measurement")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this size first (calibrates PMC byte counters)")
     args = ap.parse_args()
@@ -123,8 +235,8 @@ def main():
     from synth import CONFIGS
     cfg = CONFIGS[args.config]
     if cfg.kind == "fused":
-        print("the fused LM-head workload is not benchmarked by this build", file=sys.stderr)
-        sys.exit(2)
+        main_lm_head(args, cfg)
+        return
 
     base = None
     if not args.no_cpu_baseline:
@@ -240,6 +352,32 @@ def main():
                                f"V_target={cfg.v_target} V_draft={cfg.v_draft} logits={cfg.dtype}",
                    "path_tokens_per_step": live, "parallelism": "single GPU"},
         "kernels": kernels, "three_calls": three_calls, "roofline": roof, "cpu_baseline": base,
+    }
+    if not args.no_lm_head:
+        del inp, X, Y, out, ws, grad
+        torch.cuda.empty_cache()
+        line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
+    print(json.dumps(line), flush=True)
+
+
+def main_lm_head(args, cfg):
+    """--config C5: the fused LM-head step as the line's own workload."""
+    base = None
+    if not args.no_cpu_baseline:
+        workers = args.cpu_workers or max(1, min(16, os.cpu_count() or 1))
+        base = cpu_baseline_lm(cfg, workers)
+        print(f"[bench] cpu baseline: {base['value']:.2f} {base['unit']} on {base['cores']} cores", flush=True)
+    import torch
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    r = bench_lm_head(cfg, args.steps, args.warmup, dev)
+    line = {
+        "metric": METRIC, "value": r["value"], "unit": "path-tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "wall_ms_per_step": r["wall_ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": r["workload"], "path_tokens_per_step": r["path_tokens_per_step"],
+                   "parallelism": "single GPU"},
+        "kernels": r["kernels"], "step_TFLOP/s": r["step_TFLOP/s"], "roofline": r["roofline"], "cpu_baseline": base,
     }
     print(json.dumps(line), flush=True)
 
