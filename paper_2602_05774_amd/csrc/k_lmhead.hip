@@ -2,24 +2,30 @@
 // Y = H_t W_t^T (bf16 operands, fp32 accumulation on MFMA) are never written
 // to memory.
 //
-// Forward.  One launch covers both models.  A workgroup (four wavefronts)
-// owns 128 rows and one slice of a vocabulary; for every 128-column tile of
-// the slice it computes the 128x128 logit tile on v_mfma_f32_32x32x16_bf16
-// (each wavefront a 64x64 quadrant of 2x2 MFMA tiles, operands staged
-// through double-buffered LDS) and consumes it in place: the online
-// log-sum-exp (row softmax normalisers, Sec. "Preliminary"), the Gumbel-max
-// draws with the exact candidate filter (Alg. 1 draws z~ ~ q and z' ~ p under
-// the library's normative sampler) and the greedy maximum (Alg. 2).  Per-row
-// running state stays in LDS across the tiles of the slice; the slice's
-// result goes to a partial record.  A combine kernel merges the slices, forms
-// the drawn tokens' logits by dot products (H_r . W_z) and writes tokens and
-// the per-row statistics (log q, log alpha of Eq. acc) that the per-position
-// combine then turns into weights and the loss.
+// Matrix core tiling.  A workgroup of eight wavefronts (two per SIMD) owns a
+// 256x256 output tile; wavefront (wr, wc) computes rows wr*128 .. +127 and
+// columns wc*64 .. +63 as 4x2 tiles of v_mfma_f32_32x32x16_bf16.  Operands
+// stream through a double-buffered LDS stage of 64 K values per row.  Rows
+// that are K-contiguous in memory (hidden states, weights in the forward) are
+// staged as they are and read as one 16-byte fragment per lane; a K-major
+// operand (the weight in dH = g W_d) is staged N-contiguous and read with the
+// gfx950 transpose load (ds_read_b64_tr_b16), two per fragment.
+//
+// Forward.  One launch covers both models.  A workgroup owns 256 rows and one
+// slice of a vocabulary; for every 256-column tile of the slice it computes
+// the logit tile and consumes it in place: the online log-sum-exp (row
+// softmax normalisers, Sec. "Preliminary"), the Gumbel-max draws with the
+// exact candidate filter (Alg. 1 draws z~ ~ q and z' ~ p under the library's
+// normative sampler) and the greedy maximum (Alg. 2).  Per-row running state
+// stays in LDS across the tiles of the slice; the slice's result goes to a
+// partial record.  A combine kernel merges the slices, forms the drawn
+// tokens' logits by dot products (H_r . W_z) and writes tokens and the
+// per-row statistics (log q, log alpha of Eq. acc).
 //
 // Backward (derivative of Eq. advance through the LM head).  The draft
 // logits are recomputed tile by tile; g = loss_scale/T_q ((a+b) q - a e_z~ -
 // b e_z') is written in bf16 (the gradient with respect to the logits); then
-// dH_d = g W_d on MFMA, the W_d tiles read column-wise out of LDS.
+// dH_d = g W_d.
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
 
@@ -28,19 +34,22 @@ namespace vsd {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LDK = BK + 8;     // padded K-contiguous LDS row (bf16): 144 B, conflict-free 16-B reads
-constexpr int LDN = BN + 8;     // padded N-contiguous LDS row (bf16) of the NN GEMM's B tile
-constexpr int LDT = BN + 4;     // padded fp32 epilogue tile row
-constexpr int kStageElems = (BM + BN) * LDK;        // A and B tiles of one stage (bf16)
-constexpr int kLdsBytes = 2 * kStageElems * 2;      // double buffer; also holds the fp32 tile
-constexpr int kXcds = 8;                            // MI355X: 8 XCDs, workgroups dealt round-robin
-constexpr int kGroupRows = 8;                       // row tiles per L2 reuse group
-static_assert(BM * LDT * 4 <= kLdsBytes, "epilogue tile must fit the operand buffers");
-static_assert(BM * LDK + BK * LDN <= kStageElems, "NN stage must fit");
-static_assert(kLmTile == BN, "vocabulary tile width");
+constexpr int TM = 256, TN = 256, TK = 64;   // workgroup tile and K per stage
+constexpr int kThreads = 512;                // eight wavefronts
+constexpr int LDK = TK + 8;                  // K-contiguous LDS row (bf16): 144 B, conflict-free 16-B reads
+constexpr int LDN = TN + 32;                 // N-contiguous LDS row (bf16) of a K-major operand: 576 B
+constexpr int LDT = TN + 4;                  // fp32 epilogue row
+constexpr int kStageElems = 2 * TM * LDK;    // A and B of one stage (bf16)
+constexpr int kLdsBytes = 2 * kStageElems * 2;
+constexpr int kXcds = 8;                     // MI355X: 8 XCDs, workgroups dealt round-robin
+constexpr int kGroupRows = 4;                // row tiles per L2 reuse group
+static_assert(TM * LDK == TK * LDN, "both B layouts fill the same stage slot");
+static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit the operand buffers");
+static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -64,91 +73,149 @@ __device__ __forceinline__ void tile_of(int pid, int nrt, int ncol, int& rt, int
   col = in / rows;
 }
 
-// ---------------------------------------------------------------- NT GEMM ---
-// acc = A[row0 .. +BM, 0 .. K) * B[col0 .. +BN, 0 .. K)^T; A and B are bf16,
-// row-major along K with row strides lda / ldb; rows >= nrow and columns
-// >= ncol read as zero; K % BK == 0.  Wavefront w owns the 64x64 quadrant
-// (w >> 1, w & 1): acc[ti*2 + tj] is its 32x32 tile (ti, tj).
-struct NtTile {
+// ------------------------------------------------------------- GEMM core ---
+// acc = A[row0 .. +TM, 0 .. K) * B, accumulated over K in order.  A is bf16
+// [*, K] row-major (stride lda).  NN = false: B is [N, K] row-major (stride
+// ldb) and the tile takes rows col0 .. +TN of it; NN = true: B is [K, N]
+// row-major and the tile takes columns col0 .. +TN.  Rows >= nrow, columns
+// >= ncol and K >= K read as zero; NN needs ncol % 8 == 0, NT needs K % 8 ==
+// 0 (A's K tail is read element-wise when K % TK != 0).
+// Wavefront w = (wr, wc) = (w >> 2, w & 3) accumulates acc[ti*2 + tj] =
+// rows wr*128 + ti*32 .. +31, columns wc*64 + tj*32 .. +31.
+template <bool NN>
+struct Core {
   const bf16_t* A;
   const bf16_t* B;
   int64_t lda, ldb;
   int64_t row0, nrow;
   int col0, ncol, K;
 
-  __device__ __forceinline__ void load_stage(int k0, uint4 (&ra)[4], uint4 (&rb)[4]) const {
+  __device__ __forceinline__ uint4 load_a(int64_t r, int k) const {
+    if (r >= nrow) return make_uint4(0, 0, 0, 0);
+    const bf16_t* p = A + r * lda + k;
+    if (k + 8 <= K) return *reinterpret_cast<const uint4*>(p);
+    uint32_t w[4] = {0, 0, 0, 0};
+    for (int e = 0; e < 8; ++e)
+      if (k + e < K) w[e >> 1] |= (uint32_t)p[e] << (16 * (e & 1));
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+
+  __device__ __forceinline__ void load(int k0, uint4 (&ra)[4], uint4 (&rb)[4]) const {
     const int t = threadIdx.x;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int c = t + 256 * j;  // 16-byte chunk of the 128 x 64 tile
+      const int c = t + kThreads * j;  // 16-byte chunk of the 256 x 64 tile
       const int r = c >> 3, kc = (c & 7) * 8;
-      ra[j] = (row0 + r < nrow) ? *reinterpret_cast<const uint4*>(A + (row0 + r) * lda + k0 + kc)
-                                : make_uint4(0, 0, 0, 0);
-      rb[j] = (col0 + r < ncol) ? *reinterpret_cast<const uint4*>(B + (int64_t)(col0 + r) * ldb + k0 + kc)
-                                : make_uint4(0, 0, 0, 0);
+      ra[j] = load_a(row0 + r, k0 + kc);
+      if (!NN) {
+        rb[j] = (col0 + r < ncol && k0 + kc < K)
+                    ? *reinterpret_cast<const uint4*>(B + (int64_t)(col0 + r) * ldb + k0 + kc)
+                    : make_uint4(0, 0, 0, 0);
+      } else {
+        const int kr = c >> 5, nc = (c & 31) * 8;  // 64 K rows x 256 columns
+        rb[j] = (k0 + kr < K && col0 + nc < ncol)
+                    ? *reinterpret_cast<const uint4*>(B + (int64_t)(k0 + kr) * ldb + col0 + nc)
+                    : make_uint4(0, 0, 0, 0);
+      }
     }
   }
 
-  __device__ __forceinline__ static void store_stage(bf16_t* lds, const uint4 (&ra)[4], const uint4 (&rb)[4]) {
+  __device__ __forceinline__ static void store(bf16_t* L, const uint4 (&ra)[4], const uint4 (&rb)[4]) {
     const int t = threadIdx.x;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int c = t + 256 * j;
+      const int c = t + kThreads * j;
       const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(lds + r * LDK + kc) = ra[j];
-      *reinterpret_cast<uint4*>(lds + BM * LDK + r * LDK + kc) = rb[j];
+      *reinterpret_cast<uint4*>(L + r * LDK + kc) = ra[j];
+      if (!NN) {
+        *reinterpret_cast<uint4*>(L + TM * LDK + r * LDK + kc) = rb[j];
+      } else {
+        const int kr = c >> 5, nc = (c & 31) * 8;
+        *reinterpret_cast<uint4*>(L + TM * LDK + kr * LDN + nc) = rb[j];
+      }
+    }
+  }
+
+  // The B fragment of tile column n0 (32 wide) at K offset ks*16.
+  __device__ __forceinline__ static bf16x8 frag_b(const bf16_t* L, int n0, int ks, int lane) {
+    if (!NN) return *reinterpret_cast<const bf16x8*>(L + TM * LDK + (n0 + (lane & 31)) * LDK + ks * 16 + (lane >> 5) * 8);
+    // Transpose load: in each 16-lane group, source lane s names row
+    // k = base + s/4 and columns 4(s%4) .. +3; lane i of the group then holds
+    // rows base .. base+3 of column i.  Group g covers rows (g >> 1)*8 and
+    // columns (g & 1)*16 of the 16 x 32 fragment; two loads give 8 rows.
+    const int g = lane >> 4, s = lane & 15;
+    const bf16_t* p = L + TM * LDK + (ks * 16 + (g >> 1) * 8 + (s >> 2)) * LDN + n0 + (g & 1) * 16 + 4 * (s & 3);
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    // (whole-vector casts: the two loads feed the MFMA registers directly)
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * LDN));
+    return __builtin_shufflevector(__builtin_bit_cast(bf16x4, lo), __builtin_bit_cast(bf16x4, hi), 0, 1, 2, 3, 4,
+                                   5, 6, 7);
+  }
+
+  __device__ __forceinline__ static void compute(const bf16_t* L, f32x16 (&acc)[8]) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wr = w >> 2, wc = w & 3;
+#pragma unroll
+    for (int ks = 0; ks < TK / 16; ++ks) {
+      bf16x8 a[4], b[2];
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti)
+        a[ti] = *reinterpret_cast<const bf16x8*>(L + (wr * 128 + ti * 32 + (lane & 31)) * LDK + ks * 16 + (lane >> 5) * 8);
+#pragma unroll
+      for (int tj = 0; tj < 2; ++tj) b[tj] = frag_b(L, wc * 64 + tj * 32, ks, lane);
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < 2; ++tj) acc[ti * 2 + tj] = mfma(a[ti], b[tj], acc[ti * 2 + tj]);
     }
   }
 
   // Ends with a barrier: on return the LDS operand buffers are free.
-  __device__ void run(bf16_t* lds, f32x16 (&acc)[4]) const {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int wr = w >> 1, wc = w & 1;
+  __device__ void run(bf16_t* lds, f32x16 (&acc)[8]) const {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] = f32x16{};
+    for (int q = 0; q < 8; ++q) acc[q] = f32x16{};
     uint4 ra[4], rb[4];
-    const int nst = K / BK;
-    load_stage(0, ra, rb);
-    store_stage(lds, ra, rb);
+    const int nst = (K + TK - 1) / TK;
+    load(0, ra, rb);
+    store(lds, ra, rb);
     __syncthreads();
     for (int st = 0; st < nst; ++st) {
-      const bf16_t* cur = lds + (st & 1) * kStageElems;
-      if (st + 1 < nst) load_stage((st + 1) * BK, ra, rb);
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        bf16x8 a[2], b[2];
-#pragma unroll
-        for (int ti = 0; ti < 2; ++ti) {
-          const int ar = wr * 64 + ti * 32 + (lane & 31);
-          a[ti] = *reinterpret_cast<const bf16x8*>(cur + ar * LDK + ks * 16 + (lane >> 5) * 8);
-          const int br = wc * 64 + ti * 32 + (lane & 31);
-          b[ti] = *reinterpret_cast<const bf16x8*>(cur + BM * LDK + br * LDK + ks * 16 + (lane >> 5) * 8);
-        }
-#pragma unroll
-        for (int ti = 0; ti < 2; ++ti)
-#pragma unroll
-          for (int tj = 0; tj < 2; ++tj) acc[ti * 2 + tj] = mfma(a[ti], b[tj], acc[ti * 2 + tj]);
-      }
-      if (st + 1 < nst) store_stage(lds + ((st + 1) & 1) * kStageElems, ra, rb);
+      if (st + 1 < nst) load((st + 1) * TK, ra, rb);
+      compute(lds + (st & 1) * kStageElems, acc);
+      if (st + 1 < nst) store(lds + ((st + 1) & 1) * kStageElems, ra, rb);
       __syncthreads();
     }
   }
 };
 
-// The four quadrants' accumulators into the fp32 tile T[BM][LDT].
-__device__ __forceinline__ void spill(const f32x16 (&acc)[4], float* T) {
+// Round rd of the epilogue: wavefront (wr, wc) writes its accumulator tiles
+// ti = 2 rd, 2 rd + 1 into buffer T + wr * 64 * LDT, whose row q is tile row
+// wr*128 + rd*64 + q.
+template <int RD>
+__device__ __forceinline__ void spill(const f32x16 (&acc)[8], float* T) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int wr = w >> 1, wc = w & 1;
+  const int wr = w >> 2, wc = w & 3;
+  float* Tb = T + wr * 64 * LDT;
 #pragma unroll
-  for (int ti = 0; ti < 2; ++ti)
+  for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
     for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int row = wr * 64 + ti * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-        const int col = wc * 64 + tj * 32 + (lane & 31);
-        T[row * LDT + col] = acc[ti * 2 + tj][i];
+        const int q = t2 * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+        Tb[q * LDT + wc * 64 + tj * 32 + (lane & 31)] = acc[(2 * RD + t2) * 2 + tj][i];
       }
+}
+
+// Epilogue rows of round rd for wavefront w, iteration it (0..7): 32 lanes
+// per row, 8 columns per lane.  Returns the buffer row pointer; rl = tile row.
+__device__ __forceinline__ const float* epi_row(const float* T, int rd, int it, int& rl) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int hb = w >> 2;
+  const int q = (w & 3) * 16 + it * 2 + (lane >> 5);
+  rl = hb * 128 + rd * 64 + q;
+  return T + hb * 64 * LDT + q * LDT + (lane & 31) * 8;
 }
 
 // --------------------------------------------------------- epilogue helpers ---
@@ -156,7 +223,7 @@ __device__ __forceinline__ uint32_t word_of(const uint4& p, int k) {
   return k == 0 ? p.x : k == 1 ? p.y : k == 2 ? p.z : p.w;
 }
 
-// Candidate filter of the Gumbel-max draw.  With u from word w (S3) and
+// Candidate filter of the Gumbel-max draw.  With u from word w and
 // j' = (~w) >> 8 <= 2^24 (1 - u), the variate obeys
 // G = -ln(-ln u) <= -ln(1 - u) <= (24 - log2 j') ln 2, so an element whose
 // bound x/T + (24 - log2 j') ln 2 stays below the best key so far, thr, less
@@ -172,7 +239,6 @@ __device__ __forceinline__ bool bound_ok(float v, uint32_t w, float c2, float of
   return fmaf(v, c2, off) >= __builtin_amdgcn_logf((float)((~w) >> 8));
 }
 
-// Reductions over the 16 lanes that share a row (lanes 16g .. 16g+15).
 __device__ __forceinline__ void lse_merge(float& mraw, float& mc, float& s, float omraw, float omc, float os) {
   const float nm = fmaxf(mc, omc);
   s = s * __builtin_amdgcn_exp2f(mc - nm) + os * __builtin_amdgcn_exp2f(omc - nm);
@@ -187,17 +253,6 @@ __device__ __forceinline__ void best_merge(float& key, int& idx, float okey, int
   }
 }
 
-__device__ __forceinline__ void group_lse(float& mraw, float& mc, float& s) {
-#pragma unroll
-  for (int off = 8; off >= 1; off >>= 1)
-    lse_merge(mraw, mc, s, __shfl_xor(mraw, off, kWave), __shfl_xor(mc, off, kWave), __shfl_xor(s, off, kWave));
-}
-
-__device__ __forceinline__ void group_best(float& key, int& idx) {
-#pragma unroll
-  for (int off = 8; off >= 1; off >>= 1) best_merge(key, idx, __shfl_xor(key, off, kWave), __shfl_xor(idx, off, kWave));
-}
-
 struct RowState {
   float mraw, mc, s;  // log-sum-exp: raw maximum, its scaled value, sum of exp2(x c2 - mc)
   float key;          // best Gumbel key so far
@@ -208,159 +263,169 @@ struct RowState {
 };
 static_assert(sizeof(RowState) == sizeof(LmPartial), "partial record layout");
 
-// One pass over the column tiles of one slice of one model for rows
-// row0 .. row0+127.  TARGET = false: draft logits, keys of family 0 over
-// every column.  TARGET = true: target logits, log-sum-exp over every column,
-// keys of family 1 and the greedy maximum over the mapped columns, each
-// identified by its draft index.
+__device__ __forceinline__ RowState empty_state() {
+  return RowState{kNegBig, kNegBig, 0.0f, -INFINITY, 0x7FFFFFFF, -INFINITY, 0x7FFFFFFF, 0};
+}
+
+__device__ __forceinline__ void state_merge(RowState& a, const RowState& b) {
+  lse_merge(a.mraw, a.mc, a.s, b.mraw, b.mc, b.s);
+  best_merge(a.key, a.idx, b.key, b.idx);
+  best_merge(a.gval, a.gidx, b.gval, b.gidx);
+}
+
+// Fold eight consecutive columns c .. c+7 of row r (values x; columns past
+// the vocabulary hold -inf) into the running state st of one row segment.
+// Every lane of a wavefront works on the same columns of a different row, so
+// map lookups and Philox group changes are uniform across the wavefront.
+// TARGET = false: keys of family 0 over every column.  TARGET = true: keys of
+// family 1 and the greedy maximum over the mapped columns, each identified by
+// its draft index; the last Philox call (group cg, words cw) is reused, and
+// for an ascending map the draft indices increase along the row, so a new
+// call is made once per four mapped columns.
 template <bool TARGET>
-__device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds, float* T, RowState* rs) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+__device__ __forceinline__ void fold8(const LmFwdArgs& a, const float (&x)[8], uint32_t r, int c, int nvalid,
+                                      float inv_t, float c2, RowState& st, int& cg, uint4& cw) {
+  float cm = x[0];
+#pragma unroll
+  for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
+  if (cm > st.mraw) {
+    const float nmc = cm * c2;
+    st.s *= __builtin_amdgcn_exp2f(st.mc - nmc);
+    st.mc = nmc;
+    st.mraw = cm;
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) st.s += __builtin_amdgcn_exp2f(fmaf(x[k], c2, -st.mc));
+  if (!a.sample) return;
+  const float off = bound_offset(st.key);
+  if (!TARGET) {
+    const uint32_t c0 = (uint32_t)c >> 2;
+    const uint4 p0 = philox4x32_10(c0, r, 0u, a.offset, a.k0, a.k1);
+    const uint4 p1 = philox4x32_10(c0 + 1, r, 0u, a.offset, a.k0, a.k1);
+    uint32_t cand = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      cand |= (k < nvalid && bound_ok(x[k], word_of(k < 4 ? p0 : p1, k & 3), c2, off)) ? (1u << k) : 0u;
+    if (__ballot(cand != 0u) != 0ull) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (cand & (1u << k)) {  // columns increase along the row: strict > keeps the smallest index
+          const float key = gumbel_key(x[k], inv_t, word_of(k < 4 ? p0 : p1, k & 3));
+          if (key > st.key) {
+            st.key = key;
+            st.idx = c + k;
+          }
+        }
+      }
+    }
+  } else {
+    int v[8];
+    if (a.inv == nullptr) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = k < nvalid ? c + k : -1;
+    } else if (nvalid == 8) {
+      load8(a.inv + c, v);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = k < nvalid ? a.inv[c + k] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if (v[k] >= 0) {
+        const int grp = v[k] >> 2;
+        if (grp != cg) {
+          cg = grp;
+          cw = philox4x32_10((uint32_t)grp, r, 1u, a.offset, a.k0, a.k1);
+        }
+        const uint32_t wk = word_of(cw, v[k] & 3);
+        best_merge(st.gval, st.gidx, x[k], v[k]);
+        if (bound_ok(x[k], wk, c2, off)) best_merge(st.key, st.idx, gumbel_key(x[k], inv_t, wk), v[k]);
+      }
+    }
+  }
+}
+
+// One slice of one model for rows row0 .. row0+255.  TARGET = false: draft
+// logits; TARGET = true: target logits (log-sum-exp over every column, draws
+// and greedy maximum over the mapped ones).  In the epilogue of each tile,
+// wavefront w = (seg, hb) = (w >> 1, w & 1) and lane l take tile rows
+// hb*128 + rd*64 + l (rounds rd = 0, 1) and columns seg*64 .. +63: each
+// thread carries the state of two row segments across the slice's tiles, and
+// the four segments of a row are merged once, at the end, through LDS.
+template <bool TARGET>
+__device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds, float* T) {
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hb = w & 1, seg = w >> 1;
   const int V = TARGET ? a.Vt : a.Vd;
   const int nslice = TARGET ? a.nslice_t : a.nslice_d;
-  const int ntiles = (V + BN - 1) / BN;
+  const int ntiles = (V + TN - 1) / TN;
   const int t_begin = (int)((int64_t)ntiles * slice / nslice);
   const int t_end = (int)((int64_t)ntiles * (slice + 1) / nslice);
   const float inv_t = TARGET ? a.inv_tp : a.inv_tq;
   const float c2 = inv_t * kLog2e;
-  const uint32_t fam = TARGET ? 1u : 0u;
-  if (threadIdx.x < BM)
-    rs[threadIdx.x] = RowState{kNegBig, kNegBig, 0.0f, -INFINITY, 0x7FFFFFFF, -INFINITY, 0x7FFFFFFF, 0};
-  const bf16_t* Hs = static_cast<const bf16_t*>(TARGET ? a.Ht : a.Hd);
-  const bf16_t* Ws = static_cast<const bf16_t*>(TARGET ? a.Wt : a.Wd);
-  NtTile g{Hs, Ws, a.H, a.H, row0, a.R, 0, V, a.H};
+  RowState st[2] = {empty_state(), empty_state()};
+  Core<false> g{static_cast<const bf16_t*>(TARGET ? a.Ht : a.Hd), static_cast<const bf16_t*>(TARGET ? a.Wt : a.Wd),
+                a.H, a.H, row0, a.R, 0, V, a.H};
   for (int tile = t_begin; tile < t_end; ++tile) {
-    g.col0 = tile * BN;
-    f32x16 acc[4];
+    g.col0 = tile * TN;
+    f32x16 acc[8];
     g.run(lds, acc);
-    spill(acc, T);
-    __syncthreads();
-    // wavefront w: rows w*32 .. +31, four at a time; 16 lanes per row, 8 columns per lane
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) {
+      if (rd == 0)
+        spill<0>(acc, T);
+      else
+        spill<1>(acc, T);
+      __syncthreads();
+      const int64_t r = row0 + hb * 128 + rd * 64 + lane;
+      if (r < a.R) {
+        const float* src = T + (hb * 64 + lane) * LDT + seg * 64;
+        int cg = -1;
+        uint4 cw = make_uint4(0, 0, 0, 0);
 #pragma unroll 1
-    for (int it = 0; it < 8; ++it) {
-      const int rl = w * 32 + it * 4 + (lane >> 4);
-      const int64_t r = row0 + rl;
-      const int c = g.col0 + (lane & 15) * 8;
-      float x[8];
-      load8(T + rl * LDT + (lane & 15) * 8, x);
-      const int nvalid = r < a.R ? min(8, max(0, V - c)) : 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (k >= nvalid) x[k] = -INFINITY;
-      float mraw = kNegBig, mc = kNegBig, s = 0.0f;
-      {
-        float cm = x[0];
-#pragma unroll
-        for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
-        if (cm > mraw) {
-          mraw = cm;
-          mc = cm * c2;
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c2, -mc));
-      }
-      float bkey = -INFINITY, gval = -INFINITY;
-      int bidx = 0x7FFFFFFF, gidx = 0x7FFFFFFF;
-      if (a.sample) {
-        const float off = bound_offset(rs[rl].key);
-        if (!TARGET) {
-          const uint32_t c0 = (uint32_t)c >> 2;
-          const uint4 p0 = philox4x32_10(c0, (uint32_t)r, fam, a.offset, a.k0, a.k1);
-          const uint4 p1 = philox4x32_10(c0 + 1, (uint32_t)r, fam, a.offset, a.k0, a.k1);
-          uint32_t cand = 0;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const bool ok = k < nvalid && bound_ok(x[k], word_of(k < 4 ? p0 : p1, k & 3), c2, off);
-            cand |= ok ? (1u << k) : 0u;
-          }
-          if (__ballot(cand != 0u) != 0ull) {
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-              if (cand & (1u << k)) {  // columns increase with k: strict > keeps the smallest index
-                const float key = gumbel_key(x[k], inv_t, word_of(k < 4 ? p0 : p1, k & 3));
-                if (key > bkey) {
-                  bkey = key;
-                  bidx = c + k;
-                }
-              }
-            }
-          }
-        } else {
-          // Draft indices of the lane's columns (-1: unmapped).  For an
-          // ascending map they are consecutive, v_a .. v_a + m - 1 with
-          // m <= 8, and lie in the Philox counters v_a>>2 .. (v_a>>2) + 2;
-          // any other index (a map that is not ascending) gets its own call.
-          int v[8];
-          int va = 0x7FFFFFFF;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            v[k] = k < nvalid ? (a.inv != nullptr ? a.inv[c + k] : c + k) : -1;
-            va = (v[k] >= 0 && v[k] < va) ? v[k] : va;
-          }
-          const uint32_t gb = va == 0x7FFFFFFF ? 0u : (uint32_t)va >> 2;
-          const uint4 p0 = philox4x32_10(gb, (uint32_t)r, fam, a.offset, a.k0, a.k1);
-          const uint4 p1 = philox4x32_10(gb + 1, (uint32_t)r, fam, a.offset, a.k0, a.k1);
-          const uint4 p2 = philox4x32_10(gb + 2, (uint32_t)r, fam, a.offset, a.k0, a.k1);
-          uint32_t wv[8];
-          uint32_t cand = 0;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            wv[k] = 0;
-            if (v[k] >= 0) {
-              const uint32_t gi = ((uint32_t)v[k] >> 2) - gb;
-              const int e = v[k] & 3;
-              wv[k] = gi == 0 ? word_of(p0, e)
-                    : gi == 1 ? word_of(p1, e)
-                    : gi == 2 ? word_of(p2, e)
-                              : word_of(philox4x32_10((uint32_t)v[k] >> 2, (uint32_t)r, fam, a.offset, a.k0, a.k1), e);
-              best_merge(gval, gidx, x[k], v[k]);
-              cand |= bound_ok(x[k], wv[k], c2, off) ? (1u << k) : 0u;
-            }
-          }
-          if (__ballot(cand != 0u) != 0ull) {
+        for (int ch = 0; ch < 8; ++ch) {
+          const int c = g.col0 + seg * 64 + ch * 8;
+          const int nvalid = min(8, V - c);
+          if (nvalid <= 0) break;
+          float x[8];
+          load8(src + ch * 8, x);
+          if (nvalid < 8) {
 #pragma unroll
             for (int k = 0; k < 8; ++k)
-              if (cand & (1u << k)) best_merge(bkey, bidx, gumbel_key(x[k], inv_t, wv[k]), v[k]);
+              if (k >= nvalid) x[k] = -INFINITY;
           }
+          fold8<TARGET>(a, x, (uint32_t)r, c, nvalid, inv_t, c2, st[rd], cg, cw);
         }
       }
-      group_lse(mraw, mc, s);
-      if (a.sample) {
-        group_best(bkey, bidx);
-        if (TARGET) group_best(gval, gidx);
-      }
-      if ((lane & 15) == 0 && r < a.R) {
-        RowState st = rs[rl];
-        lse_merge(st.mraw, st.mc, st.s, mraw, mc, s);
-        if (a.sample) {
-          best_merge(st.key, st.idx, bkey, bidx);
-          if (TARGET) best_merge(st.gval, st.gidx, gval, gidx);
-        }
-        rs[rl] = st;
-      }
+      __syncthreads();  // the buffers are the next round's (or the next GEMM's)
     }
-    __syncthreads();  // the tile buffer is the next GEMM's operand buffer
   }
-  if (threadIdx.x < BM && row0 + threadIdx.x < a.R) {
-    const RowState st = rs[threadIdx.x];
+  RowState* red = reinterpret_cast<RowState*>(T);  // [TM rows][4 segments]
+#pragma unroll
+  for (int rd = 0; rd < 2; ++rd) red[(hb * 128 + rd * 64 + lane) * 4 + seg] = st[rd];
+  __syncthreads();
+  if (threadIdx.x < TM && row0 + threadIdx.x < a.R) {
+    RowState m = red[threadIdx.x * 4];
+#pragma unroll
+    for (int sg = 1; sg < 4; ++sg) state_merge(m, red[threadIdx.x * 4 + sg]);  // segments in column order
     const int col = TARGET ? slice : a.nslice_t + slice;
     a.part[(row0 + threadIdx.x) * (a.nslice_t + a.nslice_d) + col] =
-        LmPartial{st.mraw, st.mc, st.s, st.key, st.idx, st.gval, st.gidx, 0};
+        LmPartial{m.mraw, m.mc, m.s, m.key, m.idx, m.gval, m.gidx, 0};
   }
 }
 
-__global__ __launch_bounds__(256, 2) void k_lm_fwd(LmFwdArgs a) {
+__global__ __launch_bounds__(kThreads, 1) void k_lm_fwd(LmFwdArgs a) {
   __shared__ __align__(16) unsigned char smem[kLdsBytes];
-  __shared__ RowState rs[BM];
   bf16_t* lds = reinterpret_cast<bf16_t*>(smem);
   float* T = reinterpret_cast<float*>(smem);
-  const int nrt = (int)((a.R + BM - 1) / BM);
+  const int nrt = (int)((a.R + TM - 1) / TM);
   int rt, col;
   tile_of(blockIdx.x, nrt, a.nslice_t + a.nslice_d, rt, col);
   if (col < a.nslice_t)
-    lm_pass<true>(a, (int64_t)rt * BM, col, lds, T, rs);
+    lm_pass<true>(a, (int64_t)rt * TM, col, lds, T);
   else
-    lm_pass<false>(a, (int64_t)rt * BM, col - a.nslice_t, lds, T, rs);
+    lm_pass<false>(a, (int64_t)rt * TM, col - a.nslice_t, lds, T);
 }
 
 // Inverse of the draft->target map: inv[t] = v where d2t[v] = t, else -1.
@@ -488,155 +553,94 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
 }
 
 // ----------------------------------------------------------- backward pass ---
-// g for one 128x128 tile of the recomputed draft logits, written in bf16 to
+// g for one 256x256 tile of the recomputed draft logits, written in bf16 to
 // G [R, ldg] (columns [0, Vd) only).
-__global__ __launch_bounds__(256, 2) void k_lm_bwd_g(LmBwdArgs a) {
+__global__ __launch_bounds__(kThreads, 1) void k_lm_bwd_g(LmBwdArgs a) {
   __shared__ __align__(16) unsigned char smem[kLdsBytes];
   bf16_t* lds = reinterpret_cast<bf16_t*>(smem);
   float* T = reinterpret_cast<float*>(smem);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nrt = (int)((a.R + BM - 1) / BM);
+  const int lane = threadIdx.x & 63;
+  const int nrt = (int)((a.R + TM - 1) / TM);
   int rt, ct;
-  tile_of(blockIdx.x, nrt, (a.Vd + BN - 1) / BN, rt, ct);
-  const int64_t row0 = (int64_t)rt * BM;
-  const int col0 = ct * BN;
-  NtTile g{static_cast<const bf16_t*>(a.Hd), static_cast<const bf16_t*>(a.Wd), a.H, a.H, row0, a.R, col0, a.Vd,
-           a.H};
-  f32x16 acc[4];
+  tile_of(blockIdx.x, nrt, (a.Vd + TN - 1) / TN, rt, ct);
+  const int64_t row0 = (int64_t)rt * TM;
+  const int col0 = ct * TN;
+  Core<false> g{static_cast<const bf16_t*>(a.Hd), static_cast<const bf16_t*>(a.Wd), a.H, a.H, row0, a.R, col0,
+                a.Vd, a.H};
+  f32x16 acc[8];
   g.run(lds, acc);
-  spill(acc, T);
-  __syncthreads();
   const float c2 = a.inv_tq * kLog2e;
   const float k = a.scale * a.inv_tq;
   bf16_t* G = static_cast<bf16_t*>(a.G);
+#pragma unroll
+  for (int rd = 0; rd < 2; ++rd) {
+    if (rd == 0)
+      spill<0>(acc, T);
+    else
+      spill<1>(acc, T);
+    __syncthreads();
 #pragma unroll 1
-  for (int it = 0; it < 8; ++it) {
-    const int rl = w * 32 + it * 4 + (lane >> 4);
-    const int64_t r = row0 + rl;
-    const int c = col0 + (lane & 15) * 8;
-    const int nvalid = min(8, a.Vd - c);
-    if (r >= a.R || nvalid <= 0) continue;
-    const float ca = a.coef_a[r], cb = a.coef_b[r];
-    float gv[8];
-    if (ca == 0.0f && cb == 0.0f) {
+    for (int it = 0; it < 8; ++it) {
+      int rl;
+      const float* src = epi_row(T, rd, it, rl);
+      const int64_t r = row0 + rl;
+      const int c = col0 + (lane & 31) * 8;
+      const int nvalid = min(8, a.Vd - c);
+      if (r >= a.R || nvalid <= 0) continue;
+      const float ca = a.coef_a[r], cb = a.coef_b[r];
+      float gv[8];
+      if (ca == 0.0f && cb == 0.0f) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) gv[j] = 0.0f;
-    } else {
-      float x[8];
-      load8(T + rl * LDT + (lane & 15) * 8, x);
-      const float lse2 = a.lse_q[r] * kLog2e;
-      const float kab = k * (ca + cb), ka = k * ca, kb = k * cb;
-      const int zd = a.tok_d[r], zt = a.tok_t[r];
+        for (int j = 0; j < 8; ++j) gv[j] = 0.0f;
+      } else {
+        float x[8];
+        load8(src, x);
+        const float lse2 = a.lse_q[r] * kLog2e;
+        const float kab = k * (ca + cb), ka = k * ca, kb = k * cb;
+        const int zd = a.tok_d[r], zt = a.tok_t[r];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float t = kab * __builtin_amdgcn_exp2f(fmaf(x[j], c2, -lse2));
-        t -= (c + j == zd) ? ka : 0.0f;
-        t -= (c + j == zt) ? kb : 0.0f;
-        gv[j] = t;
+        for (int j = 0; j < 8; ++j) {
+          float t = kab * __builtin_amdgcn_exp2f(fmaf(x[j], c2, -lse2));
+          t -= (c + j == zd) ? ka : 0.0f;
+          t -= (c + j == zt) ? kb : 0.0f;
+          gv[j] = t;
+        }
+      }
+      bf16_t* out = G + r * a.ldg + c;
+      if (nvalid == 8) {
+        store8(out, gv);
+      } else {
+        for (int j = 0; j < nvalid; ++j) store1(out + j, gv[j]);
       }
     }
-    bf16_t* out = G + r * a.ldg + c;
-    if (nvalid == 8) {
-      store8(out, gv);
-    } else {
-      for (int j = 0; j < nvalid; ++j) store1(out + j, gv[j]);
-    }
+    __syncthreads();
   }
 }
 
-// C[M, N] = A[M, K] B[K, N], bf16 operands (row-major, strides lda / ldb),
-// fp32 accumulation, bf16 result (stride ldc).  A's tile is staged
-// K-contiguous; B's tile is staged as it lies in memory (N-contiguous) and
-// each lane gathers its eight K values of one column with 16-bit LDS reads.
-// N % 8 == 0; K is arbitrary (the tail reads as zero).
-__global__ __launch_bounds__(256, 2) void k_lm_gemm_nn(LmGemmNNArgs a) {
+// dH[R, H] = G[R, Vd] W_d[Vd, H] (bf16 in, fp32 accumulation, bf16 out):
+// one 256x256 tile per workgroup, W_d's tiles read through the transpose
+// load.
+__global__ __launch_bounds__(kThreads, 1) void k_lm_gemm_nn(LmGemmNNArgs a) {
   __shared__ __align__(16) bf16_t lds[2 * kStageElems];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int wr = w >> 1, wc = w & 1;
-  const int nrt = (int)((a.M + BM - 1) / BM);
+  const int wr = w >> 2, wc = w & 3;
+  const int nrt = (int)((a.M + TM - 1) / TM);
   int rt, ct;
-  tile_of(blockIdx.x, nrt, (a.N + BN - 1) / BN, rt, ct);
-  const int64_t row0 = (int64_t)rt * BM;
-  const int n0 = ct * BN;
-  const int t = threadIdx.x;
-  const bf16_t* A = static_cast<const bf16_t*>(a.A);
-  const bf16_t* B = static_cast<const bf16_t*>(a.B);
-  f32x16 acc[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) acc[q] = f32x16{};
-  const int nst = (a.K + BK - 1) / BK;
-  uint4 ra[4], rb[4];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = t + 256 * j;
-      {  // A: row r, K offset kc .. kc+7
-        const int r = c >> 3, kc = (c & 7) * 8;
-        const int64_t gr = row0 + r;
-        const int gk = k0 + kc;
-        if (gr < a.M && gk + 8 <= a.K) {
-          ra[j] = *reinterpret_cast<const uint4*>(A + gr * a.lda + gk);
-        } else {
-          uint32_t wv[4] = {0, 0, 0, 0};
-          if (gr < a.M)
-            for (int e = 0; e < 8; ++e)
-              if (gk + e < a.K) wv[e >> 1] |= (uint32_t)A[gr * a.lda + gk + e] << (16 * (e & 1));
-          ra[j] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-        }
-      }
-      {  // B: K row kr, N offset nc .. nc+7
-        const int kr = c >> 4, nc = (c & 15) * 8;
-        const int gk = k0 + kr, gn = n0 + nc;
-        rb[j] = (gk < a.K && gn < a.N) ? *reinterpret_cast<const uint4*>(B + (int64_t)gk * a.ldb + gn)
-                                      : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store = [&](bf16_t* buf) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = t + 256 * j;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(buf + r * LDK + kc) = ra[j];
-      const int kr = c >> 4, nc = (c & 15) * 8;
-      *reinterpret_cast<uint4*>(buf + BM * LDK + kr * LDN + nc) = rb[j];
-    }
-  };
-  load(0);
-  store(lds);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const bf16_t* cur = lds + (st & 1) * kStageElems;
-    const bf16_t* curb = cur + BM * LDK;
-    if (st + 1 < nst) load((st + 1) * BK);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 av[2], bv[2];
-#pragma unroll
-      for (int ti = 0; ti < 2; ++ti) {
-        const int ar = wr * 64 + ti * 32 + (lane & 31);
-        av[ti] = *reinterpret_cast<const bf16x8*>(cur + ar * LDK + ks * 16 + (lane >> 5) * 8);
-        const int bn = wc * 64 + ti * 32 + (lane & 31);
-        const int kb = ks * 16 + (lane >> 5) * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) bv[ti][e] = __builtin_bit_cast(__bf16, curb[(kb + e) * LDN + bn]);
-      }
-#pragma unroll
-      for (int ti = 0; ti < 2; ++ti)
-#pragma unroll
-        for (int tj = 0; tj < 2; ++tj) acc[ti * 2 + tj] = mfma(av[ti], bv[tj], acc[ti * 2 + tj]);
-    }
-    if (st + 1 < nst) store(lds + ((st + 1) & 1) * kStageElems);
-    __syncthreads();
-  }
+  tile_of(blockIdx.x, nrt, (a.N + TN - 1) / TN, rt, ct);
+  const int64_t row0 = (int64_t)rt * TM;
+  const int n0 = ct * TN;
+  Core<true> g{static_cast<const bf16_t*>(a.A), static_cast<const bf16_t*>(a.B), a.lda, a.ldb, row0, a.M, n0, a.N,
+               a.K};
+  f32x16 acc[8];
+  g.run(lds, acc);
   bf16_t* C = static_cast<bf16_t*>(a.C);
 #pragma unroll
-  for (int ti = 0; ti < 2; ++ti)
+  for (int ti = 0; ti < 4; ++ti)
 #pragma unroll
     for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int64_t row = row0 + wr * 64 + ti * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+        const int64_t row = row0 + wr * 128 + ti * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
         const int col = n0 + wc * 64 + tj * 32 + (lane & 31);
         if (row < a.M && col < a.N) store1(C + row * a.ldc + col, acc[ti * 2 + tj][i]);
       }
@@ -651,8 +655,8 @@ hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32
 }
 
 hipError_t launch_lm_fwd(const LmFwdArgs& a, hipStream_t s) {
-  const int64_t nrt = (a.R + BM - 1) / BM;
-  hipLaunchKernelGGL(k_lm_fwd, dim3((unsigned)(nrt * (a.nslice_t + a.nslice_d))), dim3(256), 0, s, a);
+  const int64_t nrt = (a.R + TM - 1) / TM;
+  hipLaunchKernelGGL(k_lm_fwd, dim3((unsigned)(nrt * (a.nslice_t + a.nslice_d))), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -662,12 +666,12 @@ hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s) {
-  const int64_t nrt = (a.R + BM - 1) / BM;
-  hipLaunchKernelGGL(k_lm_bwd_g, dim3((unsigned)(nrt * ((a.Vd + BN - 1) / BN))), dim3(256), 0, s, a);
+  const int64_t nrt = (a.R + TM - 1) / TM;
+  hipLaunchKernelGGL(k_lm_bwd_g, dim3((unsigned)(nrt * ((a.Vd + TN - 1) / TN))), dim3(kThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   LmGemmNNArgs gm{a.G, a.Wd, a.dH, a.R, a.ldg, a.H, a.H, a.H, a.Vd};
-  hipLaunchKernelGGL(k_lm_gemm_nn, dim3((unsigned)(nrt * ((a.H + BN - 1) / BN))), dim3(256), 0, s, gm);
+  hipLaunchKernelGGL(k_lm_gemm_nn, dim3((unsigned)(nrt * ((a.H + TN - 1) / TN))), dim3(kThreads), 0, s, gm);
   return hipGetLastError();
 }
 

@@ -59,8 +59,9 @@ vsd_status check_dims(const vsd_dims* d) {
     if (d->dtype != VSD_BF16) return fail(VSD_ERR_UNSUPPORTED, "the fused LM head takes bf16 operands only");
     // workgroup ids of the fused kernels are 32-bit: row tiles x vocabulary tiles
     const int64_t nrt = (R + vsd::kLmTile - 1) / vsd::kLmTile;
-    const int64_t vt = std::max<int64_t>((d->v_draft + vsd::kLmTile - 1) / vsd::kLmTile,
-                                         vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
+    const int64_t vt = std::max<int64_t>(
+        std::max<int64_t>((d->v_draft + vsd::kLmTile - 1) / vsd::kLmTile, (d->hidden_dim + vsd::kLmTile - 1) / vsd::kLmTile),
+        vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
     if (nrt * vt >= kMaxRows)
       return fail(VSD_ERR_INVALID_SHAPE, "fused LM head: R=%lld rows x %lld vocabulary tiles too large",
                   (long long)R, (long long)vt);

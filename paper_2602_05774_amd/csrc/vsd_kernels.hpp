@@ -80,8 +80,8 @@ struct BwdArgs {
 };
 
 // ------------------------------------------------ fused LM-head variant ---
-constexpr int kLmTile = 128;           // rows and vocabulary columns per logit tile
-constexpr int kLmTilesPerSlice = 32;   // vocabulary tiles one forward workgroup walks
+constexpr int kLmTile = 256;           // rows and vocabulary columns per logit tile
+constexpr int kLmTilesPerSlice = 16;   // vocabulary tiles one forward workgroup walks
 
 // Vocabulary slices of a V-column pass (a function of V only, so the float
 // outputs of a row do not depend on the batch size).
