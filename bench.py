@@ -33,6 +33,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+# VALU issue peak without packed fp32: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# (a wave64 instruction occupies a SIMD for 4 cycles), in lane-ops per second
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, TFLOP/s
 
 METRIC = "path-tokens scored/sec (fwd+bwd) and achieved HBM GB/s at V=128256"
@@ -112,6 +115,18 @@ def cpu_baseline_lm(cfg, workers, per_worker=1):
     return {"value": rows / wall, "unit": "path-tokens/s", "cores": workers, "kind": "oracle",
             "sample": f"{npos} positions ({rows} path-tokens) of the {cfg.name} recipe, float64 LM-head logits + "
                       f"sample+score+grad, {workers} worker processes, {wall:.1f} s wall"}
+
+
+def copy_calibration(mib, dev):
+    """One plain device copy of `mib` MiB: the PMC byte counters of this
+    dispatch calibrate those of the kernels."""
+    import torch
+    src_buf = torch.ones(mib << 20, dtype=torch.uint8, device=dev)
+    dst_buf = torch.empty_like(src_buf)
+    torch.cuda.synchronize()
+    dst_buf.copy_(src_buf)
+    torch.cuda.synchronize()
+    del src_buf, dst_buf
 
 
 def bench_lm_head(cfg, steps, warmup, dev):
@@ -265,13 +280,7 @@ def main():
 
     tok = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
     if args.copy_calibration_mib:
-        n = args.copy_calibration_mib << 20
-        src_buf = torch.ones(n, dtype=torch.uint8, device=dev)
-        dst_buf = torch.empty_like(src_buf)
-        torch.cuda.synchronize()
-        dst_buf.copy_(src_buf)
-        torch.cuda.synchronize()
-        del src_buf, dst_buf
+        copy_calibration(args.copy_calibration_mib, dev)
 
     def step_fused(ev=None):
         """One EM step: one-pass sample + score, then the backward."""
@@ -338,11 +347,26 @@ def main():
     three_calls = {"ms_per_step": t_step3, "sample_ms": t_sample3, "score_ms": t_score3, "bwd_ms": t_bwd3,
                    "score_GB/s": gbs(ss_bytes, t_score3),
                    "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score3 + t_bwd3) / HBM_PEAK_GBS}
+    # The one-pass sampler is bound by VALU issue (its counters show the SIMDs
+    # issuing at their peak rate): its roofline counts the method's essential
+    # lane operations per live row -- 4 per logit for the two log-sum-exps
+    # (max, fma, exp2, add), 40 per Philox4x32-10 call (10 rounds of two
+    # 32x32->64 products and two 3-way XORs; ceil(V_d/4) calls per family, two
+    # families) and 6 per key for the candidate bound (not, shift, convert,
+    # log2, fma, compare).  The backward is bound by HBM.
+    ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4) + 6.0 * 2 * cfg.v_draft)
+    kernels["sample_score"]["valu_lane_ops"] = ss_ops
+    kernels["sample_score"]["TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
     dominant = "sample_score" if t_ss >= t_bwd else "bwd"
     k = kernels[dominant]
-    roof = {"bound": "hbm", "kernel": "k_sample (fused, mapped, bf16)" if dominant == "sample_score" else "k_bwd",
-            "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": k["GB/s"] / HBM_PEAK_GBS,
-            "traffic": measured_traffic(cfg.name, dominant)}
+    if dominant == "sample_score":
+        roof = {"bound": "alu", "kernel": "k_sample (one-pass sample + score, mapped, bf16)",
+                "achieved": k["TOP/s"], "peak": VALU_PEAK_TOPS, "unit": "TOP/s (VALU lane-ops)",
+                "frac": k["TOP/s"] / VALU_PEAK_TOPS, "hbm_GB/s": k["GB/s"], "hbm_frac": k["GB/s"] / HBM_PEAK_GBS,
+                "traffic": measured_traffic(cfg.name, dominant)}
+    else:
+        roof = {"bound": "hbm", "kernel": "k_bwd", "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": k["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name, dominant)}
     line = {
         "metric": METRIC, "value": live / (t_step * 1e-3), "unit": "path-tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step, "wall_ms_per_step": wall * 1e3 / args.steps,
@@ -370,6 +394,8 @@ def main_lm_head(args, cfg):
     import torch
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration_mib:
+        copy_calibration(args.copy_calibration_mib, dev)
     r = bench_lm_head(cfg, args.steps, args.warmup, dev)
     line = {
         "metric": METRIC, "value": r["value"], "unit": "path-tokens/s", "n_gpus": 1, "steps": args.steps,
