@@ -38,7 +38,8 @@ MODE_BASIC, MODE_ARW, MODE_ARW_CAR = 0, 1, 2
 CAR_PROB, CAR_LOGPROB = 0, 1
 
 DEFAULT_PARAMS = dict(temp_draft=1.0, temp_target=1.0, w_base=1.05, car_tau=0.2,
-                      mode=MODE_ARW_CAR, car_input=CAR_PROB, loss_scale=1.0)
+                      mode=MODE_ARW_CAR, car_input=CAR_PROB, loss_scale=1.0,
+                      kl_weight=0.0, kl_topk=10)
 
 
 def log_softmax_normaliser(logits, temperature):
@@ -225,3 +226,18 @@ def loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None)
             used = lq_d if frozen["accept_flag"][s, i] else lq_t
             total += frozen["o_prime"][s, i] * (used - frozen["c"][s, i] * lq_d)
     return -total / W
+
+
+def loss_with_klv(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None):
+    """loss_from_logits plus kl_weight times the position's top-K term
+    (oracle.klv), the E-step quantities frozen; its derivative with respect to
+    X is what grad_position plus the KL rows give."""
+    from . import klv
+    p = dict(DEFAULT_PARAMS)
+    if params:
+        p.update(params)
+    base = loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, p)
+    if p["kl_weight"] == 0.0:
+        return base
+    KL = klv.position_terms(X, Y, d2t, depth, int(p["kl_topk"]), p["temp_draft"], p["temp_target"])[3]
+    return base + p["kl_weight"] * KL

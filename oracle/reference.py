@@ -8,7 +8,7 @@ every bf16 value exactly).
 """
 import numpy as np
 
-from . import paths, sampler
+from . import klv, paths, sampler
 
 
 def sample_position(Xp, Yp_mapped, depth, first_row, temp_draft, temp_target, seed, offset):
@@ -37,7 +37,11 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
     given, is a tuple of three [len(positions)*N*L] arrays used instead of
     sampling (scoring then follows the given tokens).
     Returns a dict of per-row arrays [len(positions)*N*L] (or [.., V_d] for
-    grad, [.., 3] for log_alpha / log_q) and per-position arrays.
+    grad, [.., 3] for log_alpha / log_q) and per-position arrays.  With
+    params kl_weight > 0 the top-K term (oracle.klv) joins the loss and the
+    gradient, and kl_row [rows], kl_idx and kl_grad [rows, K] (the gradient's
+    sparse part, loss_scale kl_weight / N (q_hat - p_hat) / T_q at kl_idx)
+    and kl_pos [positions] are returned.
     """
     p = dict(paths.DEFAULT_PARAMS)
     p.update(params or {})
@@ -52,7 +56,9 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
             "o_prime", "beta", "zeta", "coef_a", "coef_b", "LS"]
     acc = {k: [] for k in keys}
     out = {"tok_draft": [], "tok_target": [], "tok_greedy": [], "exp_accept_len": [],
-           "loss_pos": [], "W": [], "grad": []}
+           "loss_pos": [], "W": [], "grad": [], "kl_row": [], "kl_idx": [], "kl_grad": [], "kl_pos": []}
+    lam = float(p["kl_weight"])
+    K = int(p["kl_topk"])
     for k, pos in enumerate(positions):
         if tokens is None:
             toks = sample_position(X[k], Y[k][:, :, d2t_arr], depth[k], int(pos) * N * L,
@@ -68,16 +74,35 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
         out["tok_target"].append(toks[1].reshape(-1))
         out["tok_greedy"].append(toks[2].reshape(-1))
         out["exp_accept_len"].append(sc["exp_accept_len"])
-        out["loss_pos"].append(sc["loss"])
+        loss = sc["loss"]
+        if lam > 0.0:
+            L_row, omega, dx, KL = klv.position_terms(X[k], Y[k], None if d2t is None else d2t_arr, depth[k], K,
+                                                      p["temp_draft"], p["temp_target"])
+            loss = loss + lam * KL
+            kl_grad = p["loss_scale"] * lam / N * dx
+            out["kl_row"].append(L_row.reshape(-1))
+            out["kl_idx"].append(omega.reshape(N * L, K))
+            out["kl_grad"].append(kl_grad.reshape(N * L, K))
+            out["kl_pos"].append(KL)
+        out["loss_pos"].append(loss)
         out["W"].append(sc["W"])
         if want_grad:
             g = paths.grad_position(X[k], sc["lse_q"], toks[0], toks[1], sc["coef_a"], sc["coef_b"],
                                     p["temp_draft"], p["loss_scale"])
+            if lam > 0.0:
+                for s in range(N):
+                    for i in range(int(depth[k][s])):
+                        g[s, i, omega[s, i]] += kl_grad[s, i]
             out["grad"].append(g.reshape(N * L, Vd))
     res = {k: np.concatenate(v) for k, v in acc.items()}
     for k in ("tok_draft", "tok_target", "tok_greedy", "exp_accept_len"):
         res[k] = np.concatenate(out[k])
     res["loss_pos"] = np.asarray(out["loss_pos"])
+    if lam > 0.0:
+        res["kl_row"] = np.concatenate(out["kl_row"])
+        res["kl_idx"] = np.concatenate(out["kl_idx"])
+        res["kl_grad"] = np.concatenate(out["kl_grad"])
+        res["kl_pos"] = np.asarray(out["kl_pos"])
     res["W"] = np.asarray(out["W"])
     res["loss_total"] = p["loss_scale"] * res["loss_pos"].sum()
     if want_grad:
