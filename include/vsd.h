@@ -145,6 +145,25 @@
  *   grad->grad_hidden [R, H] (bf16) receives g . weight_d.
  *   grad->grad_weight must be NULL (the weight gradient is not computed).
  *   dims->ld_target is unused.
+ *
+ * VSD (KL): the top-K renormalised KL term (params->kl_weight > 0)
+ * ---------------------------------------------------------------
+ *   The paper's KL variant (Eq. klv) adds a token-level distillation term
+ *   over the K target tokens of highest probability.  Per live row r, with
+ *   y_v = Y[r][d2t[v]] over the draft vocabulary:
+ *     Omega_r  = the K draft indices with the largest y_v (equal values: the
+ *                smaller index first), in that order;
+ *     p_hat(v) = exp(y_v/T_p) / sum_{u in Omega_r} exp(y_u/T_p),
+ *     q_hat(v) = exp(X[r][v]/T_q) / sum_{u in Omega_r} exp(X[r][u]/T_q);
+ *     kl_row[r] = - sum_{v in Omega_r} p_hat(v) log q_hat(v).
+ *   Per position KL_x = (1/N) sum over live rows of kl_row (the path-level
+ *   divergence is the expected sum of the per-step ones), and
+ *   loss_pos[x] = L_x + kl_weight KL_x.  The gradient gains
+ *   kl_grad[r][k] = loss_scale kl_weight / N (q_hat - p_hat)(Omega_r[k]) / T_q
+ *   at draft index kl_idx[r][k] = Omega_r[k]; vsd_weighted_loss_bwd adds
+ *   these when given kl_idx and kl_grad.  K <= v_draft.  Computed by
+ *   vsd_score_paths on materialised logits (the one-pass and fused LM-head
+ *   calls return VSD_ERR_UNSUPPORTED with kl_weight > 0).
  */
 #ifndef VSD_H
 #define VSD_H
@@ -156,7 +175,7 @@
 extern "C" {
 #endif
 
-#define VSD_ABI_VERSION 1
+#define VSD_ABI_VERSION 2
 
 typedef enum vsd_status {
   VSD_OK = 0,
@@ -212,6 +231,8 @@ typedef struct vsd_params {
   int32_t mode;        /* vsd_grad_mode */
   int32_t car_input;   /* vsd_car_input */
   float loss_scale;    /* multiplies the summed loss and the gradient */
+  float kl_weight;     /* >= 0; weight of the top-K renormalised KL term (0 = off) */
+  int32_t kl_topk;     /* K of that term, 1..16 (used when kl_weight > 0) */
 } vsd_params;
 
 /* Source of one model's logits.  Materialised (dims->hidden_dim == 0):
@@ -238,9 +259,14 @@ typedef struct vsd_score_out {
   float* zeta;            /* [R]   optional: CAR weight */
   float* coef_a;          /* [R]   required: coefficient of -log q(z~) */
   float* coef_b;          /* [R]   required: coefficient of -log q(z') */
-  float* loss_pos;        /* [P]   optional: L_x (unscaled) */
-  float* loss_total;      /* [1]   optional: loss_scale * sum_x L_x */
+  float* loss_pos;        /* [P]   optional: L_x + kl_weight KL_x (unscaled) */
+  float* loss_total;      /* [1]   optional: loss_scale * sum_x loss_pos */
   int32_t* device_error;  /* [1]   required */
+  /* Top-K renormalised KL term (kl_weight > 0; see "VSD (KL)" above): */
+  int32_t* kl_idx;        /* [R,K] required with the term: the row's top-K draft indices (-1 masked) */
+  float* kl_grad;         /* [R,K] required with the term: the term's gradient at kl_idx */
+  float* kl_row;          /* [R]   optional: the row's term (0 masked) */
+  float* kl_pos;          /* [P]   optional: KL_x */
 } vsd_score_out;
 
 typedef struct vsd_grad {
@@ -305,12 +331,15 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
  * touched.  grad_logits has the layout of X (stride ld_draft) and its dtype
  * (bf16 rounded to nearest-even).  Fused LM head: X is recomputed from the
  * draft hidden states, g is written to grad_logits in bf16, and grad_hidden
- * = g . weight_d (fp32 accumulation of the bf16 g, bf16 result). */
+ * = g . weight_d (fp32 accumulation of the bf16 g, bf16 result).
+ * kl_idx / kl_grad ([R, K] from vsd_score_paths) add the top-K KL term's
+ * gradient: required when params->kl_weight > 0, ignored otherwise. */
 vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
                                  const vsd_src* draft, const float* lse_draft,
                                  const int32_t* tok_draft,
                                  const int32_t* tok_target, const float* coef_a,
-                                 const float* coef_b, const vsd_grad* grad,
+                                 const float* coef_b, const int32_t* kl_idx,
+                                 const float* kl_grad, const vsd_grad* grad,
                                  int32_t* device_error, void* hip_stream);
 
 /* Bytes of workspace vsd_score_paths needs for `dims` (host only). */

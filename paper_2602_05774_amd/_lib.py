@@ -30,7 +30,8 @@ class VsdDims(ctypes.Structure):
 
 class VsdParams(ctypes.Structure):
     _fields_ = [("temp_draft", c_f32), ("temp_target", c_f32), ("w_base", c_f32), ("car_tau", c_f32),
-                ("mode", c_i32), ("car_input", c_i32), ("loss_scale", c_f32)]
+                ("mode", c_i32), ("car_input", c_i32), ("loss_scale", c_f32), ("kl_weight", c_f32),
+                ("kl_topk", c_i32)]
 
 
 class VsdSrc(ctypes.Structure):
@@ -41,7 +42,7 @@ class VsdScoreOut(ctypes.Structure):
     _fields_ = [(name, c_vp) for name in (
         "lse_draft", "lse_target", "log_alpha", "log_q_tok", "survival", "exp_accept_len",
         "accept_flag", "valid_flag", "o_prime", "beta", "zeta", "coef_a", "coef_b",
-        "loss_pos", "loss_total", "device_error")]
+        "loss_pos", "loss_total", "device_error", "kl_idx", "kl_grad", "kl_row", "kl_pos")]
 
 
 class VsdGrad(ctypes.Structure):
@@ -75,7 +76,7 @@ def load():
                                            P(VsdScoreOut), c_vp, ctypes.c_size_t, c_vp]
     lib.vsd_sample_score_paths.restype = c_i32
     lib.vsd_weighted_loss_bwd.argtypes = [P(VsdDims), P(VsdParams), P(VsdSrc), c_vp, c_vp, c_vp, c_vp,
-                                          c_vp, P(VsdGrad), c_vp, c_vp]
+                                          c_vp, c_vp, c_vp, P(VsdGrad), c_vp, c_vp]
     lib.vsd_weighted_loss_bwd.restype = c_i32
     lib.vsd_score_workspace_bytes.argtypes = [P(VsdDims), P(ctypes.c_size_t)]
     lib.vsd_score_workspace_bytes.restype = c_i32

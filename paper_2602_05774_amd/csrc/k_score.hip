@@ -12,8 +12,17 @@
 //                (Eq. beta_update), CAR zeta (Eq. zeta_update), the loss of
 //                Eq. advance / Eq. basic and the per-row coefficients a, b.
 // k_loss_total   one workgroup: loss_scale * sum over positions, fixed order.
+//
+// With the top-K renormalised KL term on (VSD (KL) variant, Eq. klv),
+// k_score_rows also selects, while it streams the target row, the K mapped
+// target tokens with the largest logits (exact wavefront top-K, vsd_topk.hpp;
+// a mapped column is found by a bit mask and its draft index by the inverse
+// map), then forms p_hat and q_hat renormalised over them, the row's term
+// -sum p_hat log q_hat and its gradient coefficients; k_combine adds the
+// per-position average over paths to the loss.
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
+#include "vsd_topk.hpp"
 
 namespace vsd {
 
@@ -93,8 +102,51 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
   return RowLse{mraw, (log2f(s) - delta) * kLn2};
 }
 
+// row_lse of the target row, also offering every mapped column to a
+// wavefront top-K (value = raw target logit, index = its draft index).
 template <typename T, bool MAPPED>
+__device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const uint32_t* mask,
+                               const int32_t* inv) {
+  float mraw = kNegBig, mc = kNegBig, s = 0.0f;
+  constexpr int step = 8 * kWave;
+  auto idx_of = [&](int col) { return MAPPED ? inv[col] : col; };
+  for (int chunk = 0; chunk < V; chunk += step) {
+    const int base = chunk + lane * 8;
+    const int nvalid = min(8, V - base);
+    float x[8];
+    if (nvalid >= 8) {
+      load8(row + base, x);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = k < nvalid ? load1(row + base + k) : -INFINITY;
+    }
+    float cm = x[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
+    if (cm > mraw) {
+      const float nmc = cm * c;
+      s *= __builtin_amdgcn_exp2f(mc - nmc);
+      mc = nmc;
+      mraw = cm;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -mc));
+    uint32_t mbits = nvalid > 0 ? 0xFFu : 0u;
+    if (MAPPED && nvalid > 0) mbits = (mask[base >> 5] >> (base & 31)) & 0xFFu;
+    tk.reserve(step, lane);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) tk.offer(x[k], base + k, k < nvalid && ((mbits >> k) & 1u), idx_of, lane);
+  }
+  wave_lse2(mc, s);
+  mraw = wave_max(mraw);
+  const float delta = fmaf(mraw, c, -mc);
+  return RowLse{mraw, (log2f(s) - delta) * kLn2};
+}
+
+template <typename T, bool MAPPED, bool KL>
 __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
+  __shared__ float kl_bv[KL ? kRowsPerBlock * kTopKCap : 1];
+  __shared__ int kl_bi[KL ? kRowsPerBlock * kTopKCap : 1];
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (r >= a.R) return;
@@ -117,12 +169,27 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
       a.lse_q[r] = 0.0f;
       if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
     }
+    if (KL) {
+      if (lane < a.kl_k) {
+        a.kl_idx[r * a.kl_k + lane] = -1;
+        a.kl_grad[r * a.kl_k + lane] = 0.0f;
+      }
+      if (lane == 0) a.kl_row[r] = 0.0f;
+    }
     return;
   }
   const T* X = static_cast<const T*>(a.X) + r * a.ld_d;
   const T* Y = static_cast<const T*>(a.Y) + r * a.ld_t;
   const RowLse q = row_lse(X, a.Vd, a.inv_tq * kLog2e, lane);
-  const RowLse p = row_lse(Y, a.Vt, a.inv_tp * kLog2e, lane);
+  WaveTopK tk;
+  RowLse p;
+  if (KL) {
+    const int slot = threadIdx.x >> 6;
+    tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
+    p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.map_mask, a.inv);
+  } else {
+    p = row_lse(Y, a.Vt, a.inv_tp * kLog2e, lane);
+  }
   const float lse_q = q.mraw * a.inv_tq + q.tail;
   const float lse_p = p.mraw * a.inv_tp + p.tail;
   if (lane < 3) {  // lane f gathers family f
@@ -146,6 +213,28 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   if (lane == 0) {
     a.lse_q[r] = lse_q;
     if (a.lse_p != nullptr) a.lse_p[r] = lse_p;
+  }
+  if (KL) {
+    // lane k < K holds the k-th of the top K: p_hat and q_hat renormalised
+    // over the K, the row term -sum p_hat log q_hat and its gradient
+    // coefficients loss_scale * kl_weight / N * (q_hat - p_hat) / T_q
+    tk.finish(lane);
+    const bool mine = lane < a.kl_k;
+    const int v = mine ? tk.bi[lane] : 0;
+    const float pa = mine ? tk.bv[lane] * a.inv_tp : -INFINITY;
+    const float qa = mine ? load1(X + v) * a.inv_tq : -INFINITY;
+    const float pm = wave_max(pa), qm = wave_max(qa);
+    const float pe = mine ? expf(pa - pm) : 0.0f;
+    const float qe = mine ? expf(qa - qm) : 0.0f;
+    const float ps = wave_sum(pe), qs = wave_sum(qe);
+    const float p_hat = pe / ps, q_hat = qe / qs;
+    const float log_q_hat = qa - qm - logf(qs);
+    const float term = wave_sum(mine ? -p_hat * log_q_hat : 0.0f);
+    if (mine) {
+      a.kl_idx[r * a.kl_k + lane] = v;
+      a.kl_grad[r * a.kl_k + lane] = a.kl_gscale * (q_hat - p_hat);
+    }
+    if (lane == 0) a.kl_row[r] = term;
   }
 }
 
@@ -200,10 +289,11 @@ __global__ __launch_bounds__(1024) void k_combine(CombineArgs a) {
   }
   const int64_t row0 = ((int64_t)pos * a.N + s) * a.L;
   float LSd = 0.0f, LSt = 0.0f, LSg = 0.0f, LQd = 0.0f, LQt = 0.0f;
-  float ea = 0.0f, wsum = 0.0f, lsum = 0.0f;
+  float ea = 0.0f, wsum = 0.0f, lsum = 0.0f, klsum = 0.0f;
   for (int l = 0; l < a.L; ++l) {
     const bool live = real && l < d;
     const int64_t row = row0 + l;
+    if (live && a.kl_row != nullptr) klsum += a.kl_row[row];
     if (live) {  // prefix sums of log alpha (log survival) and of log q
       LSd += a.la[row * 3 + 0];
       LSt += a.la[row * 3 + 1];
@@ -264,7 +354,16 @@ __global__ __launch_bounds__(1024) void k_combine(CombineArgs a) {
     }
     if (a.ea) a.ea[(int64_t)pos * a.N + s] = ea;
   }
-  if (threadIdx.x == 0) a.loss_pos[pos] = W > 0.0f ? -total / W : 0.0f;
+  if (a.kl_row != nullptr) {
+    // KL_x = (1/N) sum over live slots of the row terms, weighted into the loss
+    const float kl = block_sum(klsum, redf) / (float)a.N;
+    if (threadIdx.x == 0) {
+      a.loss_pos[pos] = (W > 0.0f ? -total / W : 0.0f) + a.kl_weight * kl;
+      if (a.kl_pos != nullptr) a.kl_pos[pos] = kl;
+    }
+  } else if (threadIdx.x == 0) {
+    a.loss_pos[pos] = W > 0.0f ? -total / W : 0.0f;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_loss_total(const float* loss_pos, int32_t P, float scale, float* out) {
@@ -278,17 +377,39 @@ __global__ __launch_bounds__(256) void k_loss_total(const float* loss_pos, int32
 template <typename T>
 hipError_t launch_rows_t(const ScoreRowArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
-  if (a.d2t != nullptr)
-    hipLaunchKernelGGL((k_score_rows<T, true>), grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_score_rows<T, false>), grid, dim3(256), 0, s, a);
+  if (a.kl_k > 0) {
+    if (a.d2t != nullptr)
+      hipLaunchKernelGGL((k_score_rows<T, true, true>), grid, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_score_rows<T, false, true>), grid, dim3(256), 0, s, a);
+  } else if (a.d2t != nullptr) {
+    hipLaunchKernelGGL((k_score_rows<T, true, false>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_score_rows<T, false, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
+}
+
+// Bit mask of the mapped target columns (bit t of word t/32), from the
+// inverse map.
+__global__ void k_map_mask(const int32_t* inv, int Vt, uint32_t* mask) {
+  const int w = blockIdx.x * blockDim.x + threadIdx.x;
+  if (w * 32 >= Vt) return;
+  uint32_t m = 0;
+  for (int b = 0; b < 32 && w * 32 + b < Vt; ++b) m |= (inv[w * 32 + b] >= 0 ? 1u : 0u) << b;
+  mask[w] = m;
 }
 
 }  // namespace
 
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s) {
   return bf16 ? launch_rows_t<bf16_t>(a, s) : launch_rows_t<float>(a, s);
+}
+
+hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s) {
+  const int words = (Vt + 31) / 32;
+  hipLaunchKernelGGL(k_map_mask, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, s, inv, Vt, mask);
+  return hipGetLastError();
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {

@@ -8,6 +8,7 @@
 
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
+#include "vsd_topk.hpp"
 
 namespace {
 
@@ -130,19 +131,26 @@ vsd_status check_params(const vsd_params* p) {
   if (p->car_input != VSD_CAR_PROB && p->car_input != VSD_CAR_LOGPROB)
     return fail(VSD_ERR_INVALID_VALUE, "car_input=%d", p->car_input);
   if (!std::isfinite(p->loss_scale)) return fail(VSD_ERR_INVALID_VALUE, "loss_scale must be finite");
+  if (!std::isfinite(p->kl_weight) || p->kl_weight < 0.0f)
+    return fail(VSD_ERR_INVALID_VALUE, "kl_weight must be finite and >= 0");
+  if (p->kl_weight > 0.0f && (p->kl_topk < 1 || p->kl_topk > vsd::kMaxTopK))
+    return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d outside [1,%d]", p->kl_topk, vsd::kMaxTopK);
   return VSD_OK;
 }
+
+bool kl_on(const vsd_params* p) { return p->kl_weight > 0.0f; }
 
 vsd_status hip_fail(hipError_t e, const char* what) {
   return fail(VSD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
 struct WorkspaceLayout {
-  size_t la, lq, loss, inv, part, total;
+  size_t la, lq, loss, klrow, inv, mask, part, total;
 };
 
-// la [R,3], lq [R,3], loss [P] fp32; fused LM head also: inv [v_target]
-// int32 and the slice partials [R, nslice_t + nslice_d].
+// la [R,3], lq [R,3], loss [P], KL row terms [R] fp32; the inverse map
+// [v_target] int32 and the mapped-column bit mask [ceil(v_target/32)]; fused
+// LM head also the slice partials [R, nslice_t + nslice_d].
 WorkspaceLayout workspace_layout(const vsd_dims* d) {
   const int64_t R = rows_of(d);
   const int64_t P = (int64_t)d->B * d->T;
@@ -150,11 +158,12 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   w.la = 0;
   w.lq = w.la + align_up((size_t)R * 3 * sizeof(float));
   w.loss = w.lq + align_up((size_t)R * 3 * sizeof(float));
-  w.inv = w.loss + align_up((size_t)P * sizeof(float));
-  w.part = w.inv;
-  w.total = w.inv;
+  w.klrow = w.loss + align_up((size_t)P * sizeof(float));
+  w.inv = w.klrow + align_up((size_t)R * sizeof(float));
+  w.mask = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
+  w.part = w.mask + align_up((size_t)((d->v_target + 31) / 32) * sizeof(uint32_t));
+  w.total = w.part;
   if (d->hidden_dim > 0) {
-    w.part = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
     const size_t nsl = (size_t)(vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
     w.total = w.part + align_up((size_t)R * nsl * sizeof(vsd::LmPartial));
   }
@@ -180,7 +189,7 @@ vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const
 // in la / lq.
 vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* params, const int32_t* valid_depth,
                                     const vsd_score_out* out, const float* la, const float* lq, float* loss_pos,
-                                    hipStream_t s) {
+                                    const float* kl_row, hipStream_t s) {
   vsd::CombineArgs ca{};
   ca.la = la;
   ca.lq = lq;
@@ -202,6 +211,9 @@ vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* para
   ca.mode = params->mode;
   ca.car_input = params->car_input;
   ca.inv_tau = 1.0f / params->car_tau;
+  ca.kl_row = kl_row;
+  ca.kl_pos = kl_row != nullptr ? out->kl_pos : nullptr;
+  ca.kl_weight = params->kl_weight;
   for (int l = 0; l < dims->L; ++l) ca.w[l] = (float)std::pow((double)params->w_base, (double)(l + 1));
   hipError_t e = vsd::launch_combine(ca, s);
   if (e != hipSuccess) return hip_fail(e, "k_combine launch");
@@ -367,6 +379,14 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
   if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
+  if (kl_on(params)) {
+    if (is_fused(dims))
+      return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
+    if (params->kl_topk > dims->v_draft)
+      return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d > v_draft=%d", params->kl_topk, dims->v_draft);
+    if (out->kl_idx == nullptr || out->kl_grad == nullptr)
+      return fail(VSD_ERR_NULL_POINTER, "out->kl_idx and out->kl_grad are required with kl_weight > 0");
+  }
   const WorkspaceLayout wl = workspace_layout(dims);
 
   char* ws = static_cast<char*>(workspace);
@@ -379,8 +399,22 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
     const int32_t* const tin[3] = {tok_draft, tok_target, tok_greedy};
     st = lm_forward(dims, params, draft, target, d2t, valid_depth, 0, 0, tin, nullptr, out, ws, wl, la, lq, s);
     if (st != VSD_OK) return st;
-    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s)) != VSD_OK) return st;
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s)) != VSD_OK)
+      return st;
     return ok();
+  }
+
+  float* kl_row = nullptr;
+  hipError_t e;
+  if (kl_on(params)) {
+    kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
+    if (d2t != nullptr) {
+      int32_t* inv = reinterpret_cast<int32_t*>(ws + wl.inv);
+      e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
+      if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
+      e = vsd::launch_map_mask(inv, dims->v_target, reinterpret_cast<uint32_t*>(ws + wl.mask), s);
+      if (e != hipSuccess) return hip_fail(e, "k_map_mask launch");
+    }
   }
 
   vsd::ScoreRowArgs ra{};
@@ -404,10 +438,19 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   ra.Vt = dims->v_target;
   ra.inv_tq = 1.0f / params->temp_draft;
   ra.inv_tp = 1.0f / params->temp_target;
-  hipError_t e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
+  if (kl_on(params)) {
+    ra.kl_k = params->kl_topk;
+    ra.map_mask = reinterpret_cast<const uint32_t*>(ws + wl.mask);
+    ra.inv = reinterpret_cast<const int32_t*>(ws + wl.inv);
+    ra.kl_idx = out->kl_idx;
+    ra.kl_grad = out->kl_grad;
+    ra.kl_row = kl_row;
+    ra.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
+  }
+  e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
   if (e != hipSuccess) return hip_fail(e, "k_score_rows launch");
 
-  vsd_status st2 = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s);
+  vsd_status st2 = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s);
   if (st2 != VSD_OK) return st2;
   return ok();
 }
@@ -425,6 +468,8 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
   if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
+  if (kl_on(params))
+    return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed by vsd_score_paths (set kl_weight = 0 here)");
 
   const WorkspaceLayout wl = workspace_layout(dims);
   char* ws = static_cast<char*>(workspace);
@@ -438,7 +483,8 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
     st = lm_forward(dims, params, draft, target, d2t, valid_depth, seed, offset, nullptr, tout, out, ws, wl, la,
                     lq, s);
     if (st != VSD_OK) return st;
-    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s)) != VSD_OK) return st;
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s)) != VSD_OK)
+      return st;
     return ok();
   }
 
@@ -473,15 +519,16 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   a.tblock = (int32_t)(512 * ((dims->v_target + 512 * nchunks - 1) / (512 * nchunks)));
   hipError_t e = vsd::launch_sample(a, dims->dtype == VSD_BF16, s);
   if (e != hipSuccess) return hip_fail(e, "k_sample (fused) launch");
-  st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, s);
+  st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s);
   if (st != VSD_OK) return st;
   return ok();
 }
 
 vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
                                  const float* lse_draft, const int32_t* tok_draft, const int32_t* tok_target,
-                                 const float* coef_a, const float* coef_b, const vsd_grad* grad,
-                                 int32_t* device_error, void* hip_stream) {
+                                 const float* coef_a, const float* coef_b, const int32_t* kl_idx,
+                                 const float* kl_grad, const vsd_grad* grad, int32_t* device_error,
+                                 void* hip_stream) {
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
   if ((st = check_params(params)) != VSD_OK) return st;
@@ -496,6 +543,12 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
   if (grad == nullptr || grad->grad_logits == nullptr) return fail(VSD_ERR_NULL_POINTER, "grad->grad_logits is NULL");
   if (!aligned16(grad->grad_logits)) return fail(VSD_ERR_MISALIGNED, "grad_logits not 16-byte aligned");
   if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+  if (kl_on(params)) {
+    if (is_fused(dims))
+      return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
+    if (kl_idx == nullptr || kl_grad == nullptr)
+      return fail(VSD_ERR_NULL_POINTER, "kl_idx and kl_grad are required with kl_weight > 0");
+  }
 
   if (is_fused(dims)) {
     // grad_logits receives g (bf16, stride ld_draft), then dH = g W_d
@@ -540,6 +593,11 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
   a.Vd = dims->v_draft;
   a.inv_tq = 1.0f / params->temp_draft;
   a.scale = params->loss_scale;
+  if (kl_on(params)) {
+    a.kl_idx = kl_idx;
+    a.kl_grad = kl_grad;
+    a.kl_k = params->kl_topk;
+  }
   hipError_t e = vsd::launch_bwd(a, dims->dtype == VSD_BF16, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "k_bwd launch");
   return ok();

@@ -43,6 +43,14 @@ struct ScoreRowArgs {
   int64_t R, ld_d, ld_t;
   int32_t L, Vd, Vt;
   float inv_tq, inv_tp;
+  // top-K renormalised KL term (kl_k > 0 turns it on)
+  int32_t kl_k;
+  const uint32_t* map_mask;  // [ceil(Vt/32)] bit t: target column t is mapped (with d2t)
+  const int32_t* inv;        // [Vt] draft index of target column t, -1 unmapped (with d2t)
+  int32_t* kl_idx;           // [R, kl_k]
+  float* kl_grad;            // [R, kl_k]
+  float* kl_row;             // [R]
+  float kl_gscale;           // loss_scale * kl_weight / N / T_q
 };
 
 struct CombineArgs {
@@ -63,6 +71,9 @@ struct CombineArgs {
   int32_t P, N, L;
   int32_t mode, car_input;
   float inv_tau;
+  const float* kl_row;       // [R] KL row terms, or null (term off)
+  float* kl_pos;             // optional [P]
+  float kl_weight;
   float w[kMaxL];            // w(l) = w_base^l, l = 1..L
 };
 
@@ -77,6 +88,9 @@ struct BwdArgs {
   int64_t R, ld;
   int32_t Vd;
   float inv_tq, scale;
+  const int32_t* kl_idx;     // [R, kl_k] or null: sparse KL gradient terms added to the row
+  const float* kl_grad;      // [R, kl_k]
+  int32_t kl_k;
 };
 
 // ------------------------------------------------ fused LM-head variant ---
@@ -168,6 +182,7 @@ hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s);
 hipError_t launch_loss_total(const float* loss_pos, int32_t P, float scale, float* out, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, bool bf16, hipStream_t s);
 

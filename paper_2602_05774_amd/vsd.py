@@ -54,10 +54,12 @@ class Params:
     mode: int = VSD_GRAD_ARW_CAR
     car_input: int = VSD_CAR_PROB
     loss_scale: float = 1.0
+    kl_weight: float = 0.0   # top-K renormalised KL term (VSD (KL)); 0 = off
+    kl_topk: int = 10
 
     def c(self):
         return _lib.VsdParams(self.temp_draft, self.temp_target, self.w_base, self.car_tau,
-                              self.mode, self.car_input, self.loss_scale)
+                              self.mode, self.car_input, self.loss_scale, self.kl_weight, self.kl_topk)
 
 
 @dataclass(frozen=True)
@@ -100,6 +102,10 @@ class ScoreResult(NamedTuple):
     loss_pos: torch.Tensor
     loss_total: torch.Tensor
     device_error: torch.Tensor
+    kl_idx: Optional[torch.Tensor] = None   # [R, K] int32 (KL term on)
+    kl_grad: Optional[torch.Tensor] = None  # [R, K] float32
+    kl_row: Optional[torch.Tensor] = None   # [R]
+    kl_pos: Optional[torch.Tensor] = None   # [P]
 
 
 def _ptr(t):
@@ -216,9 +222,11 @@ def _workspace_bytes(prob, X):
     return score_workspace_bytes(prob, X.dtype)
 
 
-def alloc_score_outputs(prob, device, full=True):
-    """Output tensors for score_paths (optional ones only when full=True)."""
+def alloc_score_outputs(prob, device, full=True, kl_topk=0):
+    """Output tensors for score_paths (optional ones only when full=True;
+    the KL term's arrays when kl_topk > 0)."""
     R, P, PN = prob.R, prob.P, prob.P * prob.N
+    K = int(kl_topk)
     f = lambda n: torch.empty(n, dtype=torch.float32, device=device)
     u8 = lambda n: torch.empty(n, dtype=torch.uint8, device=device)
     return ScoreResult(
@@ -228,7 +236,10 @@ def alloc_score_outputs(prob, device, full=True):
         accept_flag=u8(R) if full else None, valid_flag=u8(R) if full else None,
         o_prime=f(R) if full else None, beta=f(R) if full else None, zeta=f(R) if full else None,
         coef_a=f(R), coef_b=f(R), loss_pos=f(P) if full else None, loss_total=f(1),
-        device_error=torch.zeros(1, dtype=torch.int32, device=device))
+        device_error=torch.zeros(1, dtype=torch.int32, device=device),
+        kl_idx=torch.empty(R, K, dtype=torch.int32, device=device) if K else None,
+        kl_grad=torch.empty(R, K, dtype=torch.float32, device=device) if K else None,
+        kl_row=f(R) if K and full else None, kl_pos=f(P) if K and full else None)
 
 
 def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None, valid_depth=None,
@@ -243,7 +254,7 @@ def score_paths(prob, params, X, Y, tok_draft, tok_target, tok_greedy, d2t=None,
     _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
     dev = X.device
     if out is None:
-        out = alloc_score_outputs(prob, dev)
+        out = alloc_score_outputs(prob, dev, kl_topk=params.kl_topk if params.kl_weight > 0 else 0)
     nbytes = _workspace_bytes(prob, X)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -290,12 +301,13 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
 
 
 def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,
-                      grad=None, device_error=None):
+                      grad=None, device_error=None, kl_idx=None, kl_grad=None):
     """Gradient of loss_scale * sum_x L_x with respect to the draft logits
     (same shape, stride and dtype as X).  For an LmHead source, returns
     LmHeadGrad(grad_hidden [R, H], grad_logits [R, ld]): the logit gradient is
     written in bf16 and then contracted with the weight; `grad`, if given, is
-    such a pair to fill."""
+    such a pair to fill.  kl_idx / kl_grad (from score_paths' output) add the
+    top-K KL term's gradient when params.kl_weight > 0."""
     lib = _lib.load()
     _check_src("X", X, prob, prob.v_draft)
     dev = X.device
@@ -324,5 +336,6 @@ def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a,
         g = _lib.VsdGrad(grad.data_ptr(), None, None)
     _lib.check(lib.vsd_weighted_loss_bwd(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
                                          _ptr(lse_draft), _ptr(tok_draft), _ptr(tok_target), _ptr(coef_a),
-                                         _ptr(coef_b), ctypes.byref(g), _ptr(device_error), _stream(dev)))
+                                         _ptr(coef_b), _ptr(kl_idx), _ptr(kl_grad), ctypes.byref(g),
+                                         _ptr(device_error), _stream(dev)))
     return grad

@@ -64,7 +64,7 @@ def run_step(cfg, inp, params=None, tokens=None, fused=False):
     sc = vsd.score_paths(prob, params, inp["X"], inp["Y"], *tokens, inp["d2t"], inp["valid_depth"])
     grad = torch.full_like(inp["X"], SENTINEL)
     vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a, sc.coef_b,
-                          grad=grad)
+                          grad=grad, kl_idx=sc.kl_idx, kl_grad=sc.kl_grad)
     torch.cuda.synchronize()
     return dict(tokens=tokens, score=sc, grad=grad, err_sample=err_s)
 
@@ -83,7 +83,8 @@ def oracle_positions(cfg, inp, positions, params=None, tokens=None, want_grad=Tr
     if tokens is not None:
         tok = tuple(t.cpu().numpy()[rows] for t in tokens)
     p = dict(temp_draft=params.temp_draft, temp_target=params.temp_target, w_base=params.w_base,
-             car_tau=params.car_tau, mode=params.mode, car_input=params.car_input, loss_scale=params.loss_scale)
+             car_tau=params.car_tau, mode=params.mode, car_input=params.car_input, loss_scale=params.loss_scale,
+             kl_weight=params.kl_weight, kl_topk=params.kl_topk)
     ora = reference.run_positions(X, Y, d2t, depth, list(positions), cfg.N, cfg.L, p, seed=cfg.philox_seed,
                                   offset=cfg.philox_offset, tokens=tok, want_grad=want_grad)
     return rows, ora

@@ -36,7 +36,7 @@ def test_every_declared_function_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.vsd_abi_version() == 1
+    assert lib.vsd_abi_version() == 2
     for code, name in _lib.STATUS_NAMES.items():
         assert lib.vsd_status_string(code).decode() == name
     assert lib.vsd_status_string(99).decode() == "VSD_ERR_UNKNOWN"
@@ -119,8 +119,8 @@ def test_score_rejects_missing_required_outputs_and_small_workspace(lib):
 def test_bwd_rejects_bad_arguments(lib):
     src = _lib.VsdSrc(FAKE, None, None)
     g = _lib.VsdGrad(FAKE, None, None)
-    call = lambda dims, params, grad, err=FAKE, lse=FAKE: lib.vsd_weighted_loss_bwd(
-        ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src), lse, FAKE, FAKE, FAKE, FAKE,
+    call = lambda dims, params, grad, err=FAKE, lse=FAKE, kl=(None, None): lib.vsd_weighted_loss_bwd(
+        ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src), lse, FAKE, FAKE, FAKE, FAKE, *kl,
         ctypes.byref(grad), err, None)
     assert call(_dims(L=0), _params(), g) == 2
     assert call(_dims(), _params(temp_draft=0.0), g) == 3
@@ -128,6 +128,7 @@ def test_bwd_rejects_bad_arguments(lib):
     assert call(_dims(), _params(), _lib.VsdGrad(FAKE + 2, None, None)) == 4
     assert call(_dims(), _params(), g, err=None) == 1
     assert call(_dims(), _params(), g, lse=None) == 1
+    assert call(_dims(), _params(kl_weight=0.5, kl_topk=10), g) == 1            # KL on: kl_idx / kl_grad required
 
 
 def test_workspace_query_scales_with_rows(lib):
@@ -191,15 +192,38 @@ def test_fused_lm_head_validation(lib):
     plain, fused = ctypes.c_size_t(), ctypes.c_size_t()
     assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), ctypes.byref(plain)) == 0
     assert lib.vsd_score_workspace_bytes(ctypes.byref(fdims()), ctypes.byref(fused)) == 0
-    assert fused.value >= plain.value + 24 * 32 + 1000 * 4
+    assert fused.value >= plain.value + 24 * 2 * 32      # two slice partials of 32 bytes per row
     assert score(fdims(), ws_bytes=fused.value - 1) == 7
     # backward: grad_hidden required, grad_weight unsupported, ld_draft checked
     def bwd(dims, grad):
         return lib.vsd_weighted_loss_bwd(ctypes.byref(dims), ctypes.byref(_params()), ctypes.byref(head), FAKE,
-                                         FAKE, FAKE, FAKE, FAKE, ctypes.byref(grad), FAKE, None)
+                                         FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(grad), FAKE, None)
     assert bwd(fdims(), _lib.VsdGrad(FAKE, None, None)) == 1
     assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE + 8, None)) == 4
     assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE, FAKE)) == 6
     assert bwd(fdims(ld_draft=999), _lib.VsdGrad(FAKE, FAKE, None)) == 2
     assert bwd(fdims(ld_draft=1004), _lib.VsdGrad(FAKE, FAKE, None)) == 2   # 2008 bytes: not 16-B rows
     assert bwd(fdims(), _lib.VsdGrad(None, FAKE, None)) == 1
+
+
+def test_kl_term_validation(lib):
+    """kl_weight / kl_topk checks and the entry points that do not compute the term."""
+    for kw in (dict(kl_weight=-0.1), dict(kl_weight=float("nan")), dict(kl_weight=0.5, kl_topk=0),
+               dict(kl_weight=0.5, kl_topk=17)):
+        assert _score(lib, params=_params(**kw)) == 3
+    # kl_topk beyond the draft vocabulary
+    assert _score(lib, dims=_dims(v_draft=8, v_target=8, ld_draft=8, ld_target=8),
+                  params=_params(kl_weight=0.5, kl_topk=9)) == 3
+    # kl_idx / kl_grad required
+    assert _score(lib, params=_params(kl_weight=0.5, kl_topk=10)) == 1
+    full = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE, kl_idx=FAKE, kl_grad=FAKE)
+    head = _lib.VsdSrc(None, FAKE, FAKE)
+    fdims = _dims(dtype=_lib.VSD_BF16, hidden_dim=128)
+    pr = _params(kl_weight=0.5, kl_topk=10)
+    st = lib.vsd_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head), None,
+                             None, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
+    assert st == 6                                   # fused LM head: not with the KL term
+    src = _lib.VsdSrc(FAKE, None, None)
+    st = lib.vsd_sample_score_paths(ctypes.byref(_dims()), ctypes.byref(pr), ctypes.byref(src), ctypes.byref(src),
+                                    None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
+    assert st == 6                                   # one-pass call: not with the KL term

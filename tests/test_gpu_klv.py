@@ -1,0 +1,74 @@
+"""GPU parity of the top-K renormalised KL term (VSD (KL), Eq. klv) against the
+oracle (oracle/klv.py through reference.run_positions).
+
+The top-K sets are integers and compared exactly (order included: larger
+target logit first, equal logits by the smaller draft index; C4's bf16 target
+rows have real ties).  The row terms, the per-position averages, the loss with
+the term, the sparse gradient coefficients and the full gradient rows are
+compared under the materialised path's bars.  Cases: C1 in full (fp32,
+shared vocabulary), C3-recipe rows at the full vocabularies (mapped: mask and
+inverse map), C4-recipe rows (ragged, peaked bf16 with ties, T_q = 0.5),
+K = 1 and K = 16, a draft vocabulary of exactly K tokens.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_05774_amd as vsd
+from synth import CONFIGS, make_inputs, make_inputs_numpy_c1, scaled
+from tests.gpu_common import compare, log, oracle_positions, params_of, run_step
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _lin_ok(got, ref):
+    return np.abs(got - ref) <= 1e-3 * np.abs(ref) + 1e-6
+
+
+def check_kl(cfg, inp, positions, params, label):
+    log(f"[{label}] KL term K={params.kl_topk} weight={params.kl_weight}")
+    gpu = run_step(cfg, inp, params)
+    assert int(gpu["score"].device_error.item()) == 0 and int(gpu["err_sample"].item()) == 0
+    rows, ora = oracle_positions(cfg, inp, positions, params)
+    summary = compare(cfg, gpu, rows, ora, positions, label=label)
+    sc = gpu["score"]
+    idx = sc.kl_idx.cpu().numpy()[rows]
+    bad = np.argwhere(idx != ora["kl_idx"])
+    assert bad.size == 0, f"{label} kl_idx: first mismatch row {rows[bad[0][0]]}: gpu {idx[bad[0][0]]} oracle {ora['kl_idx'][bad[0][0]]}"
+    for name, got, ref in (("kl_row", sc.kl_row.cpu().numpy()[rows], ora["kl_row"]),
+                           ("kl_grad", sc.kl_grad.cpu().numpy()[rows], ora["kl_grad"]),
+                           ("kl_pos", sc.kl_pos.cpu().numpy()[np.asarray(positions)], ora["kl_pos"])):
+        ok = _lin_ok(got, ref)
+        assert ok.all(), f"{label} {name}: max err {np.max(np.abs(got - ref))}"
+    log(f"[{label}] ok: {summary['worst']}")
+    return summary
+
+
+def test_c1_full_with_kl():
+    cfg = CONFIGS["C1"]
+    host = make_inputs_numpy_c1(cfg)
+    inp = {"X": torch.as_tensor(host["X"]).to(DEV), "Y": torch.as_tensor(host["Y"]).to(DEV), "d2t": None,
+           "valid_depth": None}
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.3, kl_topk=10), "C1 KL")
+
+
+def test_mapped_full_vocabularies_with_kl():
+    cfg = scaled("C3", B=1, T=3)
+    inp = make_inputs(cfg, DEV)
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.5, kl_topk=10), "C3s KL")
+
+
+@pytest.mark.parametrize("K", [1, 16])
+def test_ragged_peaked_ties_with_kl(K):
+    cfg = scaled("C4", B=1, T=3, v_draft=4000, v_target=4000)
+    inp = make_inputs(cfg, DEV)
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=1.5, kl_topk=K, loss_scale=0.5),
+             f"C4s KL K={K}")
+
+
+def test_vocabulary_of_exactly_k_tokens():
+    cfg = scaled("C2", B=1, T=2, N=3, L=2, v_draft=16, v_target=16)
+    inp = make_inputs(cfg, DEV)
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.8, kl_topk=16), "V=K KL")
