@@ -8,7 +8,8 @@ bf16 logits already resident in HBM, synthetic and seeded.  One step = every
 row of the batch through vsd_sample_score_paths (E-step draws and path
 scoring in one pass over the logits) and vsd_weighted_loss_bwd on one stream.
 The same step through the three separate calls (vsd_sample_paths,
-vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it.
+vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it,
+and once more with the top-K renormalised KL term on (K = 10, "kl_variant").
 W untimed steps, then exactly K steps timed between stream synchronisations;
 per-call durations come from HIP events recorded on the stream the kernels
 run on.
@@ -326,7 +327,29 @@ def main():
         total = sum(e[0].elapsed_time(e[nev - 1]) for e in evs) / args.steps
         return seg, total, wall
 
+    params_kl = vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target, kl_weight=0.1, kl_topk=10)
+    out_kl = vsd.alloc_score_outputs(prob, dev, kl_topk=params_kl.kl_topk)
+
+    def step_kl(ev=None):
+        """The three-call step with the top-K renormalised KL term on."""
+        if ev:
+            ev[0].record()
+        s = vsd.sample_paths(prob, X, Y, d2t, depth, cfg.temp_draft, cfg.temp_target, cfg.philox_seed,
+                             cfg.philox_offset, device_error=err)
+        if ev:
+            ev[1].record()
+        vsd.score_paths(prob, params_kl, X, Y, s.tok_draft, s.tok_target, s.tok_greedy, d2t, depth, out=out_kl,
+                        workspace=ws)
+        if ev:
+            ev[2].record()
+        vsd.weighted_loss_bwd(prob, params_kl, X, out_kl.lse_draft, s.tok_draft, s.tok_target, out_kl.coef_a,
+                              out_kl.coef_b, grad=grad, device_error=err, kl_idx=out_kl.kl_idx,
+                              kl_grad=out_kl.kl_grad)
+        if ev:
+            ev[3].record()
+
     (t_sample3, t_score3, t_bwd3), t_step3, _ = timed(step_three_calls, 4)
+    (_, t_score_kl, t_bwd_kl), t_step_kl, _ = timed(step_kl, 4)
     (t_ss, t_bwd), t_step, wall = timed(step_fused, 3)
     if int(err.item()) != 0 or int(out.device_error.item()) != 0:
         raise RuntimeError("device error reported during the benchmark")
@@ -357,6 +380,10 @@ def main():
     ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4) + 6.0 * 2 * cfg.v_draft)
     kernels["sample_score"]["valu_lane_ops"] = ss_ops
     kernels["sample_score"]["TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
+    kl_variant = {"kl_topk": params_kl.kl_topk, "kl_weight": params_kl.kl_weight, "ms_per_step": t_step_kl,
+                  "score_ms": t_score_kl, "score_GB/s": gbs(ss_bytes, t_score_kl),
+                  "bwd_ms": t_bwd_kl, "bwd_GB/s": gbs(bwd_bytes, t_bwd_kl),
+                  "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score_kl + t_bwd_kl) / HBM_PEAK_GBS}
     dominant = "sample_score" if t_ss >= t_bwd else "bwd"
     k = kernels[dominant]
     if dominant == "sample_score":
@@ -375,10 +402,11 @@ def main():
         "config": {"workload": f"{cfg.name}: B={cfg.B} T={cfg.T} N={cfg.N} L={cfg.L} "
                                f"V_target={cfg.v_target} V_draft={cfg.v_draft} logits={cfg.dtype}",
                    "path_tokens_per_step": live, "parallelism": "single GPU"},
-        "kernels": kernels, "three_calls": three_calls, "roofline": roof, "cpu_baseline": base,
+        "kernels": kernels, "three_calls": three_calls, "kl_variant": kl_variant, "roofline": roof,
+        "cpu_baseline": base,
     }
     if not args.no_lm_head:
-        del inp, X, Y, out, ws, grad
+        del inp, X, Y, out, out_kl, ws, grad
         torch.cuda.empty_cache()
         line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
     print(json.dumps(line), flush=True)

@@ -103,23 +103,23 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
 }
 
 // row_lse of the target row, also offering every mapped column to a
-// wavefront top-K (value = raw target logit, index = its draft index).
+// wavefront top-K (value = raw target logit, index = its draft index).  Four
+// chunks are in flight per lane as in row_lse; a chunk's 8 elements are
+// offered only when some lane's largest mapped value reaches the threshold
+// (one ballot per chunk once the threshold has risen).
 template <typename T, bool MAPPED>
 __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const uint32_t* mask,
                                const int32_t* inv) {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
+  constexpr int U = 4;
   constexpr int step = 8 * kWave;
   auto idx_of = [&](int col) { return MAPPED ? inv[col] : col; };
-  for (int chunk = 0; chunk < V; chunk += step) {
-    const int base = chunk + lane * 8;
-    const int nvalid = min(8, V - base);
-    float x[8];
-    if (nvalid >= 8) {
-      load8(row + base, x);
-    } else {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) x[k] = k < nvalid ? load1(row + base + k) : -INFINITY;
-    }
+  auto bits_of = [&](int base, int nvalid) -> uint32_t {
+    if (nvalid <= 0) return 0u;
+    const uint32_t keep = nvalid >= 8 ? 0xFFu : ((1u << nvalid) - 1u);
+    return MAPPED ? ((mask[base >> 5] >> (base & 31)) & keep) : keep;
+  };
+  auto fold = [&](int base, const float (&x)[8], uint32_t bits) {
     float cm = x[0];
 #pragma unroll
     for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
@@ -131,11 +131,32 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -mc));
-    uint32_t mbits = nvalid > 0 ? 0xFFu : 0u;
-    if (MAPPED && nvalid > 0) mbits = (mask[base >> 5] >> (base & 31)) & 0xFFu;
-    tk.reserve(step, lane);
+    tk.offer8(x, base, bits, idx_of, lane);
+  };
+  int chunk = 0;
+  for (; chunk + U * step <= V; chunk += U * step) {
+    float x[U][8];
+    uint32_t bits[U];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) tk.offer(x[k], base + k, k < nvalid && ((mbits >> k) & 1u), idx_of, lane);
+    for (int u = 0; u < U; ++u) {
+      const int base = chunk + u * step + lane * 8;
+      load8(row + base, x[u]);
+      bits[u] = bits_of(base, 8);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) fold(chunk + u * step + lane * 8, x[u], bits[u]);
+  }
+  for (; chunk < V; chunk += step) {
+    const int base = chunk + lane * 8;
+    const int nvalid = min(8, V - base);
+    float x[8];
+    if (nvalid >= 8) {
+      load8(row + base, x);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = k < nvalid ? load1(row + base + k) : -INFINITY;
+    }
+    fold(base, x, bits_of(base, nvalid));
   }
   wave_lse2(mc, s);
   mraw = wave_max(mraw);

@@ -1,15 +1,15 @@
 // Exact top-K of (value, index) pairs offered by one wavefront, K <= kMaxTopK.
 //
 // Order: the larger value first, equal values by the smaller index.  An offer
-// qualifies only if it beats the current K-th best (a wavefront-uniform
-// threshold, -inf until K entries are known); qualifying offers are appended
-// to a per-wavefront LDS buffer at positions given by a ballot prefix count.
-// When the next round of offers could overflow the buffer the wavefront
-// selects the K best buffered entries (K rounds of wavefront argmax), keeps
-// them at the front in order and raises the threshold.  An element that fails
-// the threshold is worse than K known elements, so it cannot be in the final
-// top K: the result is exact.  After finish() the K best are at the front of
-// the buffer, in order.  Values must not be -inf (sentinel of empty slots).
+// takes part only if it is not below the current K-th best (a
+// wavefront-uniform threshold, -inf until K entries are known); such offers
+// are appended to a per-wavefront LDS buffer at positions given by a
+// wavefront prefix sum.  Whenever more than 64 entries are buffered the
+// wavefront selects the K best (K rounds of wavefront argmax), keeps them at
+// the front in order and raises the threshold.  An element below the
+// threshold is worse than K known elements, so it cannot be in the final top
+// K: the result is exact.  After finish() the K best are at the front of the
+// buffer, in order.  Values must not be -inf (sentinel of empty slots).
 #pragma once
 
 #include "vsd_device.hpp"
@@ -17,7 +17,7 @@
 namespace vsd {
 
 constexpr int kMaxTopK = 16;
-constexpr int kTopKCap = 1024;  // entries per wavefront buffer
+constexpr int kTopKCap = 640;   // entries per wavefront buffer (a full round of 8 offers per lane fits)
 
 struct WaveTopK {
   float* bv;   // LDS [kTopKCap]
@@ -40,57 +40,66 @@ struct WaveTopK {
     thi = 0x7FFFFFFF;
   }
 
-  // One offer per lane: value v of column col (valid lanes only); idx_of(col)
-  // gives the index the order and the result use (evaluated for lanes that
-  // reach the threshold only).  At most 64 entries are appended.
+  // Offer a lane's 8 values x of columns base .. base+7 (bit k of `bits`:
+  // column base+k takes part).  A value equal to the threshold is appended
+  // too (its index decides at the next compaction).  Returns at once when no
+  // lane has a candidate; idx_of(col) gives the index kept with an entry.
   template <class IdxOf>
-  __device__ __forceinline__ void offer(float v, int col, bool valid, IdxOf idx_of, int lane) {
-    bool q = valid && v >= thv;
-    if (__ballot(q) == 0ull) return;
-    int idx = 0x7FFFFFFF;
-    if (q) {
-      idx = idx_of(col);
-      q = beats(v, idx, thv, thi);
-    }
-    const uint64_t m = __ballot(q);
-    if (m == 0ull) return;
-    if (q) {
-      const int pos = n + (int)__builtin_popcountll(m & ((1ull << lane) - 1ull));
-      bv[pos] = v;
-      bi[pos] = idx;
-    }
-    n += (int)__builtin_popcountll(m);
-  }
-
-  // Room for `upcoming` more entries, compacting first if needed.
-  __device__ __forceinline__ void reserve(int upcoming, int lane) {
-    if (n + upcoming > kTopKCap) compact(lane);
-  }
-
-  // Keep the K best buffered entries, in order, at the front.
-  __device__ void compact(int lane) {
-    constexpr int kPer = kTopKCap / kWave;
-    float ev[kPer];
-    int ei[kPer];
-    const int nt = (n + kWave - 1) / kWave;
+  __device__ __forceinline__ void offer8(const float (&x)[8], int base, uint32_t bits, IdxOf idx_of, int lane) {
+    float best = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < kPer; ++t) {
-      const int j = lane + kWave * t;
-      const bool in = t < nt && j < n;
-      ev[t] = in ? bv[j] : -INFINITY;
-      ei[t] = in ? bi[j] : 0x7FFFFFFF;
+    for (int k = 0; k < 8; ++k) best = ((bits >> k) & 1u) ? fmaxf(best, x[k]) : best;
+    if (__ballot(best >= thv) == 0ull) return;
+    append8(x, base, bits, idx_of, lane);
+  }
+
+  template <class IdxOf>
+  __device__ void append8(const float (&x)[8], int base, uint32_t bits, IdxOf idx_of, int lane) {
+    uint32_t q = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) q |= (((bits >> k) & 1u) && x[k] >= thv) ? (1u << k) : 0u;
+    const int cnt = __builtin_popcount(q);
+    int incl = cnt;  // inclusive prefix sum of cnt over the lanes
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
+    }
+    const int total = __shfl(incl, kWave - 1, kWave);
+    if (n + total > kTopKCap) compact(lane);
+    int pos = n + incl - cnt;
+    for (int k = 0; k < 8; ++k) {
+      if ((q >> k) & 1u) {
+        bv[pos] = x[k];
+        bi[pos] = idx_of(base + k);
+        ++pos;
+      }
+    }
+    n += total;
+    if (n > kWave) compact(lane);  // keeps the threshold close to the K-th best so far
+  }
+
+  // Keep the K best buffered entries, in order, at the front.  Selected
+  // entries are marked in LDS (value -inf); the K winners are written after
+  // the last scan.
+  __device__ void compact(int lane) {
+    if (n <= kWave) {
+      compact_small(lane);
+      return;
     }
     float kv = -INFINITY;
     int ki = 0x7FFFFFFF;
     int cnt = 0;
     for (int r = 0; r < K; ++r) {
       float lv = -INFINITY;
-      int li = 0x7FFFFFFF;
-#pragma unroll
-      for (int t = 0; t < kPer; ++t) {
-        if (t < nt && beats(ev[t], ei[t], lv, li)) {
-          lv = ev[t];
-          li = ei[t];
+      int li = 0x7FFFFFFF, lj = -1;
+      for (int j = lane; j < n; j += kWave) {
+        const float v = bv[j];
+        const int i = bi[j];
+        if (beats(v, i, lv, li)) {
+          lv = v;
+          li = i;
+          lj = j;
         }
       }
       float wv = lv;
@@ -104,14 +113,48 @@ struct WaveTopK {
           wi = oi;
         }
       }
-      if (wv == -INFINITY) break;  // fewer than K entries buffered
-      // indices are unique, so exactly one entry matches the winner
+      if (wv == -INFINITY) break;
+      if (lj >= 0 && li == wi && lv == wv) bv[lj] = -INFINITY;  // indices are unique: one owner
+      if (lane == r) {
+        kv = wv;
+        ki = wi;
+      }
+      ++cnt;
+    }
+    if (lane < cnt) {
+      bv[lane] = kv;
+      bi[lane] = ki;
+    }
+    n = cnt;
+    if (cnt == K) {
+      thv = __shfl(kv, K - 1, kWave);
+      thi = __shfl(ki, K - 1, kWave);
+    }
+  }
+
+  // compact() for at most one entry per lane.
+  __device__ void compact_small(int lane) {
+    float ev = lane < n ? bv[lane] : -INFINITY;
+    int ei = lane < n ? bi[lane] : 0x7FFFFFFF;
+    float kv = -INFINITY;
+    int ki = 0x7FFFFFFF;
+    int cnt = 0;
+    for (int r = 0; r < K; ++r) {
+      float wv = ev;
+      int wi = ei;
 #pragma unroll
-      for (int t = 0; t < kPer; ++t) {
-        if (t < nt && ei[t] == wi && ev[t] == wv) {
-          ev[t] = -INFINITY;
-          ei[t] = 0x7FFFFFFF;
+      for (int off = 32; off >= 1; off >>= 1) {
+        const float ov = __shfl_xor(wv, off, kWave);
+        const int oi = __shfl_xor(wi, off, kWave);
+        if (beats(ov, oi, wv, wi)) {
+          wv = ov;
+          wi = oi;
         }
+      }
+      if (wv == -INFINITY) break;
+      if (ei == wi && ev == wv) {
+        ev = -INFINITY;
+        ei = 0x7FFFFFFF;
       }
       if (lane == r) {
         kv = wv;
@@ -119,7 +162,6 @@ struct WaveTopK {
       }
       ++cnt;
     }
-    // this wavefront's LDS reads above precede these writes (in order)
     if (lane < cnt) {
       bv[lane] = kv;
       bi[lane] = ki;
