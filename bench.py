@@ -9,7 +9,8 @@ row of the batch through vsd_sample_score_paths (E-step draws and path
 scoring in one pass over the logits) and vsd_weighted_loss_bwd on one stream.
 The same step through the three separate calls (vsd_sample_paths,
 vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it,
-and once more with the top-K renormalised KL term on (K = 10, "kl_variant").
+and the step once more, both ways, with the top-K renormalised KL term on
+(K = 10, "kl_variant").
 W untimed steps, then exactly K steps timed between stream synchronisations;
 per-call durations come from HIP events recorded on the stream the kernels
 run on.
@@ -348,10 +349,27 @@ def main():
         if ev:
             ev[3].record()
 
+    tok_kl = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+
+    def step_kl_fused(ev=None):
+        """The one-pass step with the top-K renormalised KL term on."""
+        if ev:
+            ev[0].record()
+        vsd.sample_score_paths(prob, params_kl, X, Y, d2t, depth, cfg.philox_seed, cfg.philox_offset, out=out_kl,
+                               workspace=ws, tokens=tok_kl)
+        if ev:
+            ev[1].record()
+        vsd.weighted_loss_bwd(prob, params_kl, X, out_kl.lse_draft, tok_kl[0], tok_kl[1], out_kl.coef_a,
+                              out_kl.coef_b, grad=grad, device_error=err, kl_idx=out_kl.kl_idx,
+                              kl_grad=out_kl.kl_grad)
+        if ev:
+            ev[2].record()
+
     (t_sample3, t_score3, t_bwd3), t_step3, _ = timed(step_three_calls, 4)
     (_, t_score_kl, t_bwd_kl), t_step_kl, _ = timed(step_kl, 4)
+    (t_ss_kl, t_bwd_kl1), t_step_kl1, _ = timed(step_kl_fused, 3)
     (t_ss, t_bwd), t_step, wall = timed(step_fused, 3)
-    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0 or int(out_kl.device_error.item()) != 0:
         raise RuntimeError("device error reported during the benchmark")
 
     live = prob.R if depth is None else int((tok[0] >= 0).sum().item())
@@ -380,10 +398,14 @@ def main():
     ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4) + 6.0 * 2 * cfg.v_draft)
     kernels["sample_score"]["valu_lane_ops"] = ss_ops
     kernels["sample_score"]["TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
-    kl_variant = {"kl_topk": params_kl.kl_topk, "kl_weight": params_kl.kl_weight, "ms_per_step": t_step_kl,
-                  "score_ms": t_score_kl, "score_GB/s": gbs(ss_bytes, t_score_kl),
-                  "bwd_ms": t_bwd_kl, "bwd_GB/s": gbs(bwd_bytes, t_bwd_kl),
-                  "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score_kl + t_bwd_kl) / HBM_PEAK_GBS}
+    kl_variant = {"kl_topk": params_kl.kl_topk, "kl_weight": params_kl.kl_weight,
+                  "one_pass": {"ms_per_step": t_step_kl1, "path_tokens_per_s": live / (t_step_kl1 * 1e-3),
+                               "sample_score_ms": t_ss_kl, "bwd_ms": t_bwd_kl1},
+                  "three_calls": {"ms_per_step": t_step_kl, "score_ms": t_score_kl,
+                                  "score_GB/s": gbs(ss_bytes, t_score_kl), "bwd_ms": t_bwd_kl,
+                                  "bwd_GB/s": gbs(bwd_bytes, t_bwd_kl),
+                                  "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score_kl + t_bwd_kl)
+                                  / HBM_PEAK_GBS}}
     dominant = "sample_score" if t_ss >= t_bwd else "bwd"
     k = kernels[dominant]
     if dominant == "sample_score":

@@ -161,9 +161,10 @@
  *   loss_pos[x] = L_x + kl_weight KL_x.  The gradient gains
  *   kl_grad[r][k] = loss_scale kl_weight / N (q_hat - p_hat)(Omega_r[k]) / T_q
  *   at draft index kl_idx[r][k] = Omega_r[k]; vsd_weighted_loss_bwd adds
- *   these when given kl_idx and kl_grad.  K <= v_draft.  Computed by
- *   vsd_score_paths on materialised logits (the one-pass and fused LM-head
- *   calls return VSD_ERR_UNSUPPORTED with kl_weight > 0).
+ *   these when given kl_idx and kl_grad.  K <= v_draft.  Computed on
+ *   materialised logits by vsd_score_paths and vsd_sample_score_paths (same
+ *   outputs, same results); with the fused LM head (hidden_dim > 0) both
+ *   return VSD_ERR_UNSUPPORTED when kl_weight > 0.
  */
 #ifndef VSD_H
 #define VSD_H

@@ -31,8 +31,14 @@
 // per-row LDS tile.  Chunks are software pipelined: the next chunk's map
 // entries and rows are loaded while the current chunk is drawn, and the target
 // gathers of the next chunk are issued at the end of the current one.
+//
+// With the top-K renormalised KL term (one-pass mode), the target wavefront
+// also offers each chunk's mapped target logits, already in draft-index
+// order, to an exact wavefront top-K (vsd_topk.hpp) and, after the row, forms
+// the term over the K (as k_score_rows does).
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
+#include "vsd_topk.hpp"
 
 namespace vsd {
 
@@ -229,9 +235,10 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
 
 // The target wavefront of a row: z' and z-bar and, fused, the target
 // log-sum-exp (unmapped) or the other half of the target stream (mapped).
-template <typename T, bool MAPPED, bool FUSED>
+template <typename T, bool MAPPED, bool FUSED, bool KL>
 __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int Vt, FamilyDraw& f, Best& bg,
-                            LaneLse& lp, bool& map_bad, int lane) {
+                            LaneLse& lp, bool& map_bad, WaveTopK& tk, int lane) {
+  auto same = [](int col) { return col; };
   const int nfull = Vd / kChunk;
   auto greedy = [&](int base, const float (&y)[8], int nvalid) {
 #pragma unroll
@@ -295,6 +302,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       }
       greedy(base, y, 8);
       f.draw(base, y, 8);
+      if (KL) tk.offer8(y, base, 0xFFu, same, lane);
       if (next) {
         if (MAPPED)
           gather(tn);
@@ -332,6 +340,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
     if (FUSED && !MAPPED) lp.add8(y, f.c2);
     greedy(base, y, nvalid);
     f.draw(base, y, nvalid);
+    if (KL) tk.offer8(y, base, nvalid > 0 ? (1u << nvalid) - 1u : 0u, same, lane);
   }
   if (FUSED && MAPPED) {  // target elements past the last chunk's block: odd half-blocks
     const int nchunks = (Vd + kChunk - 1) / kChunk;
@@ -340,10 +349,12 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
   }
 }
 
-template <typename T, bool MAPPED, bool FUSED>
+template <typename T, bool MAPPED, bool FUSED, bool KL>
 __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   __shared__ __align__(16) T ytile[kRowsPerBlock][kChunk];
   __shared__ RowShared sh[kRowsPerBlock];
+  __shared__ float kl_bv[KL ? kRowsPerBlock * kTopKCap : 1];
+  __shared__ int kl_bi[KL ? kRowsPerBlock * kTopKCap : 1];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x >> 6;
   const int slot = wave >> 1;       // row within the block
@@ -389,8 +400,15 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
       FamilyDraw f{(uint32_t)r, 1u, a.offset, a.k0, a.k1, a.inv_tp, cp2};
       Best bg{-INFINITY, 0x7FFFFFFF};
       bool map_bad = false;
-      target_wave<T, MAPPED, FUSED>(Y, a.d2t, ytile[slot], a.Vd, a.Vt, f, bg, lp, map_bad, lane);
+      WaveTopK tk;
+      if (KL) tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
+      target_wave<T, MAPPED, FUSED, KL>(Y, a.d2t, ytile[slot], a.Vd, a.Vt, f, bg, lp, map_bad, tk, lane);
       if (map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
+      if (KL) {
+        tk.finish(lane);
+        kl_row_term(tk, X, a.Vd, a.inv_tq, a.inv_tp, a.kl_gscale, a.kl_idx + r * a.kl_k, a.kl_grad + r * a.kl_k,
+                    a.kl_row + r, lane);
+      }
       wave_argmax(f.best.key, f.best.idx);
       wave_argmax(bg.key, bg.idx);
       if (FUSED) lp.reduce();
@@ -421,6 +439,13 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
         a.lse_q[r] = 0.0f;
         if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
       }
+    }
+    if (KL) {
+      if (lane < a.kl_k) {
+        a.kl_idx[r * a.kl_k + lane] = -1;
+        a.kl_grad[r * a.kl_k + lane] = 0.0f;
+      }
+      if (lane == 0) a.kl_row[r] = 0.0f;
     }
     return;
   }
@@ -458,13 +483,13 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   }
 }
 
-template <typename T, bool FUSED>
+template <typename T, bool FUSED, bool KL>
 hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
   if (a.d2t != nullptr)
-    hipLaunchKernelGGL((k_sample<T, true, FUSED>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_sample<T, true, FUSED, KL>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_sample<T, false, FUSED>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_sample<T, false, FUSED, KL>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -472,8 +497,13 @@ hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s) {
   const bool fused = a.lse_q != nullptr;
-  if (bf16) return fused ? launch_t<bf16_t, true>(a, s) : launch_t<bf16_t, false>(a, s);
-  return fused ? launch_t<float, true>(a, s) : launch_t<float, false>(a, s);
+  const bool kl = fused && a.kl_k > 0;
+  if (bf16) {
+    if (kl) return launch_t<bf16_t, true, true>(a, s);
+    return fused ? launch_t<bf16_t, true, false>(a, s) : launch_t<bf16_t, false, false>(a, s);
+  }
+  if (kl) return launch_t<float, true, true>(a, s);
+  return fused ? launch_t<float, true, false>(a, s) : launch_t<float, false, false>(a, s);
 }
 
 }  // namespace vsd

@@ -236,26 +236,9 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
     if (a.lse_p != nullptr) a.lse_p[r] = lse_p;
   }
   if (KL) {
-    // lane k < K holds the k-th of the top K: p_hat and q_hat renormalised
-    // over the K, the row term -sum p_hat log q_hat and its gradient
-    // coefficients loss_scale * kl_weight / N * (q_hat - p_hat) / T_q
     tk.finish(lane);
-    const bool mine = lane < a.kl_k;
-    const int v = mine ? tk.bi[lane] : 0;
-    const float pa = mine ? tk.bv[lane] * a.inv_tp : -INFINITY;
-    const float qa = mine ? load1(X + v) * a.inv_tq : -INFINITY;
-    const float pm = wave_max(pa), qm = wave_max(qa);
-    const float pe = mine ? expf(pa - pm) : 0.0f;
-    const float qe = mine ? expf(qa - qm) : 0.0f;
-    const float ps = wave_sum(pe), qs = wave_sum(qe);
-    const float p_hat = pe / ps, q_hat = qe / qs;
-    const float log_q_hat = qa - qm - logf(qs);
-    const float term = wave_sum(mine ? -p_hat * log_q_hat : 0.0f);
-    if (mine) {
-      a.kl_idx[r * a.kl_k + lane] = v;
-      a.kl_grad[r * a.kl_k + lane] = a.kl_gscale * (q_hat - p_hat);
-    }
-    if (lane == 0) a.kl_row[r] = term;
+    kl_row_term(tk, X, a.Vd, a.inv_tq, a.inv_tp, a.kl_gscale, a.kl_idx + r * a.kl_k, a.kl_grad + r * a.kl_k,
+                a.kl_row + r, lane);
   }
 }
 

@@ -185,6 +185,17 @@ vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const
   return VSD_OK;
 }
 
+// Validation of the KL outputs (kl_weight > 0) shared by the scoring calls.
+vsd_status check_kl_out(const vsd_dims* dims, const vsd_params* params, const vsd_score_out* out) {
+  if (!kl_on(params)) return VSD_OK;
+  if (is_fused(dims)) return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
+  if (params->kl_topk > dims->v_draft)
+    return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d > v_draft=%d", params->kl_topk, dims->v_draft);
+  if (out->kl_idx == nullptr || out->kl_grad == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "out->kl_idx and out->kl_grad are required with kl_weight > 0");
+  return VSD_OK;
+}
+
 // The per-position combine (and the loss total) over row statistics already
 // in la / lq.
 vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* params, const int32_t* valid_depth,
@@ -379,14 +390,7 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
   if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
-  if (kl_on(params)) {
-    if (is_fused(dims))
-      return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
-    if (params->kl_topk > dims->v_draft)
-      return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d > v_draft=%d", params->kl_topk, dims->v_draft);
-    if (out->kl_idx == nullptr || out->kl_grad == nullptr)
-      return fail(VSD_ERR_NULL_POINTER, "out->kl_idx and out->kl_grad are required with kl_weight > 0");
-  }
+  if ((st = check_kl_out(dims, params, out)) != VSD_OK) return st;
   const WorkspaceLayout wl = workspace_layout(dims);
 
   char* ws = static_cast<char*>(workspace);
@@ -468,8 +472,7 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
   if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
-  if (kl_on(params))
-    return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed by vsd_score_paths (set kl_weight = 0 here)");
+  if ((st = check_kl_out(dims, params, out)) != VSD_OK) return st;
 
   const WorkspaceLayout wl = workspace_layout(dims);
   char* ws = static_cast<char*>(workspace);
@@ -517,9 +520,18 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   // multiple of 512 elements
   const int64_t nchunks = ((int64_t)dims->v_draft + 511) / 512;
   a.tblock = (int32_t)(512 * ((dims->v_target + 512 * nchunks - 1) / (512 * nchunks)));
+  float* kl_row = nullptr;
+  if (kl_on(params)) {
+    kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
+    a.kl_k = params->kl_topk;
+    a.kl_idx = out->kl_idx;
+    a.kl_grad = out->kl_grad;
+    a.kl_row = kl_row;
+    a.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
+  }
   hipError_t e = vsd::launch_sample(a, dims->dtype == VSD_BF16, s);
   if (e != hipSuccess) return hip_fail(e, "k_sample (fused) launch");
-  st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s);
+  st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s);
   if (st != VSD_OK) return st;
   return ok();
 }

@@ -281,7 +281,7 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
     _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
     dev = X.device
     if out is None:
-        out = alloc_score_outputs(prob, dev)
+        out = alloc_score_outputs(prob, dev, kl_topk=params.kl_topk if params.kl_weight > 0 else 0)
     if tokens is None:
         tokens = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
     for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), tokens):

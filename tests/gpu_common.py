@@ -51,7 +51,7 @@ def run_step(cfg, inp, params=None, tokens=None, fused=False):
         tokens = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
         grad = torch.full_like(inp["X"], SENTINEL)
         vsd.weighted_loss_bwd(prob, params, inp["X"], sc.lse_draft, tokens[0], tokens[1], sc.coef_a, sc.coef_b,
-                              grad=grad)
+                              grad=grad, kl_idx=sc.kl_idx, kl_grad=sc.kl_grad)
         torch.cuda.synchronize()
         return dict(tokens=tokens, score=sc, grad=grad, err_sample=sc.device_error)
     if tokens is None:

@@ -207,7 +207,7 @@ def test_fused_lm_head_validation(lib):
 
 
 def test_kl_term_validation(lib):
-    """kl_weight / kl_topk checks and the entry points that do not compute the term."""
+    """kl_weight / kl_topk checks of the scoring calls; the fused LM head does not compute the term."""
     for kw in (dict(kl_weight=-0.1), dict(kl_weight=float("nan")), dict(kl_weight=0.5, kl_topk=0),
                dict(kl_weight=0.5, kl_topk=17)):
         assert _score(lib, params=_params(**kw)) == 3
@@ -223,7 +223,16 @@ def test_kl_term_validation(lib):
     st = lib.vsd_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head), None,
                              None, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
     assert st == 6                                   # fused LM head: not with the KL term
-    src = _lib.VsdSrc(FAKE, None, None)
-    st = lib.vsd_sample_score_paths(ctypes.byref(_dims()), ctypes.byref(pr), ctypes.byref(src), ctypes.byref(src),
+    st = lib.vsd_sample_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head),
                                     None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
-    assert st == 6                                   # one-pass call: not with the KL term
+    assert st == 6                                   # one-pass call with the fused LM head: not with the KL term
+    src = _lib.VsdSrc(FAKE, None, None)
+    bare = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    st = lib.vsd_sample_score_paths(ctypes.byref(_dims()), ctypes.byref(pr), ctypes.byref(src), ctypes.byref(src),
+                                    None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(bare), FAKE, 1 << 30, None)
+    assert st == 1                                   # one-pass call: kl_idx / kl_grad required
+    small = _dims(v_draft=8, v_target=8, ld_draft=8, ld_target=8)
+    st = lib.vsd_sample_score_paths(ctypes.byref(small), ctypes.byref(_params(kl_weight=0.5, kl_topk=9)),
+                                    ctypes.byref(src), ctypes.byref(src), None, None, 0, 0, FAKE, FAKE, FAKE,
+                                    ctypes.byref(full), FAKE, 1 << 30, None)
+    assert st == 3                                   # one-pass call: kl_topk beyond the draft vocabulary

@@ -8,7 +8,10 @@ the term, the sparse gradient coefficients and the full gradient rows are
 compared under the materialised path's bars.  Cases: C1 in full (fp32,
 shared vocabulary), C3-recipe rows at the full vocabularies (mapped: mask and
 inverse map), C4-recipe rows (ragged, peaked bf16 with ties, T_q = 0.5),
-K = 1 and K = 16, a draft vocabulary of exactly K tokens.
+K = 1 and K = 16, a draft vocabulary of exactly K tokens.  Every case runs
+through both the three-call path (score_paths forms the term while it streams
+the target row) and the one-pass sample_score_paths (the target wavefront
+offers the mapped logits it gathered for sampling).
 """
 import numpy as np
 import pytest
@@ -27,9 +30,13 @@ def _lin_ok(got, ref):
     return np.abs(got - ref) <= 1e-3 * np.abs(ref) + 1e-6
 
 
-def check_kl(cfg, inp, positions, params, label):
+FUSED = pytest.mark.parametrize("fused", [False, True], ids=["three_call", "one_pass"])
+
+
+def check_kl(cfg, inp, positions, params, label, fused):
+    label = f"{label} {'one-pass' if fused else 'three-call'}"
     log(f"[{label}] KL term K={params.kl_topk} weight={params.kl_weight}")
-    gpu = run_step(cfg, inp, params)
+    gpu = run_step(cfg, inp, params, fused=fused)
     assert int(gpu["score"].device_error.item()) == 0 and int(gpu["err_sample"].item()) == 0
     rows, ora = oracle_positions(cfg, inp, positions, params)
     summary = compare(cfg, gpu, rows, ora, positions, label=label)
@@ -46,29 +53,33 @@ def check_kl(cfg, inp, positions, params, label):
     return summary
 
 
-def test_c1_full_with_kl():
+@FUSED
+def test_c1_full_with_kl(fused):
     cfg = CONFIGS["C1"]
     host = make_inputs_numpy_c1(cfg)
     inp = {"X": torch.as_tensor(host["X"]).to(DEV), "Y": torch.as_tensor(host["Y"]).to(DEV), "d2t": None,
            "valid_depth": None}
-    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.3, kl_topk=10), "C1 KL")
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.3, kl_topk=10), "C1 KL", fused)
 
 
-def test_mapped_full_vocabularies_with_kl():
+@FUSED
+def test_mapped_full_vocabularies_with_kl(fused):
     cfg = scaled("C3", B=1, T=3)
     inp = make_inputs(cfg, DEV)
-    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.5, kl_topk=10), "C3s KL")
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.5, kl_topk=10), "C3s KL", fused)
 
 
+@FUSED
 @pytest.mark.parametrize("K", [1, 16])
-def test_ragged_peaked_ties_with_kl(K):
+def test_ragged_peaked_ties_with_kl(K, fused):
     cfg = scaled("C4", B=1, T=3, v_draft=4000, v_target=4000)
     inp = make_inputs(cfg, DEV)
     check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=1.5, kl_topk=K, loss_scale=0.5),
-             f"C4s KL K={K}")
+             f"C4s KL K={K}", fused)
 
 
-def test_vocabulary_of_exactly_k_tokens():
+@FUSED
+def test_vocabulary_of_exactly_k_tokens(fused):
     cfg = scaled("C2", B=1, T=2, N=3, L=2, v_draft=16, v_target=16)
     inp = make_inputs(cfg, DEV)
-    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.8, kl_topk=16), "V=K KL")
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.8, kl_topk=16), "V=K KL", fused)
