@@ -16,7 +16,9 @@ One training position (prefix x) at a time, following the paper's order:
 Readings where the paper leaves a choice (each also listed in the design notes):
   * level l uses the length-l prefix of the depth-L path of slot s; the
     correction path is the length-l prefix of slot s's target path;
-  * all three families at slot (s,i) read the same logit rows;
+  * all three families at slot (s,i) read the same logit rows, unless each
+    family's own context rows are given (exact context: X, Y with a leading
+    family axis, the rows of the conditionals along z~, z' and z-bar);
   * the oracle's indicator in beta's numerator is the binary gate I~, o' keeps
     the weight w(l) (so w cancels and beta is a local acceptance rate);
   * beta = 0 when no other live path has o' > 0;
@@ -57,38 +59,49 @@ def length_weight(level, w_base):
 def score_position(X, Y, d2t, depth, tok_d, tok_t, tok_g, params=None):
     """Score the N paths of one position.
 
-    X      [N, L, V_d]  draft logits of each slot's row
-    Y      [N, L, V_t]  target logits of each slot's row
+    X      [N, L, V_d]  draft logits of each slot's row, or [3, N, L, V_d]:
+                        the rows along each family's own path (z~, z', z-bar)
+    Y      [N, L, V_t]  target logits of each slot's row, or [3, N, L, V_t]
     d2t    [V_d] int or None (identity)
     depth  [N]   valid depth d_s in [1, L]
     tok_*  [N, L] tokens of the three families (draft-index space; -1 masked)
-    Returns a dict of float64 / bool arrays indexed [s, i-1] (rows) or [s].
+    Returns a dict of float64 / bool arrays indexed [s, i-1] (rows) or [s];
+    lse_q / lse_p are those of the z~ rows, and with per-family rows
+    lse_q_ctx [N, L, 3] holds the draft normaliser of every family's row.
     """
     p = dict(DEFAULT_PARAMS)
     if params:
         p.update(params)
     X = np.asarray(X)
     Y = np.asarray(Y)
-    N, L, Vd = X.shape
+    ctx = X.ndim == 4
+    if not ctx:  # one row per slot, read by every family
+        X = X[None]
+        Y = Y[None]
+    N, L, Vd = X.shape[1:]
     d2t = np.arange(Vd) if d2t is None else np.asarray(d2t)
     depth = np.asarray(depth, dtype=np.int64)
     toks = [np.asarray(t, dtype=np.int64) for t in (tok_d, tok_t, tok_g)]
     Tq, Tp = float(p["temp_draft"]), float(p["temp_target"])
     live = np.arange(L)[None, :] < depth[:, None]          # [N, L]
 
-    # Row statistics and per-token log probabilities (Sec. "Preliminary").
-    lse_q = np.zeros((N, L))
-    lse_p = np.zeros((N, L))
+    # Row statistics and per-token log probabilities (Sec. "Preliminary"),
+    # family f on its own row (row set f, or the shared one).
+    nrow = X.shape[0]
+    lse_q = np.zeros((nrow, N, L))
+    lse_p = np.zeros((nrow, N, L))
     log_q = np.zeros((3, N, L))
     log_p = np.zeros((3, N, L))
     for s in range(N):
         for i in range(depth[s]):
-            lse_q[s, i] = log_softmax_normaliser(X[s, i], Tq)
-            lse_p[s, i] = log_softmax_normaliser(Y[s, i], Tp)
+            for k in range(nrow):
+                lse_q[k, s, i] = log_softmax_normaliser(X[k, s, i], Tq)
+                lse_p[k, s, i] = log_softmax_normaliser(Y[k, s, i], Tp)
             for f in range(3):
+                k = f if ctx else 0
                 z = toks[f][s, i]
-                log_q[f, s, i] = float(X[s, i, z]) / Tq - lse_q[s, i]
-                log_p[f, s, i] = float(Y[s, i, d2t[z]]) / Tp - lse_p[s, i]
+                log_q[f, s, i] = float(X[k, s, i, z]) / Tq - lse_q[k, s, i]
+                log_p[f, s, i] = float(Y[k, s, i, d2t[z]]) / Tp - lse_p[k, s, i]
     # Eq. acc: alpha = min(1, p/q)  <=>  log alpha = min(0, log p - log q).
     log_alpha = np.where(live[None], np.minimum(0.0, log_p - log_q), 0.0)
 
@@ -166,7 +179,10 @@ def score_position(X, Y, d2t, depth, tok_d, tok_t, tok_g, params=None):
         coef_a /= W
         coef_b /= W
 
-    return dict(lse_q=np.where(live, lse_q, 0.0), lse_p=np.where(live, lse_p, 0.0),
+    out = {}
+    if ctx:
+        out["lse_q_ctx"] = np.moveaxis(np.where(live[None], lse_q, 0.0), 0, -1)
+    return dict(out, lse_q=np.where(live, lse_q[0], 0.0), lse_p=np.where(live, lse_p[0], 0.0),
                 log_alpha=np.moveaxis(log_alpha, 0, -1),
                 log_q=np.moveaxis(np.where(live[None], log_q, 0.0), 0, -1),
                 survival=survival, exp_accept_len=exp_accept_len,
@@ -182,6 +198,8 @@ def grad_position(X, lse_q, tok_d, tok_t, coef_a, coef_b, temp_draft=1.0, loss_s
     Per row, d(-log q(z))/dX_v = (q(v) - [v = z]) / T_q, so with the row's
     coefficients a (for z~) and b (for z'):
       g_v = loss_scale / T_q * ((a + b) q(v) - a [v = z~] - b [v = z']).
+    With per-family rows z~ and z' sit on different rows: the gradient on the
+    z~ rows is this with b = 0, on the z' rows with a = 0 (grad_position_ctx).
     """
     X = np.asarray(X, dtype=np.float64)
     N, L, Vd = X.shape
@@ -199,6 +217,16 @@ def grad_position(X, lse_q, tok_d, tok_t, coef_a, coef_b, temp_draft=1.0, loss_s
     return g
 
 
+def grad_position_ctx(X_draft_path, X_corr_path, lse_draft_path, lse_corr_path, tok_d, tok_t, coef_a, coef_b,
+                      temp_draft=1.0, loss_scale=1.0):
+    """Gradients with per-family rows: (d/dX along z~, d/dX along z'), each
+    [N, L, V_d]; the rows along z-bar only gate and get none."""
+    zero = np.zeros_like(np.asarray(coef_a, dtype=np.float64))
+    g_d = grad_position(X_draft_path, lse_draft_path, tok_d, tok_t, coef_a, zero, temp_draft, loss_scale)
+    g_c = grad_position(X_corr_path, lse_corr_path, tok_d, tok_t, zero, coef_b, temp_draft, loss_scale)
+    return g_d, g_c
+
+
 def loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None):
     """L_x recomputed from logits with the E-step quantities (flags, o', c) frozen.
 
@@ -210,7 +238,8 @@ def loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None)
     if params:
         p.update(params)
     X = np.asarray(X, dtype=np.float64)
-    N, L, Vd = X.shape
+    Xd, Xc = (X[0], X[1]) if X.ndim == 4 else (X, X)   # rows along z~ and along z'
+    N, L, Vd = Xd.shape
     Tq = float(p["temp_draft"])
     W = frozen["o_prime"].sum()
     if W == 0:
@@ -220,9 +249,8 @@ def loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None)
         lq_d = 0.0
         lq_t = 0.0
         for i in range(depth[s]):
-            lse = log_softmax_normaliser(X[s, i], Tq)
-            lq_d += X[s, i, tok_d[s, i]] / Tq - lse
-            lq_t += X[s, i, tok_t[s, i]] / Tq - lse
+            lq_d += Xd[s, i, tok_d[s, i]] / Tq - log_softmax_normaliser(Xd[s, i], Tq)
+            lq_t += Xc[s, i, tok_t[s, i]] / Tq - log_softmax_normaliser(Xc[s, i], Tq)
             used = lq_d if frozen["accept_flag"][s, i] else lq_t
             total += frozen["o_prime"][s, i] * (used - frozen["c"][s, i] * lq_d)
     return -total / W
@@ -239,5 +267,7 @@ def loss_with_klv(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, params=None):
     base = loss_from_logits(X, Y, d2t, depth, tok_d, tok_t, tok_g, frozen, p)
     if p["kl_weight"] == 0.0:
         return base
+    if np.ndim(X) == 4:  # per-family rows: the term is taken on the rows along z~
+        X, Y = X[0], Y[0]
     KL = klv.position_terms(X, Y, d2t, depth, int(p["kl_topk"]), p["temp_draft"], p["temp_target"])[3]
     return base + p["kl_weight"] * KL

@@ -4,7 +4,8 @@ Runs the three stages of one VSD EM step for every listed position, in the
 paper's order: E-step draws (Alg. 1 and the greedy baseline of Alg. 2), path
 scoring and M-step weights, then the gradient with respect to the draft logits.
 Inputs are plain numpy arrays holding the exact logit values (float32 holds
-every bf16 value exactly).
+every bf16 value exactly).  With exact context, each family (z~, z', z-bar)
+has its own rows: the conditionals along its own path.
 """
 import numpy as np
 
@@ -28,6 +29,21 @@ def sample_position(Xp, Yp_mapped, depth, first_row, temp_draft, temp_target, se
     return toks
 
 
+def sample_step(draft_rows, target_rows, greedy_rows, d2t, live, rows_of_paths, temp_draft, temp_target,
+                seed, offset):
+    """Tokens of one depth of a set of paths from that depth's rows (exact
+    context): draft_rows [n, V_d] along z~, target_rows and greedy_rows
+    [n, V_t] along z' and z-bar; rows_of_paths [n] = global row index of
+    each path's slot at that depth (Philox counter word 1); live [n] bool.
+    Returns three int64 [n] arrays, -1 where not live."""
+    Vd = draft_rows.shape[1]
+    d2t_arr = np.arange(Vd) if d2t is None else np.asarray(d2t, dtype=np.int64)
+    toks = sampler.sample_rows_ctx(draft_rows, np.asarray(target_rows)[:, d2t_arr],
+                                   np.asarray(greedy_rows)[:, d2t_arr], rows_of_paths, temp_draft, temp_target,
+                                   seed, offset)
+    return [np.where(live, t, -1) for t in toks]
+
+
 def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
                   tokens=None, want_grad=True):
     """Oracle outputs for the given positions.
@@ -35,7 +51,11 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
     X [len(positions)*N*L, V_d], Y [len(positions)*N*L, V_t]: rows of those
     positions in row order; depth [len(positions), N] or None; tokens, if
     given, is a tuple of three [len(positions)*N*L] arrays used instead of
-    sampling (scoring then follows the given tokens).
+    sampling (scoring then follows the given tokens).  Exact context: X
+    [3, rows, V_d] and Y [3, rows, V_t] hold the rows along z~, z' and
+    z-bar; the tokens are drawn from them as sample_step does, and the result
+    gains grad_corr (the gradient on the rows along z') beside grad (on the
+    rows along z~) and lse_q_ctx [rows, 3].
     Returns a dict of per-row arrays [len(positions)*N*L] (or [.., V_d] for
     grad, [.., 3] for log_alpha / log_q) and per-position arrays.  With
     params kl_weight > 0 the top-K term (oracle.klv) joins the loss and the
@@ -45,22 +65,34 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
     """
     p = dict(paths.DEFAULT_PARAMS)
     p.update(params or {})
-    Vd = X.shape[1]
-    Vt = Y.shape[1]
+    ctx = np.ndim(X) == 3
+    Vd = X.shape[-1]
+    Vt = Y.shape[-1]
     d2t_arr = np.arange(Vd) if d2t is None else np.asarray(d2t, dtype=np.int64)
     npos = len(positions)
-    X = X.reshape(npos, N, L, Vd)
-    Y = Y.reshape(npos, N, L, Vt)
+    if ctx:  # [position, family, N, L, V]
+        X = np.moveaxis(X.reshape(3, npos, N, L, Vd), 0, 1)
+        Y = np.moveaxis(Y.reshape(3, npos, N, L, Vt), 0, 1)
+    else:
+        X = X.reshape(npos, N, L, Vd)
+        Y = Y.reshape(npos, N, L, Vt)
     depth = np.full((npos, N), L, dtype=np.int64) if depth is None else np.asarray(depth).reshape(npos, N)
     keys = ["lse_q", "lse_p", "log_alpha", "log_q", "survival", "accept_flag", "valid_flag",
-            "o_prime", "beta", "zeta", "coef_a", "coef_b", "LS"]
+            "o_prime", "beta", "zeta", "coef_a", "coef_b", "LS"] + (["lse_q_ctx"] if ctx else [])
     acc = {k: [] for k in keys}
     out = {"tok_draft": [], "tok_target": [], "tok_greedy": [], "exp_accept_len": [],
-           "loss_pos": [], "W": [], "grad": [], "kl_row": [], "kl_idx": [], "kl_grad": [], "kl_pos": []}
+           "loss_pos": [], "W": [], "grad": [], "grad_corr": [], "kl_row": [], "kl_idx": [], "kl_grad": [],
+           "kl_pos": []}
     lam = float(p["kl_weight"])
     K = int(p["kl_topk"])
     for k, pos in enumerate(positions):
-        if tokens is None:
+        if tokens is None and ctx:
+            live = (np.arange(L)[None, :] < depth[k][:, None]).reshape(-1)
+            rows = int(pos) * N * L + np.arange(N * L)
+            flat = lambda a: a.reshape(N * L, a.shape[-1])
+            toks = [t.reshape(N, L) for t in sample_step(flat(X[k][0]), flat(Y[k][1]), flat(Y[k][2]), d2t, live,
+                                                          rows, p["temp_draft"], p["temp_target"], seed, offset)]
+        elif tokens is None:
             toks = sample_position(X[k], Y[k][:, :, d2t_arr], depth[k], int(pos) * N * L,
                                    p["temp_draft"], p["temp_target"], seed, offset)
         else:
@@ -75,8 +107,10 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
         out["tok_greedy"].append(toks[2].reshape(-1))
         out["exp_accept_len"].append(sc["exp_accept_len"])
         loss = sc["loss"]
+        Xd = X[k][0] if ctx else X[k]   # rows along z~
         if lam > 0.0:
-            L_row, omega, dx, KL = klv.position_terms(X[k], Y[k], None if d2t is None else d2t_arr, depth[k], K,
+            L_row, omega, dx, KL = klv.position_terms(Xd, Y[k][0] if ctx else Y[k],
+                                                      None if d2t is None else d2t_arr, depth[k], K,
                                                       p["temp_draft"], p["temp_target"])
             loss = loss + lam * KL
             kl_grad = p["loss_scale"] * lam / N * dx
@@ -87,8 +121,14 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
         out["loss_pos"].append(loss)
         out["W"].append(sc["W"])
         if want_grad:
-            g = paths.grad_position(X[k], sc["lse_q"], toks[0], toks[1], sc["coef_a"], sc["coef_b"],
-                                    p["temp_draft"], p["loss_scale"])
+            if ctx:
+                g, gc = paths.grad_position_ctx(X[k][0], X[k][1], sc["lse_q_ctx"][..., 0], sc["lse_q_ctx"][..., 1],
+                                                toks[0], toks[1], sc["coef_a"], sc["coef_b"], p["temp_draft"],
+                                                p["loss_scale"])
+                out["grad_corr"].append(gc.reshape(N * L, Vd))
+            else:
+                g = paths.grad_position(X[k], sc["lse_q"], toks[0], toks[1], sc["coef_a"], sc["coef_b"],
+                                        p["temp_draft"], p["loss_scale"])
             if lam > 0.0:
                 for s in range(N):
                     for i in range(int(depth[k][s])):
@@ -107,4 +147,6 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
     res["loss_total"] = p["loss_scale"] * res["loss_pos"].sum()
     if want_grad:
         res["grad"] = np.concatenate(out["grad"])
+        if ctx:
+            res["grad_corr"] = np.concatenate(out["grad_corr"])
     return res

@@ -138,3 +138,14 @@ def sample_rows(draft_rows, target_rows_mapped, rows, temp_draft, temp_target, s
     k_target = gumbel_keys(target_rows_mapped, rows, 1, temp_target, seed, offset)
     return (first_argmax(k_draft), first_argmax(k_target),
             first_argmax(np.asarray(target_rows_mapped, dtype=np.float64)))
+
+
+def sample_rows_ctx(draft_rows, target_rows_mapped, greedy_rows_mapped, rows, temp_draft, temp_target, seed, offset):
+    """Draw (z~, z', z-bar) when each family has its own rows (exact context):
+    z~ from the draft rows along z~, z' from the target rows along z', z-bar
+    the first argmax of the target rows along z-bar.  The Philox counters are
+    those of sample_rows, so equal rows give equal tokens."""
+    k_draft = gumbel_keys(draft_rows, rows, 0, temp_draft, seed, offset)
+    k_target = gumbel_keys(target_rows_mapped, rows, 1, temp_target, seed, offset)
+    return (first_argmax(k_draft), first_argmax(k_target),
+            first_argmax(np.asarray(greedy_rows_mapped, dtype=np.float64)))

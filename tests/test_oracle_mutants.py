@@ -128,6 +128,59 @@ def _check_map(P):
             and np.allclose(b["log_alpha"][unclamped], a["log_alpha"][unclamped] - math.log(2), rtol=1e-12))
 
 
+def _toy(seed, V, scale):
+    def logits(prefix):
+        h = hash((seed,) + tuple(prefix)) & 0xFFFFFFFF
+        return np.random.default_rng(h).normal(0, scale, V)
+    return logits
+
+
+def _rows_along(model, path):
+    return np.stack([model(tuple(path[:i])) for i in range(len(path))])
+
+
+def _log_survival_along(q, p, path, T=1.0):
+    """log S_k of one path rebuilt from the toy model alone (no oracle code)."""
+    out, acc = [], 0.0
+    for i, z in enumerate(path):
+        lq = np.log(_softmax(q(tuple(path[:i])) / T)[z])
+        lp = np.log(_softmax(p(tuple(path[:i])))[z])
+        acc += min(0.0, lp - lq)
+        out.append(acc)
+    return np.asarray(out)
+
+
+def _check_ctx(P):
+    """Exact context: each family on its own path's rows; finite differences
+    on the rows along z~ and along z'."""
+    V, L, N = 4, 3, 3
+    q, p = _toy(1, V, 1.5), _toy(2, V, 1.5)
+    rng = np.random.default_rng(3)   # paths of z~ and z' differ at depth 1; a and b both nonzero
+    fam = [rng.integers(0, V, (N, L)) for _ in range(3)]
+    X = np.stack([np.stack([_rows_along(q, fam[f][s]) for s in range(N)]) for f in range(3)])
+    Y = np.stack([np.stack([_rows_along(p, fam[f][s]) for s in range(N)]) for f in range(3)])
+    out = P.score_position(X, Y, None, [L] * N, *fam)
+    for f in range(3):
+        for s in range(N):
+            if not np.allclose(out["LS"][s, :, f], _log_survival_along(q, p, fam[f][s]), atol=1e-12):
+                return False
+    params = dict(mode=2, temp_draft=0.8)
+    out = P.score_position(X, Y, None, [L] * N, *fam, params)
+    gd, gc = P.grad_position_ctx(X[0], X[1], out["lse_q_ctx"][..., 0], out["lse_q_ctx"][..., 1], fam[0], fam[1],
+                                 out["coef_a"], out["coef_b"], 0.8, 1.0)
+    h = 1e-6
+    for idx in np.ndindex(X.shape):
+        Xp, Xm = X.copy(), X.copy()
+        Xp[idx] += h
+        Xm[idx] -= h
+        fd = (P.loss_from_logits(Xp, Y, None, [L] * N, *fam, out, params)
+              - P.loss_from_logits(Xm, Y, None, [L] * N, *fam, out, params)) / (2 * h)
+        g = gd[idx[1:]] if idx[0] == 0 else gc[idx[1:]] if idx[0] == 1 else 0.0
+        if abs(fd - g) > 1e-6:
+            return False
+    return True
+
+
 def _check_sampler(S):
     w = (np.arange(2 ** 23, dtype=np.uint64) << np.uint64(9)).astype(np.uint32)
     ug = S.uniform_from_word(w)
@@ -150,6 +203,12 @@ def _check_sampler(S):
             return False
     x = np.zeros((1, 3), dtype=np.float32)
     if S.sample_rows(x, np.array([[0.0, 1.0, 1.0]], dtype=np.float32), [0], 1.0, 1.0, 0, 0)[2][0] != 1:
+        return False
+    # exact context: z-bar from the rows along z-bar, z' from those along z'
+    tr = np.array([[0.0, 0.0, 30.0]], dtype=np.float32)
+    gr = np.array([[0.0, 2.0, 1.0]], dtype=np.float32)
+    zc = S.sample_rows_ctx(x, tr, gr, [0], 1.0, 1.0, 0, 0)
+    if zc[2][0] != 1 or zc[1][0] != 2:
         return False
     return True
 
@@ -175,9 +234,15 @@ PATH_MUTANTS = [
     ("coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] - c[s, lev])", "coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] + c[s, lev])"),
     ("g[s, i] = loss_scale / temp_draft * row", "g[s, i] = loss_scale * row"),
     ("row[tok_t[s, i]] -= b", "row[tok_d[s, i]] -= b"),
-    ("log_p[f, s, i] = float(Y[s, i, d2t[z]]) / Tp - lse_p[s, i]", "log_p[f, s, i] = float(Y[s, i, z]) / Tp - lse_p[s, i]"),
-    ("lse_p[s, i] = log_softmax_normaliser(Y[s, i], Tp)", "lse_p[s, i] = log_softmax_normaliser(Y[s, i, d2t], Tp)"),
-    ("log_q[f, s, i] = float(X[s, i, z]) / Tq - lse_q[s, i]", "log_q[f, s, i] = float(X[s, i, z]) - lse_q[s, i]"),
+    ("log_p[f, s, i] = float(Y[k, s, i, d2t[z]]) / Tp - lse_p[k, s, i]",
+     "log_p[f, s, i] = float(Y[k, s, i, z]) / Tp - lse_p[k, s, i]"),
+    ("lse_p[k, s, i] = log_softmax_normaliser(Y[k, s, i], Tp)", "lse_p[k, s, i] = log_softmax_normaliser(Y[k, s, i, d2t], Tp)"),
+    ("log_q[f, s, i] = float(X[k, s, i, z]) / Tq - lse_q[k, s, i]", "log_q[f, s, i] = float(X[k, s, i, z]) - lse_q[k, s, i]"),
+    # exact context: a family scored on another family's rows, gradients on the wrong rows
+    ("k = f if ctx else 0", "k = 0"),
+    ("k = f if ctx else 0", "k = (f + 1) % 3 if ctx else 0"),
+    ("g_d = grad_position(X_draft_path, lse_draft_path,", "g_d = grad_position(X_corr_path, lse_corr_path,"),
+    ("g_c = grad_position(X_corr_path, lse_corr_path,", "g_c = grad_position(X_corr_path, lse_draft_path,"),
     ("c = beta * zeta", "c = beta + zeta - 1.0"),
 ]
 
@@ -190,6 +255,10 @@ SAMPLER_MUTANTS = [
     ("return (2 * k + 1).astype(F32) * F32(2.0 ** -24)", "return (k + 1).astype(F32) * F32(2.0 ** -23)"),
     ("first_argmax(np.asarray(target_rows_mapped, dtype=np.float64))",
      "first_argmax(-np.asarray(target_rows_mapped, dtype=np.float64))"),
+    ("first_argmax(np.asarray(greedy_rows_mapped, dtype=np.float64))",
+     "first_argmax(np.asarray(target_rows_mapped, dtype=np.float64))"),
+    ("k_target = gumbel_keys(target_rows_mapped, rows, 1, temp_target, seed, offset)\n    return (first_argmax(k_draft), first_argmax(k_target),\n            first_argmax(np.asarray(greedy",
+     "k_target = gumbel_keys(greedy_rows_mapped, rows, 1, temp_target, seed, offset)\n    return (first_argmax(k_draft), first_argmax(k_target),\n            first_argmax(np.asarray(greedy"),
 ]
 
 
@@ -198,6 +267,7 @@ def test_unmutated_oracle_passes_every_check(golden_dir):
     assert _check_closed_form(paths_mod)
     assert _check_fd(paths_mod)
     assert _check_map(paths_mod)
+    assert _check_ctx(paths_mod)
     assert _check_sampler(sampler_mod)
 
 
@@ -205,7 +275,7 @@ def test_unmutated_oracle_passes_every_check(golden_dir):
 def test_path_mutant_is_caught(golden_dir, old, new):
     P = _mutant(paths_mod, old, new)
     caught = (not _check_golden(P, golden_dir)) or (not _check_closed_form(P)) \
-        or (not _check_fd(P)) or (not _check_map(P))
+        or (not _check_fd(P)) or (not _check_map(P)) or (not _check_ctx(P))
     assert caught, f"no pin caught mutant {new!r}"
 
 
