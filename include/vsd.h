@@ -165,6 +165,25 @@
  *   materialised logits by vsd_score_paths and vsd_sample_score_paths (same
  *   outputs, same results); with the fused LM head (hidden_dim > 0) both
  *   return VSD_ERR_UNSUPPORTED when kl_weight > 0.
+ *
+ * Exact context (vsd_sample_step, vsd_score_paths_ctx, vsd_weighted_loss_bwd_ctx)
+ * ------------------------------------------------------------------------------
+ *   By default the three families of a slot read the same rows: the
+ *   conditionals along the draft path.  The paper's acceptance test
+ *   (Sec. "Preliminary", Eq. acc) and survival (Eq. survival_def) are taken
+ *   along each path with its own prefix, p(.|x, z_<i) and q(.|x, z_<i); a
+ *   caller that runs the models along every path can pass those rows instead:
+ *   family f (0: z~, 1: z', 2: z-bar) then has draft rows X_f and target rows
+ *   Y_f ([R, ld] each, the layout of the shared rows), and
+ *     log alpha^f, log q^f  come from X_f, Y_f at z^f,
+ *     every later quantity  as before (flags, o', beta, zeta, a, b, loss),
+ *     the gradient          a-part on X_0 (the rows along z~), b-part on X_1
+ *                           (along z'); X_2 only gates.
+ *   The KL term, when on, is taken on X_0, Y_0.  vsd_sample_step draws one
+ *   depth of such a rollout: the models' rows at depth i depend on the
+ *   tokens at depths < i, so the draws go depth by depth, each with the
+ *   Philox counters of the slot's global row (equal rows at every depth give
+ *   exactly the tokens of vsd_sample_paths).
  */
 #ifndef VSD_H
 #define VSD_H
@@ -176,7 +195,7 @@
 extern "C" {
 #endif
 
-#define VSD_ABI_VERSION 2
+#define VSD_ABI_VERSION 3
 
 typedef enum vsd_status {
   VSD_OK = 0,
@@ -270,6 +289,12 @@ typedef struct vsd_score_out {
   float* kl_pos;          /* [P]   optional: KL_x */
 } vsd_score_out;
 
+/* Exact context: the rows of each family's own conditionals (see above). */
+typedef struct vsd_ctx_rows {
+  const void* draft[3];   /* [R, ld_draft] each: draft logits along z~, z', z-bar */
+  const void* target[3];  /* [R, ld_target] each: target logits along z~, z', z-bar */
+} vsd_ctx_rows;
+
 typedef struct vsd_grad {
   void* grad_logits;      /* [R, ld_draft]: dtype of X; fused: bf16 */
   void* grad_hidden;      /* fused: [R, H] bf16, required */
@@ -342,6 +367,55 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
                                  const float* coef_b, const int32_t* kl_idx,
                                  const float* kl_grad, const vsd_grad* grad,
                                  int32_t* device_error, void* hip_stream);
+
+/* One depth of a rollout with exact context (Alg. 1 draws and Alg. 2's
+ * greedy reference, depth by depth).  step in [0, L).  draft_rows: the draft
+ * logits at this depth along z~ of every path, path p at draft_rows + p *
+ * ld_draft (P*N rows, P = B*T, paths in (b, t, s) order); target_rows and
+ * greedy_rows: the target logits along z' and along z-bar, stride ld_target.
+ * Writes row p*L + step of tok_draft, tok_target, tok_greedy ([R] each), -1
+ * where step >= valid_depth[p]; other rows are not touched.  The draws are
+ * those of vsd_sample_paths for that row (same counters), so a rollout whose
+ * rows are equal for the three families reproduces vsd_sample_paths exactly.
+ * Materialised logits only (dims->hidden_dim must be 0). */
+vsd_status vsd_sample_step(const vsd_dims* dims, int32_t step,
+                           const void* draft_rows, const void* target_rows,
+                           const void* greedy_rows, const int32_t* d2t,
+                           const int32_t* valid_depth, float temp_draft,
+                           float temp_target, uint64_t seed, uint32_t offset,
+                           int32_t* tok_draft, int32_t* tok_target,
+                           int32_t* tok_greedy, int32_t* device_error,
+                           void* hip_stream);
+
+/* vsd_score_paths with exact context: family f's log alpha and log q from
+ * rows->draft[f] and rows->target[f].  out->lse_draft (and lse_target) are
+ * those of the rows along z~; lse_draft_corr [R] (required) receives the
+ * draft log-sum-exp of the rows along z' (the backward needs it).  KL term
+ * (kl_weight > 0) on the rows along z~.  Same workspace as vsd_score_paths.
+ * Materialised logits only. */
+vsd_status vsd_score_paths_ctx(const vsd_dims* dims, const vsd_params* params,
+                               const vsd_ctx_rows* rows, const int32_t* d2t,
+                               const int32_t* valid_depth,
+                               const int32_t* tok_draft, const int32_t* tok_target,
+                               const int32_t* tok_greedy, const vsd_score_out* out,
+                               float* lse_draft_corr, void* workspace,
+                               size_t workspace_bytes, void* hip_stream);
+
+/* vsd_weighted_loss_bwd with exact context: grad_draft_path [R, ld_draft]
+ * receives loss_scale / T_q (a q(v) - a [v = z~]) (+ the KL term's gradient)
+ * on the rows along z~ (rows->draft[0], lse_draft), and grad_corr_path
+ * receives loss_scale / T_q (b q(v) - b [v = z']) on the rows along z'
+ * (rows->draft[1], lse_draft_corr).  The two buffers must be distinct (the
+ * caller adds them where the rows are the same).  Layout and dtype as
+ * vsd_weighted_loss_bwd's grad_logits. */
+vsd_status vsd_weighted_loss_bwd_ctx(const vsd_dims* dims, const vsd_params* params,
+                                     const vsd_ctx_rows* rows, const float* lse_draft,
+                                     const float* lse_draft_corr,
+                                     const int32_t* tok_draft, const int32_t* tok_target,
+                                     const float* coef_a, const float* coef_b,
+                                     const int32_t* kl_idx, const float* kl_grad,
+                                     void* grad_draft_path, void* grad_corr_path,
+                                     int32_t* device_error, void* hip_stream);
 
 /* Bytes of workspace vsd_score_paths needs for `dims` (host only). */
 vsd_status vsd_score_workspace_bytes(const vsd_dims* dims, size_t* bytes);

@@ -45,6 +45,10 @@ class VsdScoreOut(ctypes.Structure):
         "loss_pos", "loss_total", "device_error", "kl_idx", "kl_grad", "kl_row", "kl_pos")]
 
 
+class VsdCtxRows(ctypes.Structure):
+    _fields_ = [("draft", c_vp * 3), ("target", c_vp * 3)]
+
+
 class VsdGrad(ctypes.Structure):
     _fields_ = [("grad_logits", c_vp), ("grad_hidden", c_vp), ("grad_weight", c_vp)]
 
@@ -52,6 +56,7 @@ class VsdGrad(ctypes.Structure):
 _lib = None
 
 EXPORTS = ("vsd_sample_paths", "vsd_score_paths", "vsd_sample_score_paths", "vsd_weighted_loss_bwd",
+           "vsd_sample_step", "vsd_score_paths_ctx", "vsd_weighted_loss_bwd_ctx",
            "vsd_score_workspace_bytes", "vsd_status_string", "vsd_last_error", "vsd_abi_version")
 
 
@@ -78,6 +83,15 @@ def load():
     lib.vsd_weighted_loss_bwd.argtypes = [P(VsdDims), P(VsdParams), P(VsdSrc), c_vp, c_vp, c_vp, c_vp,
                                           c_vp, c_vp, c_vp, P(VsdGrad), c_vp, c_vp]
     lib.vsd_weighted_loss_bwd.restype = c_i32
+    lib.vsd_sample_step.argtypes = [P(VsdDims), c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_f32, c_f32,
+                                    ctypes.c_uint64, ctypes.c_uint32, c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.vsd_sample_step.restype = c_i32
+    lib.vsd_score_paths_ctx.argtypes = [P(VsdDims), P(VsdParams), P(VsdCtxRows), c_vp, c_vp, c_vp, c_vp, c_vp,
+                                        P(VsdScoreOut), c_vp, c_vp, ctypes.c_size_t, c_vp]
+    lib.vsd_score_paths_ctx.restype = c_i32
+    lib.vsd_weighted_loss_bwd_ctx.argtypes = [P(VsdDims), P(VsdParams), P(VsdCtxRows), c_vp, c_vp, c_vp, c_vp,
+                                              c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.vsd_weighted_loss_bwd_ctx.restype = c_i32
     lib.vsd_score_workspace_bytes.argtypes = [P(VsdDims), P(ctypes.c_size_t)]
     lib.vsd_score_workspace_bytes.restype = c_i32
     lib.vsd_status_string.argtypes = [c_i32]

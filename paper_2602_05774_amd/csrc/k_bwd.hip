@@ -60,8 +60,8 @@ __global__ __launch_bounds__(256) void k_bwd(BwdArgs a) {
   const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (r >= a.R) return;
   T* G = static_cast<T*>(a.G) + r * a.ld;
-  const float ca = a.coef_a[r];
-  const float cb = a.coef_b[r];
+  const float ca = a.coef_a != nullptr ? a.coef_a[r] : 0.0f;
+  const float cb = a.coef_b != nullptr ? a.coef_b[r] : 0.0f;
   KlRow<KL> kl;
   kl.load(a, r);
   constexpr int step = 8 * kWave;

@@ -32,6 +32,12 @@
 // entries and rows are loaded while the current chunk is drawn, and the target
 // gathers of the next chunk are issued at the end of the current one.
 //
+// k_sample_step draws one depth of a rollout with exact context: three
+// wavefronts per path, each on its own row (z~ from the draft row along z~,
+// z' from the target row along z', z-bar from the target row along z-bar),
+// with the counters of the slot's global row, so equal rows give exactly the
+// tokens k_sample draws.
+//
 // With the top-K renormalised KL term (one-pass mode), the target wavefront
 // also offers each chunk's mapped target logits, already in draft-index
 // order, to an exact wavefront top-K (vsd_topk.hpp) and, after the row, forms
@@ -235,7 +241,7 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
 
 // The target wavefront of a row: z' and z-bar and, fused, the target
 // log-sum-exp (unmapped) or the other half of the target stream (mapped).
-template <typename T, bool MAPPED, bool FUSED, bool KL>
+template <typename T, bool MAPPED, bool FUSED, bool KL, bool DRAW = true>
 __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int Vt, FamilyDraw& f, Best& bg,
                             LaneLse& lp, bool& map_bad, WaveTopK& tk, int lane) {
   auto same = [](int col) { return col; };
@@ -301,7 +307,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
         if (FUSED) lp.add8(y, f.c2);
       }
       greedy(base, y, 8);
-      f.draw(base, y, 8);
+      if (DRAW) f.draw(base, y, 8);
       if (KL) tk.offer8(y, base, 0xFFu, same, lane);
       if (next) {
         if (MAPPED)
@@ -339,7 +345,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
     }
     if (FUSED && !MAPPED) lp.add8(y, f.c2);
     greedy(base, y, nvalid);
-    f.draw(base, y, nvalid);
+    if (DRAW) f.draw(base, y, nvalid);
     if (KL) tk.offer8(y, base, nvalid > 0 ? (1u << nvalid) - 1u : 0u, same, lane);
   }
   if (FUSED && MAPPED) {  // target elements past the last chunk's block: odd half-blocks
@@ -483,6 +489,63 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   }
 }
 
+template <typename T, bool MAPPED>
+__global__ __launch_bounds__(192) void k_sample_step(SampleStepArgs a) {
+  __shared__ __align__(16) T ytile[2][kChunk];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x >> 6;  // 0: z~, 1: z', 2: z-bar
+  const int64_t path = blockIdx.x;     // the grid has exactly one workgroup per path
+  int d = a.L;
+  if (a.depth != nullptr) {
+    d = a.depth[path];
+    if (d < 1 || d > a.L) {
+      if (lane == 0 && wave == 0) report_error(a.err, VSD_DEVERR_DEPTH_RANGE);
+      d = 0;
+    }
+  }
+  const int64_t r = path * a.L + a.step;
+  int32_t* out = wave == 0 ? a.tok_d : wave == 1 ? a.tok_t : a.tok_g;
+  if (a.step >= d) {  // masked slot
+    if (lane == 0) out[r] = -1;
+    return;
+  }
+  LaneLse unused_q, unused_p;
+  if (wave == 0) {
+    const T* X = static_cast<const T*>(a.X) + path * a.ld_d;
+    FamilyDraw f{(uint32_t)r, 0u, a.offset, a.k0, a.k1, a.inv_tq, a.inv_tq * kLog2e};
+    draft_wave<T, MAPPED, false>(X, nullptr, a.Vd, a.Vt, f, unused_q, unused_p, 0.0f, lane);
+    wave_argmax(f.best.key, f.best.idx);
+    if (lane == 0) out[r] = f.best.idx;
+    return;
+  }
+  const T* Y = static_cast<const T*>(wave == 1 ? a.Y : a.Yg) + path * a.ld_t;
+  FamilyDraw f{(uint32_t)r, 1u, a.offset, a.k0, a.k1, a.inv_tp, a.inv_tp * kLog2e};
+  Best bg{-INFINITY, 0x7FFFFFFF};
+  bool map_bad = false;
+  WaveTopK unused_tk;
+  if (wave == 1) {
+    target_wave<T, MAPPED, false, false, true>(Y, a.d2t, ytile[0], a.Vd, a.Vt, f, bg, unused_p, map_bad, unused_tk,
+                                               lane);
+    wave_argmax(f.best.key, f.best.idx);
+  } else {
+    target_wave<T, MAPPED, false, false, false>(Y, a.d2t, ytile[1], a.Vd, a.Vt, f, bg, unused_p, map_bad,
+                                                unused_tk, lane);
+    wave_argmax(bg.key, bg.idx);
+  }
+  if (map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
+  if (lane == 0) out[r] = wave == 1 ? f.best.idx : bg.idx;
+}
+
+template <typename T>
+hipError_t launch_step_t(const SampleStepArgs& a, hipStream_t s) {
+  const dim3 grid((unsigned)a.paths);
+  if (a.d2t != nullptr)
+    hipLaunchKernelGGL((k_sample_step<T, true>), grid, dim3(3 * kWave), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_sample_step<T, false>), grid, dim3(3 * kWave), 0, s, a);
+  return hipGetLastError();
+}
+
 template <typename T, bool FUSED, bool KL>
 hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
@@ -504,6 +567,10 @@ hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s) {
   }
   if (kl) return launch_t<float, true, true>(a, s);
   return fused ? launch_t<float, true, false>(a, s) : launch_t<float, false, false>(a, s);
+}
+
+hipError_t launch_sample_step(const SampleStepArgs& a, bool bf16, hipStream_t s) {
+  return bf16 ? launch_step_t<bf16_t>(a, s) : launch_step_t<float>(a, s);
 }
 
 }  // namespace vsd

@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
       a.lq[r * 3 + lane] = 0.0f;
     }
     if (lane == 0) {
-      a.lse_q[r] = 0.0f;
+      if (a.lse_q != nullptr) a.lse_q[r] = 0.0f;
       if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
     }
     if (KL) {
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   }
   const float lse_q = q.mraw * a.inv_tq + q.tail;
   const float lse_p = p.mraw * a.inv_tp + p.tail;
-  if (lane < 3) {  // lane f gathers family f
+  if (lane >= a.fam_lo && lane < a.fam_hi) {  // lane f gathers family f
     const int32_t z = a.tok[lane][r];
     float lq = 0.0f, la = 0.0f;
     if ((uint32_t)z >= (uint32_t)a.Vd) {
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
     a.lq[r * 3 + lane] = lq;
   }
   if (lane == 0) {
-    a.lse_q[r] = lse_q;
+    if (a.lse_q != nullptr) a.lse_q[r] = lse_q;
     if (a.lse_p != nullptr) a.lse_p[r] = lse_p;
   }
   if (KL) {

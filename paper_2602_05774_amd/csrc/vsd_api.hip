@@ -102,6 +102,27 @@ vsd_status check_logits(const vsd_dims* d, const vsd_src* src, const char* name,
   return VSD_OK;
 }
 
+// check_logits for a bare row pointer (the exact-context calls).
+vsd_status check_rows(const vsd_dims* d, const void* rows, const char* name, int64_t ld, int32_t v) {
+  const vsd_src src{rows, nullptr, nullptr};
+  return check_logits(d, &src, name, ld, v);
+}
+
+// Every row set of an exact-context call: materialised logits, draft rows
+// of the first `ndraft` families and target rows of the first `ntarget`.
+vsd_status check_ctx_rows(const vsd_dims* d, const vsd_ctx_rows* rows, int ndraft, int ntarget) {
+  if (is_fused(d)) return fail(VSD_ERR_UNSUPPORTED, "exact context: materialised logits only (hidden_dim must be 0)");
+  if (rows == nullptr) return fail(VSD_ERR_NULL_POINTER, "rows is NULL");
+  static const char* const dn[3] = {"draft rows along z~", "draft rows along z'", "draft rows along z-bar"};
+  static const char* const tn[3] = {"target rows along z~", "target rows along z'", "target rows along z-bar"};
+  vsd_status st;
+  for (int f = 0; f < ndraft; ++f)
+    if ((st = check_rows(d, rows->draft[f], dn[f], d->ld_draft, d->v_draft)) != VSD_OK) return st;
+  for (int f = 0; f < ntarget; ++f)
+    if ((st = check_rows(d, rows->target[f], tn[f], d->ld_target, d->v_target)) != VSD_OK) return st;
+  return VSD_OK;
+}
+
 vsd_status check_map(const vsd_dims* d, const int32_t* d2t) {
   if (d->v_draft != d->v_target && d2t == nullptr)
     return fail(VSD_ERR_MAP_REQUIRED, "v_draft=%d != v_target=%d requires d2t", d->v_draft, d->v_target);
@@ -193,6 +214,65 @@ vsd_status check_kl_out(const vsd_dims* dims, const vsd_params* params, const vs
     return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d > v_draft=%d", params->kl_topk, dims->v_draft);
   if (out->kl_idx == nullptr || out->kl_grad == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "out->kl_idx and out->kl_grad are required with kl_weight > 0");
+  return VSD_OK;
+}
+
+// Row statistics of the materialised scoring calls.  Shared rows: one
+// launch gathers the three families on X[0], Y[0].  Exact context: family f
+// on X[f], Y[f] (one launch each); the draft log-sum-exp of the rows along z'
+// goes to lse_corr.  The KL term, when on, rides on the launch that covers
+// z~'s rows; *kl_row_out receives its [R] row terms (null when off).
+vsd_status score_rows(const vsd_dims* dims, const vsd_params* params, const void* const X[3],
+                      const void* const Y[3], bool ctx, const int32_t* d2t, const int32_t* valid_depth,
+                      const int32_t* const tok[3], const vsd_score_out* out, float* lse_corr, char* ws,
+                      const WorkspaceLayout& wl, float* la, float* lq, float** kl_row_out, hipStream_t s) {
+  float* kl_row = nullptr;
+  hipError_t e;
+  if (kl_on(params)) {
+    kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
+    if (d2t != nullptr) {
+      int32_t* inv = reinterpret_cast<int32_t*>(ws + wl.inv);
+      e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
+      if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
+      e = vsd::launch_map_mask(inv, dims->v_target, reinterpret_cast<uint32_t*>(ws + wl.mask), s);
+      if (e != hipSuccess) return hip_fail(e, "k_map_mask launch");
+    }
+  }
+  *kl_row_out = kl_row;
+  for (int f = 0; f < (ctx ? 3 : 1); ++f) {
+    vsd::ScoreRowArgs ra{};
+    ra.X = X[f];
+    ra.Y = Y[f];
+    ra.d2t = d2t;
+    ra.depth = valid_depth;
+    for (int k = 0; k < 3; ++k) ra.tok[k] = tok[k];
+    ra.fam_lo = ctx ? f : 0;
+    ra.fam_hi = ctx ? f + 1 : 3;
+    ra.lse_q = f == 0 ? out->lse_draft : f == 1 ? lse_corr : nullptr;
+    ra.lse_p = f == 0 ? out->lse_target : nullptr;
+    ra.la = la;
+    ra.lq = lq;
+    ra.err = out->device_error;
+    ra.R = rows_of(dims);
+    ra.ld_d = dims->ld_draft;
+    ra.ld_t = dims->ld_target;
+    ra.L = dims->L;
+    ra.Vd = dims->v_draft;
+    ra.Vt = dims->v_target;
+    ra.inv_tq = 1.0f / params->temp_draft;
+    ra.inv_tp = 1.0f / params->temp_target;
+    if (kl_on(params) && f == 0) {
+      ra.kl_k = params->kl_topk;
+      ra.map_mask = reinterpret_cast<const uint32_t*>(ws + wl.mask);
+      ra.inv = reinterpret_cast<const int32_t*>(ws + wl.inv);
+      ra.kl_idx = out->kl_idx;
+      ra.kl_grad = out->kl_grad;
+      ra.kl_row = kl_row;
+      ra.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
+    }
+    e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
+    if (e != hipSuccess) return hip_fail(e, "k_score_rows launch");
+  }
   return VSD_OK;
 }
 
@@ -408,51 +488,13 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
     return ok();
   }
 
+  const void* const X[3] = {draft->logits, draft->logits, draft->logits};
+  const void* const Y[3] = {target->logits, target->logits, target->logits};
+  const int32_t* const tok[3] = {tok_draft, tok_target, tok_greedy};
   float* kl_row = nullptr;
-  hipError_t e;
-  if (kl_on(params)) {
-    kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
-    if (d2t != nullptr) {
-      int32_t* inv = reinterpret_cast<int32_t*>(ws + wl.inv);
-      e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
-      if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
-      e = vsd::launch_map_mask(inv, dims->v_target, reinterpret_cast<uint32_t*>(ws + wl.mask), s);
-      if (e != hipSuccess) return hip_fail(e, "k_map_mask launch");
-    }
-  }
-
-  vsd::ScoreRowArgs ra{};
-  ra.X = draft->logits;
-  ra.Y = target->logits;
-  ra.d2t = d2t;
-  ra.depth = valid_depth;
-  ra.tok[0] = tok_draft;
-  ra.tok[1] = tok_target;
-  ra.tok[2] = tok_greedy;
-  ra.lse_q = out->lse_draft;
-  ra.lse_p = out->lse_target;
-  ra.la = la;
-  ra.lq = lq;
-  ra.err = out->device_error;
-  ra.R = rows_of(dims);
-  ra.ld_d = dims->ld_draft;
-  ra.ld_t = dims->ld_target;
-  ra.L = dims->L;
-  ra.Vd = dims->v_draft;
-  ra.Vt = dims->v_target;
-  ra.inv_tq = 1.0f / params->temp_draft;
-  ra.inv_tp = 1.0f / params->temp_target;
-  if (kl_on(params)) {
-    ra.kl_k = params->kl_topk;
-    ra.map_mask = reinterpret_cast<const uint32_t*>(ws + wl.mask);
-    ra.inv = reinterpret_cast<const int32_t*>(ws + wl.inv);
-    ra.kl_idx = out->kl_idx;
-    ra.kl_grad = out->kl_grad;
-    ra.kl_row = kl_row;
-    ra.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
-  }
-  e = vsd::launch_score_rows(ra, dims->dtype == VSD_BF16, s);
-  if (e != hipSuccess) return hip_fail(e, "k_score_rows launch");
+  if ((st = score_rows(dims, params, X, Y, false, d2t, valid_depth, tok, out, nullptr, ws, wl, la, lq, &kl_row, s)) !=
+      VSD_OK)
+    return st;
 
   vsd_status st2 = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s);
   if (st2 != VSD_OK) return st2;
@@ -612,6 +654,128 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
   }
   hipError_t e = vsd::launch_bwd(a, dims->dtype == VSD_BF16, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "k_bwd launch");
+  return ok();
+}
+
+vsd_status vsd_sample_step(const vsd_dims* dims, int32_t step, const void* draft_rows, const void* target_rows,
+                           const void* greedy_rows, const int32_t* d2t, const int32_t* valid_depth, float temp_draft,
+                           float temp_target, uint64_t seed, uint32_t offset, int32_t* tok_draft,
+                           int32_t* tok_target, int32_t* tok_greedy, int32_t* device_error, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  const vsd_ctx_rows rows{{draft_rows, nullptr, nullptr}, {target_rows, greedy_rows, nullptr}};
+  if ((st = check_ctx_rows(dims, &rows, 1, 2)) != VSD_OK) return st;
+  if (step < 0 || step >= dims->L) return fail(VSD_ERR_INVALID_VALUE, "step=%d outside [0, L=%d)", step, dims->L);
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (!finite_pos(temp_draft) || !finite_pos(temp_target))
+    return fail(VSD_ERR_INVALID_VALUE, "temperatures must be finite and > 0");
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
+  if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+
+  vsd::SampleStepArgs a{};
+  a.X = draft_rows;
+  a.Y = target_rows;
+  a.Yg = greedy_rows;
+  a.d2t = d2t;
+  a.depth = valid_depth;
+  a.tok_d = tok_draft;
+  a.tok_t = tok_target;
+  a.tok_g = tok_greedy;
+  a.err = device_error;
+  a.paths = (int64_t)dims->B * dims->T * dims->N;
+  a.ld_d = dims->ld_draft;
+  a.ld_t = dims->ld_target;
+  a.L = dims->L;
+  a.step = step;
+  a.Vd = dims->v_draft;
+  a.Vt = dims->v_target;
+  a.inv_tq = 1.0f / temp_draft;
+  a.inv_tp = 1.0f / temp_target;
+  a.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(seed >> 32);
+  a.offset = offset;
+  hipError_t e = vsd::launch_sample_step(a, dims->dtype == VSD_BF16, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "k_sample_step launch");
+  return ok();
+}
+
+vsd_status vsd_score_paths_ctx(const vsd_dims* dims, const vsd_params* params, const vsd_ctx_rows* rows,
+                               const int32_t* d2t, const int32_t* valid_depth, const int32_t* tok_draft,
+                               const int32_t* tok_target, const int32_t* tok_greedy, const vsd_score_out* out,
+                               float* lse_draft_corr, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_ctx_rows(dims, rows, 3, 3)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token inputs must not be NULL");
+  if ((st = check_score_out(dims, out, workspace, workspace_bytes)) != VSD_OK) return st;
+  if ((st = check_kl_out(dims, params, out)) != VSD_OK) return st;
+  if (lse_draft_corr == nullptr) return fail(VSD_ERR_NULL_POINTER, "lse_draft_corr is NULL");
+
+  const WorkspaceLayout wl = workspace_layout(dims);
+  char* ws = static_cast<char*>(workspace);
+  float* la = out->log_alpha != nullptr ? out->log_alpha : reinterpret_cast<float*>(ws + wl.la);
+  float* lq = out->log_q_tok != nullptr ? out->log_q_tok : reinterpret_cast<float*>(ws + wl.lq);
+  float* loss_pos = out->loss_pos != nullptr ? out->loss_pos : reinterpret_cast<float*>(ws + wl.loss);
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const int32_t* const tok[3] = {tok_draft, tok_target, tok_greedy};
+  float* kl_row = nullptr;
+  if ((st = score_rows(dims, params, rows->draft, rows->target, true, d2t, valid_depth, tok, out, lse_draft_corr, ws,
+                       wl, la, lq, &kl_row, s)) != VSD_OK)
+    return st;
+  if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s)) != VSD_OK)
+    return st;
+  return ok();
+}
+
+vsd_status vsd_weighted_loss_bwd_ctx(const vsd_dims* dims, const vsd_params* params, const vsd_ctx_rows* rows,
+                                     const float* lse_draft, const float* lse_draft_corr, const int32_t* tok_draft,
+                                     const int32_t* tok_target, const float* coef_a, const float* coef_b,
+                                     const int32_t* kl_idx, const float* kl_grad, void* grad_draft_path,
+                                     void* grad_corr_path, int32_t* device_error, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_ctx_rows(dims, rows, 2, 0)) != VSD_OK) return st;
+  if (lse_draft == nullptr || lse_draft_corr == nullptr || tok_draft == nullptr || tok_target == nullptr ||
+      coef_a == nullptr || coef_b == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "log-sum-exps, tokens and coefficients are required");
+  if (grad_draft_path == nullptr || grad_corr_path == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "grad_draft_path and grad_corr_path are required");
+  if (grad_draft_path == grad_corr_path)
+    return fail(VSD_ERR_INVALID_VALUE, "grad_draft_path and grad_corr_path must be distinct buffers");
+  if (!aligned16(grad_draft_path) || !aligned16(grad_corr_path))
+    return fail(VSD_ERR_MISALIGNED, "gradient buffers not 16-byte aligned");
+  if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+  if (kl_on(params) && (kl_idx == nullptr || kl_grad == nullptr))
+    return fail(VSD_ERR_NULL_POINTER, "kl_idx and kl_grad are required with kl_weight > 0");
+
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  for (int f = 0; f < 2; ++f) {  // a-part on the rows along z~, b-part on the rows along z'
+    vsd::BwdArgs a{};
+    a.X = rows->draft[f];
+    a.G = f == 0 ? grad_draft_path : grad_corr_path;
+    a.lse_q = f == 0 ? lse_draft : lse_draft_corr;
+    a.tok_d = tok_draft;
+    a.tok_t = tok_target;
+    a.coef_a = f == 0 ? coef_a : nullptr;
+    a.coef_b = f == 0 ? nullptr : coef_b;
+    a.R = rows_of(dims);
+    a.ld = dims->ld_draft;
+    a.Vd = dims->v_draft;
+    a.inv_tq = 1.0f / params->temp_draft;
+    a.scale = params->loss_scale;
+    if (kl_on(params) && f == 0) {
+      a.kl_idx = kl_idx;
+      a.kl_grad = kl_grad;
+      a.kl_k = params->kl_topk;
+    }
+    hipError_t e = vsd::launch_bwd(a, dims->dtype == VSD_BF16, s);
+    if (e != hipSuccess) return hip_fail(e, "k_bwd launch");
+  }
   return ok();
 }
 

@@ -35,13 +35,32 @@ struct SampleArgs {
   float kl_gscale;           // loss_scale * kl_weight / N / T_q
 };
 
+// One depth of a rollout with exact context (vsd_sample_step): path p's rows
+// are X + p ld_d (along z~), Y + p ld_t (along z'), Yg + p ld_t (along
+// z-bar); its tokens go to row p L + step of the token arrays.
+struct SampleStepArgs {
+  const void* X;
+  const void* Y;
+  const void* Yg;
+  const int32_t* d2t;        // [Vd] or null
+  const int32_t* depth;      // [paths] or null
+  int32_t* tok_d;
+  int32_t* tok_t;
+  int32_t* tok_g;
+  int32_t* err;
+  int64_t paths, ld_d, ld_t;
+  int32_t L, step, Vd, Vt;
+  float inv_tq, inv_tp;
+  uint32_t k0, k1, offset;
+};
+
 struct ScoreRowArgs {
   const void* X;
   const void* Y;
   const int32_t* d2t;
   const int32_t* depth;
   const int32_t* tok[3];     // draft, target, greedy
-  float* lse_q;              // [R] required
+  float* lse_q;              // [R] optional
   float* lse_p;              // [R] optional
   float* la;                 // [R,3]
   float* lq;                 // [R,3]
@@ -49,6 +68,7 @@ struct ScoreRowArgs {
   int64_t R, ld_d, ld_t;
   int32_t L, Vd, Vt;
   float inv_tq, inv_tp;
+  int32_t fam_lo, fam_hi;    // families [fam_lo, fam_hi) gathered on these rows (columns of la / lq)
   // top-K renormalised KL term (kl_k > 0 turns it on)
   int32_t kl_k;
   const uint32_t* map_mask;  // [ceil(Vt/32)] bit t: target column t is mapped (with d2t)
@@ -89,8 +109,8 @@ struct BwdArgs {
   const float* lse_q;
   const int32_t* tok_d;
   const int32_t* tok_t;
-  const float* coef_a;
-  const float* coef_b;
+  const float* coef_a;       // [R], or null: a = 0
+  const float* coef_b;       // [R], or null: b = 0
   int64_t R, ld;
   int32_t Vd;
   float inv_tq, scale;
@@ -186,6 +206,7 @@ hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s);
 hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);
+hipError_t launch_sample_step(const SampleStepArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s);

@@ -11,6 +11,10 @@ outputs [B*T*N]; per-position outputs [B*T].
 Wherever a logit tensor is accepted, an LmHead(hidden [R, H], weight [V, H])
 may be given instead (both models alike): the fused LM-head variant, whose
 logits hidden @ weight.T are computed inside the kernels and never stored.
+
+Exact context (sample_step, score_paths_ctx, weighted_loss_bwd_ctx): each
+family (z~, z', z-bar) has its own rows, the conditionals along its own path;
+sample_step draws one depth of such a rollout at a time.
 """
 import ctypes
 from dataclasses import dataclass
@@ -23,7 +27,8 @@ from ._lib import (VSD_BF16, VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_F32, VSD_GRAD_AR
                    VSD_GRAD_BASIC, VsdError)
 
 __all__ = ["Problem", "Params", "LmHead", "LmHeadGrad", "SampleResult", "ScoreResult", "sample_paths",
-           "score_paths", "sample_score_paths", "weighted_loss_bwd", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
+           "score_paths", "sample_score_paths", "weighted_loss_bwd", "sample_step", "score_paths_ctx",
+           "weighted_loss_bwd_ctx", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
            "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]
 
 
@@ -106,6 +111,7 @@ class ScoreResult(NamedTuple):
     kl_grad: Optional[torch.Tensor] = None  # [R, K] float32
     kl_row: Optional[torch.Tensor] = None   # [R]
     kl_pos: Optional[torch.Tensor] = None   # [P]
+    lse_draft_corr: Optional[torch.Tensor] = None  # [R] exact context: draft log-sum-exp of the rows along z'
 
 
 def _ptr(t):
@@ -339,3 +345,121 @@ def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a,
                                          _ptr(coef_b), _ptr(kl_idx), _ptr(kl_grad), ctypes.byref(g),
                                          _ptr(device_error), _stream(dev)))
     return grad
+
+
+def _check_rows(name, t, nrows, v, like=None):
+    if not t.is_cuda or t.dim() != 2 or t.shape[0] != nrows or t.shape[1] < v or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a device tensor [{nrows}, ld>={v}] with unit column stride, "
+                         f"got {tuple(t.shape)}")
+    _dtype_code(t)
+    if like is not None and (t.dtype != like.dtype or t.stride(0) != like.stride(0)):
+        raise ValueError(f"{name} must share dtype and row stride with the first row tensor")
+
+
+def _ctx_dims(prob, X, Y):
+    return _lib.VsdDims(prob.B, prob.T, prob.N, prob.L, prob.v_draft, prob.v_target, _dtype_code(X), 0,
+                        X.stride(0), Y.stride(0) if Y is not None else X.stride(0))
+
+
+def sample_step(prob, step, X_rows, Y_rows, Yg_rows, d2t=None, valid_depth=None, temp_draft=1.0,
+                temp_target=1.0, seed=0, offset=0, tokens=None, device_error=None):
+    """One depth (0-based `step`) of a rollout with exact context: X_rows
+    [P*N, ld] draft logits along z~, Y_rows / Yg_rows [P*N, ld] target
+    logits along z' / z-bar at this depth.  Fills row p*L + step of the
+    three [R] token tensors (allocated, -1 filled, when tokens is None) and
+    returns SampleResult."""
+    lib = _lib.load()
+    n = prob.P * prob.N
+    _check_rows("X_rows", X_rows, n, prob.v_draft)
+    _check_rows("Y_rows", Y_rows, n, prob.v_target)
+    _check_rows("Yg_rows", Yg_rows, n, prob.v_target, like=Y_rows)
+    if Y_rows.dtype != X_rows.dtype:
+        raise ValueError("draft and target rows must share a dtype")
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, n)
+    dev = X_rows.device
+    if tokens is None:
+        tokens = [torch.full((prob.R,), -1, dtype=torch.int32, device=dev) for _ in range(3)]
+    for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), tokens):
+        _check_i32(name, t, prob.R)
+    if device_error is None:
+        device_error = torch.zeros(1, dtype=torch.int32, device=dev)
+    dims = _ctx_dims(prob, X_rows, Y_rows)
+    _lib.check(lib.vsd_sample_step(ctypes.byref(dims), int(step), _ptr(X_rows), _ptr(Y_rows), _ptr(Yg_rows),
+                                   _ptr(d2t), _ptr(valid_depth), temp_draft, temp_target, int(seed), int(offset),
+                                   _ptr(tokens[0]), _ptr(tokens[1]), _ptr(tokens[2]), _ptr(device_error),
+                                   _stream(dev)))
+    return SampleResult(tokens[0], tokens[1], tokens[2], device_error)
+
+
+def _ctx_rows(Xs, Ys):
+    rows = _lib.VsdCtxRows()
+    for f in range(3):
+        rows.draft[f] = Xs[f].data_ptr() if f < len(Xs) else None
+        rows.target[f] = Ys[f].data_ptr() if Ys is not None and f < len(Ys) else None
+    return rows
+
+
+def score_paths_ctx(prob, params, Xs, Ys, tok_draft, tok_target, tok_greedy, d2t=None, valid_depth=None,
+                    out: Optional[ScoreResult] = None, workspace=None):
+    """score_paths with exact context: Xs, Ys = three [R, ld] tensors each,
+    the rows along z~, z' and z-bar.  The result's lse_draft_corr holds the
+    draft log-sum-exp of the rows along z'."""
+    lib = _lib.load()
+    if len(Xs) != 3 or len(Ys) != 3:
+        raise ValueError("Xs and Ys must hold three row tensors each (along z~, z', z-bar)")
+    for f in range(3):
+        _check_rows(f"Xs[{f}]", Xs[f], prob.R, prob.v_draft, like=Xs[0] if f else None)
+        _check_rows(f"Ys[{f}]", Ys[f], prob.R, prob.v_target, like=Ys[0] if f else None)
+    if Ys[0].dtype != Xs[0].dtype:
+        raise ValueError("draft and target rows must share a dtype")
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    for name, t in (("tok_draft", tok_draft), ("tok_target", tok_target), ("tok_greedy", tok_greedy)):
+        _check_i32(name, t, prob.R)
+    dev = Xs[0].device
+    if out is None:
+        out = alloc_score_outputs(prob, dev, kl_topk=params.kl_topk if params.kl_weight > 0 else 0)
+    if out.lse_draft_corr is None:
+        out = out._replace(lse_draft_corr=torch.empty(prob.R, dtype=torch.float32, device=dev))
+    nbytes = score_workspace_bytes(prob, Xs[0].dtype)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dims = _ctx_dims(prob, Xs[0], Ys[0])
+    names = [f[0] for f in _lib.VsdScoreOut._fields_]
+    so = _lib.VsdScoreOut(*[None if getattr(out, k) is None else getattr(out, k).data_ptr() for k in names])
+    pr = params.c()
+    rows = _ctx_rows(Xs, Ys)
+    _lib.check(lib.vsd_score_paths_ctx(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(rows), _ptr(d2t),
+                                       _ptr(valid_depth), _ptr(tok_draft), _ptr(tok_target), _ptr(tok_greedy),
+                                       ctypes.byref(so), _ptr(out.lse_draft_corr), _ptr(workspace),
+                                       workspace.numel(), _stream(dev)))
+    return out
+
+
+def weighted_loss_bwd_ctx(prob, params, Xs, lse_draft, lse_draft_corr, tok_draft, tok_target, coef_a, coef_b,
+                          grads=None, device_error=None, kl_idx=None, kl_grad=None):
+    """weighted_loss_bwd with exact context: returns (grad on the rows along
+    z~, grad on the rows along z'), each shaped, strided and typed as Xs[0]."""
+    lib = _lib.load()
+    if len(Xs) < 2:
+        raise ValueError("Xs must hold the rows along z~ and along z'")
+    _check_rows("Xs[0]", Xs[0], prob.R, prob.v_draft)
+    _check_rows("Xs[1]", Xs[1], prob.R, prob.v_draft, like=Xs[0])
+    dev = Xs[0].device
+    if grads is None:
+        grads = (torch.empty_like(Xs[0]), torch.empty_like(Xs[0]))
+    for g in grads:
+        if g.shape != Xs[0].shape or g.stride() != Xs[0].stride() or g.dtype != Xs[0].dtype:
+            raise ValueError("gradients must match Xs[0] in shape, stride and dtype")
+    if device_error is None:
+        device_error = torch.zeros(1, dtype=torch.int32, device=dev)
+    dims = _ctx_dims(prob, Xs[0], None)
+    pr = params.c()
+    rows = _ctx_rows(Xs[:2], None)
+    _lib.check(lib.vsd_weighted_loss_bwd_ctx(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(rows),
+                                             _ptr(lse_draft), _ptr(lse_draft_corr), _ptr(tok_draft),
+                                             _ptr(tok_target), _ptr(coef_a), _ptr(coef_b), _ptr(kl_idx),
+                                             _ptr(kl_grad), _ptr(grads[0]), _ptr(grads[1]), _ptr(device_error),
+                                             _stream(dev)))
+    return grads

@@ -9,6 +9,7 @@ library's tests and the oracle's consume what it returns.
 """
 from .configs import CONFIGS, Config, get_config, scaled
 from .gen import make_inputs, make_inputs_numpy_c1, positions_rows
+from .rollout import context_rows, depth_view, make_tables
 
 __all__ = ["CONFIGS", "Config", "get_config", "scaled", "make_inputs",
-           "make_inputs_numpy_c1", "positions_rows"]
+           "make_inputs_numpy_c1", "positions_rows", "context_rows", "depth_view", "make_tables"]

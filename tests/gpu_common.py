@@ -156,19 +156,25 @@ def compare(cfg, gpu, rows, ora, positions, check_grad=True, label=""):
         bad = np.argwhere(~ok)
         assert bad.size == 0, f"{label} {name}: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {got[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
         worst[name] = float(np.max(np.abs(got - ref))) if got.size else 0.0
-    # 4. gradient
-    if check_grad and "grad" in ora:
-        g = gpu["grad"].index_select(0, torch.as_tensor(rows, device=gpu["grad"].device))[:, :cfg.v_draft]
-        g = g.float().cpu().numpy()
-        ref = ora["grad"]
-        err = np.abs(g - ref)
-        if gpu["grad"].dtype == torch.bfloat16:
-            ok = (err <= 2e-3) | ((np.abs(ref) >= 1.0) & (err <= _bf16_ulp(ref)))
-        else:
-            ok = err <= 2e-3
-        ok |= ~keep_rows[:, None]
-        bad = np.argwhere(~ok)
-        assert bad.size == 0, f"{label} grad: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {g[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
-        worst["grad"] = float(err[keep_rows].max()) if keep_rows.any() else 0.0
+    # 4. gradient (exact context: also the one on the rows along z')
+    for name in ("grad", "grad_corr"):
+        if check_grad and name in ora and name in gpu:
+            worst[name] = check_grad_rows(cfg, gpu[name], ora[name], rows, keep_rows, f"{label} {name}")
     return dict(worst=worst, near_tie_positions=sorted(tied_pos))
+
+
+def check_grad_rows(cfg, grad, ref, rows, keep_rows, label):
+    """Assert a device gradient [R, ld] equals the oracle's on `rows` under the
+    gradient bar; returns the largest error."""
+    g = grad.index_select(0, torch.as_tensor(rows, device=grad.device))[:, :cfg.v_draft]
+    g = g.float().cpu().numpy()
+    err = np.abs(g - ref)
+    if grad.dtype == torch.bfloat16:
+        ok = (err <= 2e-3) | ((np.abs(ref) >= 1.0) & (err <= _bf16_ulp(ref)))
+    else:
+        ok = err <= 2e-3
+    ok |= ~keep_rows[:, None]
+    bad = np.argwhere(~ok)
+    assert bad.size == 0, f"{label}: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {g[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
+    return float(err[keep_rows].max()) if keep_rows.any() else 0.0
 

@@ -36,7 +36,7 @@ def test_every_declared_function_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.vsd_abi_version() == 2
+    assert lib.vsd_abi_version() == 3
     for code, name in _lib.STATUS_NAMES.items():
         assert lib.vsd_status_string(code).decode() == name
     assert lib.vsd_status_string(99).decode() == "VSD_ERR_UNKNOWN"
@@ -236,3 +236,51 @@ def test_kl_term_validation(lib):
                                     ctypes.byref(src), ctypes.byref(src), None, None, 0, 0, FAKE, FAKE, FAKE,
                                     ctypes.byref(full), FAKE, 1 << 30, None)
     assert st == 3                                   # one-pass call: kl_topk beyond the draft vocabulary
+
+
+def test_exact_context_validation(lib):
+    """vsd_sample_step, vsd_score_paths_ctx and vsd_weighted_loss_bwd_ctx
+    reject invalid arguments before any launch."""
+    def step(dims=None, s=0, rows=(FAKE, FAKE, FAKE), d2t=None, temps=(1.0, 1.0), toks=(FAKE, FAKE, FAKE), err=FAKE):
+        d = dims if dims is not None else _dims()
+        return lib.vsd_sample_step(ctypes.byref(d), s, *rows, d2t, None, *temps, 0, 0, *toks, err, None)
+
+    assert step(s=-1) == 3 and step(s=3) == 3                      # step outside [0, L)
+    assert step(rows=(None, FAKE, FAKE)) == 1 and step(rows=(FAKE, FAKE, None)) == 1
+    assert step(rows=(FAKE + 8, FAKE, FAKE)) == 4
+    assert step(dims=_dims(ld_draft=999)) == 2
+    assert step(dims=_dims(hidden_dim=128, dtype=_lib.VSD_BF16)) == 6
+    assert step(dims=_dims(v_target=2000, ld_target=2000)) == 5     # map required
+    assert step(temps=(0.0, 1.0)) == 3
+    assert step(toks=(FAKE, None, FAKE)) == 1 and step(err=None) == 1
+
+    out = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    rows = _lib.VsdCtxRows((ctypes.c_void_p * 3)(FAKE, FAKE, FAKE), (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE))
+
+    def score(dims=None, params=None, r=rows, corr=FAKE, o=out):
+        d = dims if dims is not None else _dims()
+        p = params if params is not None else _params()
+        return lib.vsd_score_paths_ctx(ctypes.byref(d), ctypes.byref(p), None if r is None else ctypes.byref(r), None,
+                                       None, FAKE, FAKE, FAKE, ctypes.byref(o), corr, FAKE, 1 << 30, None)
+
+    assert score(r=None) == 1
+    partial = _lib.VsdCtxRows((ctypes.c_void_p * 3)(FAKE, FAKE, None), (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE))
+    assert score(r=partial) == 1
+    partial = _lib.VsdCtxRows((ctypes.c_void_p * 3)(FAKE, FAKE, FAKE), (ctypes.c_void_p * 3)(FAKE, FAKE + 4, FAKE))
+    assert score(r=partial) == 4
+    assert score(corr=None) == 1
+    assert score(dims=_dims(ld_target=999)) == 2
+    assert score(dims=_dims(hidden_dim=128, dtype=_lib.VSD_BF16)) == 6
+    assert score(params=_params(kl_weight=0.5, kl_topk=10)) == 1          # kl_idx / kl_grad required
+    assert score(params=_params(car_tau=0.0)) == 3
+
+    def bwd(dims=None, corr=FAKE, gd=FAKE, gc=FAKE + 4096, ca=FAKE, err=FAKE):
+        d = dims if dims is not None else _dims()
+        p = _params()
+        return lib.vsd_weighted_loss_bwd_ctx(ctypes.byref(d), ctypes.byref(p), ctypes.byref(rows), FAKE, corr, FAKE,
+                                             FAKE, ca, FAKE, None, None, gd, gc, err, None)
+
+    assert bwd(gc=FAKE) == 3                                               # aliased gradient buffers
+    assert bwd(gd=None) == 1 and bwd(corr=None) == 1 and bwd(ca=None) == 1 and bwd(err=None) == 1
+    assert bwd(gc=FAKE + 8) == 4
+    assert bwd(dims=_dims(hidden_dim=128, dtype=_lib.VSD_BF16)) == 6
