@@ -10,7 +10,8 @@ scoring in one pass over the logits) and vsd_weighted_loss_bwd on one stream.
 The same step through the three separate calls (vsd_sample_paths,
 vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it,
 and the step once more, both ways, with the top-K renormalised KL term on
-(K = 10, "kl_variant").
+(K = 10, "kl_variant"), and with exact context ("exact_context": each family
+on its own rows, drawn depth by depth).
 W untimed steps, then exactly K steps timed between stream synchronisations;
 per-call durations come from HIP events recorded on the stream the kernels
 run on.
@@ -241,6 +242,7 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=0)
     ap.add_argument("--no-lm-head", action="store_true", help="skip the fused LM-head measurement")
     ap.add_argument("--lm-steps", type=int, default=3, help="timed steps of the fused LM-head measurement")
+    ap.add_argument("--no-ctx", action="store_true", help="skip the exact-context measurement")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this size first (calibrates PMC byte counters)")
     args = ap.parse_args()
@@ -427,11 +429,73 @@ def main():
         "kernels": kernels, "three_calls": three_calls, "kl_variant": kl_variant, "roofline": roof,
         "cpu_baseline": base,
     }
+    if not args.no_ctx:
+        line["exact_context"] = bench_ctx(cfg, prob, params, inp, ws, timed, live, dev)
     if not args.no_lm_head:
         del inp, X, Y, out, out_kl, ws, grad
         torch.cuda.empty_cache()
         line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
     print(json.dumps(line), flush=True)
+
+
+def bench_ctx(cfg, prob, params, inp, ws, timed, live, dev):
+    """The step with exact context on the same workload: each family has its
+    own rows (two more copies of X and Y, distinct buffers), the draws go
+    depth by depth (L vsd_sample_step calls), then vsd_score_paths_ctx and
+    vsd_weighted_loss_bwd_ctx.  Bytes: scoring reads every live row of all
+    three families, es (V_d + V_t) each; the backward reads the rows along z~
+    (z') whose a (b) is nonzero and writes both gradients in full."""
+    import torch
+
+    import paper_2602_05774_amd as vsd
+    from synth import depth_view
+    X, Y, d2t, depth = inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"]
+    need = 2 * (X.numel() + Y.numel()) * X.element_size() + 2 * X.numel() * X.element_size()
+    free, _ = torch.cuda.mem_get_info(dev)
+    if free < need + (4 << 30):
+        return {"skipped": f"needs {need / 2**30:.1f} GiB more device memory, {free / 2**30:.1f} free"}
+    Xs = [X, X.clone(), X.clone()]
+    Ys = [Y, Y.clone(), Y.clone()]
+    grads = (torch.empty_like(X), torch.empty_like(X))
+    out = vsd.alloc_score_outputs(prob, dev, full=False)
+    out = out._replace(lse_draft_corr=torch.empty(prob.R, dtype=torch.float32, device=dev))
+    toks = [torch.full((prob.R,), -1, dtype=torch.int32, device=dev) for _ in range(3)]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    n = cfg.P * cfg.N
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        for i in range(cfg.L):
+            vsd.sample_step(prob, i, depth_view(Xs[0], n, cfg.L, i), depth_view(Ys[1], n, cfg.L, i),
+                            depth_view(Ys[2], n, cfg.L, i), d2t, depth, cfg.temp_draft, cfg.temp_target,
+                            cfg.philox_seed, cfg.philox_offset, tokens=toks, device_error=err)
+        if ev:
+            ev[1].record()
+        vsd.score_paths_ctx(prob, params, Xs, Ys, *toks, d2t, depth, out=out, workspace=ws)
+        if ev:
+            ev[2].record()
+        vsd.weighted_loss_bwd_ctx(prob, params, Xs, out.lse_draft, out.lse_draft_corr, toks[0], toks[1], out.coef_a,
+                                  out.coef_b, grads=grads, device_error=err)
+        if ev:
+            ev[3].record()
+
+    (t_sample, t_score, t_bwd), t_step, _ = timed(step, 4)
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+        raise RuntimeError("device error reported during the exact-context benchmark")
+    es = X.element_size()
+    na = int((out.coef_a != 0).sum().item())
+    nb = int((out.coef_b != 0).sum().item())
+    score_bytes = 3 * live * es * (cfg.v_draft + cfg.v_target)
+    bwd_bytes = (na + nb) * es * cfg.v_draft + 2 * prob.R * es * cfg.v_draft
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    res = {"ms_per_step": t_step, "path_tokens_per_s": live / (t_step * 1e-3), "sample_steps_ms": t_sample,
+           "score_ms": t_score, "score_bytes": score_bytes, "score_GB/s": gbs(score_bytes, t_score),
+           "bwd_ms": t_bwd, "bwd_bytes": bwd_bytes, "bwd_GB/s": gbs(bwd_bytes, t_bwd),
+           "score_bwd_frac_of_hbm_peak": gbs(score_bytes + bwd_bytes, t_score + t_bwd) / HBM_PEAK_GBS}
+    del Xs, Ys, grads
+    torch.cuda.empty_cache()
+    return res
 
 
 def main_lm_head(args, cfg):
