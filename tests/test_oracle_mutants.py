@@ -18,6 +18,7 @@ from scipy import stats
 
 import oracle.paths as paths_mod
 import oracle.sampler as sampler_mod
+import oracle.verify as verify_mod
 
 GOLDEN = ["micro_example.json", "ragged_example.json", "car_example.json"]
 MODES = {"BASIC": 0, "ARW": 1, "ARW_CAR": 2, "ARW_CAR_LOGPROB": 2}
@@ -213,6 +214,45 @@ def _check_sampler(S):
     return True
 
 
+def _check_verify(V):
+    """Speculative sampling theorem (emitted token ~ p, with a map) and the
+    closed-form mean accepted length."""
+    rng = np.random.default_rng(1)
+    Vd, Vt, N = 4, 7, 3000
+    d2t = np.array([0, 2, 3, 6])
+    x = rng.normal(0, 1.0, Vd).astype(np.float32)
+    y = rng.normal(0, 1.0, Vt).astype(np.float32)
+    X = np.broadcast_to(x, (N, 1, Vd)).copy()
+    Y = np.broadcast_to(y, (N, 1, Vt)).copy()
+    z = sampler_mod.first_argmax(sampler_mod.gumbel_keys(X[:, 0], np.arange(N), 0, 1.0, 3, 0)).reshape(N, 1)
+    acc, res, _, _ = V.verify_position(X, Y, d2t, np.ones(N, int), z, 0, seed=3)
+    emitted = np.where(acc == 1, d2t[z[:, 0]], res)
+    if np.any(emitted < 0) or stats.chisquare(np.bincount(emitted, minlength=Vt), _softmax(y.astype(float)) * N)[1] < 1e-4:
+        return False
+    L, V_, N = 3, 6, 1500
+    q_rows = rng.normal(0, 1.5, (L, V_)).astype(np.float32)
+    p_rows = rng.normal(0, 1.5, (L, V_)).astype(np.float32)
+    X = np.broadcast_to(q_rows, (N, L, V_)).copy()
+    Y = np.broadcast_to(p_rows, (N, L, V_)).copy()
+    z = sampler_mod.first_argmax(sampler_mod.gumbel_keys(X.reshape(-1, V_), np.arange(N * L), 0, 1.0, 9, 0))
+    acc, _, _, _ = V.verify_position(X, Y, None, np.full(N, L), z.reshape(N, L), 0, seed=9)
+    closed, prod = 0.0, 1.0
+    for i in range(L):
+        prod *= np.minimum(_softmax(p_rows[i].astype(float)), _softmax(q_rows[i].astype(float))).sum()
+        closed += prod
+    return abs(acc.mean() - closed) < 5 * acc.std() / math.sqrt(N)
+
+
+VERIFY_MUTANTS = [
+    ("if lu < log_alpha:", "if lu > log_alpha:"),
+    ("res = np.maximum(0.0, p - q)", "res = np.maximum(0.0, q - p)"),
+    ("res = np.maximum(0.0, p - q)", "res = p"),
+    ("q[d2t] = np.exp(x / temp_draft - lse_q)", "q[:Vd] = np.exp(x / temp_draft - lse_q)"),
+    ("                                                seed, offset)\n            break", "                                                seed, offset)"),
+    ("(Y[s, i, d2t_arr[z]] / temp_target - lse_p)", "(Y[s, i, z] / temp_target - lse_p)"),
+]
+
+
 PATH_MUTANTS = [
     ("np.minimum(0.0, log_p - log_q)", "np.maximum(0.0, log_p - log_q)"),
     ("np.minimum(0.0, log_p - log_q)", "np.minimum(0.0, log_q - log_p)"),
@@ -269,6 +309,13 @@ def test_unmutated_oracle_passes_every_check(golden_dir):
     assert _check_map(paths_mod)
     assert _check_ctx(paths_mod)
     assert _check_sampler(sampler_mod)
+    assert _check_verify(verify_mod)
+
+
+@pytest.mark.parametrize("old,new", VERIFY_MUTANTS, ids=[f"verify{i}" for i in range(len(VERIFY_MUTANTS))])
+def test_verify_mutant_is_caught(old, new):
+    V = _mutant(verify_mod, old, new)
+    assert not _check_verify(V), f"no pin caught mutant {new!r}"
 
 
 @pytest.mark.parametrize("old,new", PATH_MUTANTS, ids=[f"paths{i}" for i in range(len(PATH_MUTANTS))])
