@@ -195,7 +195,7 @@
 extern "C" {
 #endif
 
-#define VSD_ABI_VERSION 3
+#define VSD_ABI_VERSION 4
 
 typedef enum vsd_status {
   VSD_OK = 0,
@@ -416,6 +416,32 @@ vsd_status vsd_weighted_loss_bwd_ctx(const vsd_dims* dims, const vsd_params* par
                                      const int32_t* kl_idx, const float* kl_grad,
                                      void* grad_draft_path, void* grad_corr_path,
                                      int32_t* device_error, void* hip_stream);
+
+/* Decode-time verification of the draft paths (Sec. "Preliminary", Eq.
+ * acc): slot by slot, z~_i is kept iff Lambda(u_i) < log alpha_i, with u_i
+ * the uniform of Philox counter (0, row, 2, offset) word 0 (the sampler
+ * definition's u and normative log) and log alpha from vsd_score_paths
+ * (log_alpha [R,3], column 0); at the first rejection a replacement is drawn
+ * from norm(max(0, p - q)) over the whole target vocabulary (q(t) = q(v) for
+ * t = d2t[v], 0 for target tokens the draft cannot propose; p and q from the
+ * row's logits and lse_target / lse_draft) by Gumbel-max of
+ * log(max(0, p - q)) with the sampler's Gumbel variates over target indices
+ * t (counter (t >> 2, row, 3, offset), word t & 3), and the path ends.
+ * accept_len [P*N] receives the number of kept tokens (its mean given the
+ * path is the expected accepted length sum_k S_k); resample_tok [P*N] the
+ * replacement's target index, -1 when every live token was kept (no bonus
+ * token is drawn: there is no row for it) or, with probability ~1e-7, when
+ * the residual mass vanishes in float32.  With a map, `workspace` must hold
+ * vsd_score_workspace_bytes() bytes (its inverse-map region is rebuilt);
+ * without one it may be NULL.  Materialised logits only. */
+vsd_status vsd_verify_paths(const vsd_dims* dims, const vsd_params* params,
+                            const vsd_src* draft, const vsd_src* target,
+                            const int32_t* d2t, const int32_t* valid_depth,
+                            const float* log_alpha, const float* lse_draft,
+                            const float* lse_target, uint64_t seed, uint32_t offset,
+                            int32_t* accept_len, int32_t* resample_tok,
+                            void* workspace, size_t workspace_bytes,
+                            int32_t* device_error, void* hip_stream);
 
 /* Bytes of workspace vsd_score_paths needs for `dims` (host only). */
 vsd_status vsd_score_workspace_bytes(const vsd_dims* dims, size_t* bytes);

@@ -56,7 +56,7 @@ class VsdGrad(ctypes.Structure):
 _lib = None
 
 EXPORTS = ("vsd_sample_paths", "vsd_score_paths", "vsd_sample_score_paths", "vsd_weighted_loss_bwd",
-           "vsd_sample_step", "vsd_score_paths_ctx", "vsd_weighted_loss_bwd_ctx",
+           "vsd_sample_step", "vsd_score_paths_ctx", "vsd_weighted_loss_bwd_ctx", "vsd_verify_paths",
            "vsd_score_workspace_bytes", "vsd_status_string", "vsd_last_error", "vsd_abi_version")
 
 
@@ -92,6 +92,9 @@ def load():
     lib.vsd_weighted_loss_bwd_ctx.argtypes = [P(VsdDims), P(VsdParams), P(VsdCtxRows), c_vp, c_vp, c_vp, c_vp,
                                               c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
     lib.vsd_weighted_loss_bwd_ctx.restype = c_i32
+    lib.vsd_verify_paths.argtypes = [P(VsdDims), P(VsdParams), P(VsdSrc), P(VsdSrc), c_vp, c_vp, c_vp, c_vp, c_vp,
+                                     ctypes.c_uint64, ctypes.c_uint32, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp, c_vp]
+    lib.vsd_verify_paths.restype = c_i32
     lib.vsd_score_workspace_bytes.argtypes = [P(VsdDims), P(ctypes.c_size_t)]
     lib.vsd_score_workspace_bytes.restype = c_i32
     lib.vsd_status_string.argtypes = [c_i32]

@@ -779,4 +779,62 @@ vsd_status vsd_weighted_loss_bwd_ctx(const vsd_dims* dims, const vsd_params* par
   return ok();
 }
 
+vsd_status vsd_verify_paths(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                            const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                            const float* log_alpha, const float* lse_draft, const float* lse_target, uint64_t seed,
+                            uint32_t offset, int32_t* accept_len, int32_t* resample_tok, void* workspace,
+                            size_t workspace_bytes, int32_t* device_error, void* hip_stream) {
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if (is_fused(dims)) return fail(VSD_ERR_UNSUPPORTED, "verification: materialised logits only (hidden_dim must be 0)");
+  if ((st = check_sources(dims, draft, target)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (log_alpha == nullptr || lse_draft == nullptr || lse_target == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "log_alpha, lse_draft and lse_target (from scoring) are required");
+  if (accept_len == nullptr || resample_tok == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "accept_len and resample_tok are required");
+  if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
+  const WorkspaceLayout wl = workspace_layout(dims);
+  if (d2t != nullptr) {
+    if (workspace == nullptr || workspace_bytes < wl.total)
+      return fail(VSD_ERR_WORKSPACE, "workspace of %zu bytes required, %zu given", wl.total,
+                  workspace == nullptr ? (size_t)0 : workspace_bytes);
+    if (!aligned16(workspace)) return fail(VSD_ERR_MISALIGNED, "workspace not 16-byte aligned");
+  }
+
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  int32_t* inv = nullptr;
+  if (d2t != nullptr) {
+    inv = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + wl.inv);
+    hipError_t e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, device_error, s);
+    if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
+  }
+  vsd::VerifyArgs a{};
+  a.X = draft->logits;
+  a.Y = target->logits;
+  a.inv = inv;
+  a.depth = valid_depth;
+  a.la = log_alpha;
+  a.lse_q = lse_draft;
+  a.lse_p = lse_target;
+  a.accept_len = accept_len;
+  a.resample = resample_tok;
+  a.err = device_error;
+  a.paths = (int64_t)dims->B * dims->T * dims->N;
+  a.ld_d = dims->ld_draft;
+  a.ld_t = dims->ld_target;
+  a.L = dims->L;
+  a.Vd = dims->v_draft;
+  a.Vt = dims->v_target;
+  a.inv_tq = 1.0f / params->temp_draft;
+  a.inv_tp = 1.0f / params->temp_target;
+  a.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(seed >> 32);
+  a.offset = offset;
+  hipError_t e = vsd::launch_verify(a, dims->dtype == VSD_BF16, s);
+  if (e != hipSuccess) return hip_fail(e, "k_verify launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -81,10 +81,15 @@ __device__ __forceinline__ float spec_log(float x) {
   return ef * __uint_as_float(0x3F317200u) + (lm + ef * __uint_as_float(0x35BFBE8Eu));
 }
 
-// G = -log(-log u), u = (2 (w >> 9) + 1) 2^-24.
+// u = (2 (w >> 9) + 1) 2^-24: 2^23 equally spaced values in (0, 1), exact.
+__device__ __forceinline__ float uniform_from_word(uint32_t w) {
+  return (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-8f;
+}
+
+// G = -log(-log u), u = uniform_from_word(w).
 __device__ __forceinline__ float gumbel_from_word(uint32_t w) {
 #pragma clang fp contract(off)
-  const float u = (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-8f;
+  const float u = uniform_from_word(w);
   const float e = -spec_log(u);
   return -spec_log(e);
 }

@@ -1,0 +1,97 @@
+// Draw machinery shared by the sampling kernels: raw 8-element row slices,
+// the (key, index) state of a draw and one family's Philox draws with the
+// exact candidate filter (k_sample.hip states why the filter is exact).
+#pragma once
+
+#include "vsd_device.hpp"
+
+namespace vsd {
+
+__device__ __forceinline__ uint32_t word_of(const uint4& p, int k) {
+  return k == 0 ? p.x : k == 1 ? p.y : k == 2 ? p.z : p.w;
+}
+
+// Raw 8-element slice of a row as loaded (bf16: one 128-bit load).
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  uint4 v;
+  __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void unpack(float (&o)[8]) const {
+    o[0] = bf16_lo(v.x); o[1] = bf16_hi(v.x);
+    o[2] = bf16_lo(v.y); o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z); o[5] = bf16_hi(v.z);
+    o[6] = bf16_lo(v.w); o[7] = bf16_hi(v.w);
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void unpack(float (&o)[8]) const {
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+};
+
+struct Best {
+  float key;
+  int idx;
+};
+
+// State and steps common to both wavefronts of a row: the Philox draws and
+// the exact filter of one family.
+struct FamilyDraw {
+  uint32_t row, fam, offset, k0, k1;
+  float inv_t, c2;  // 1/T and log2(e)/T
+  Best best{-INFINITY, 0x7FFFFFFF};
+  float wave_best = -INFINITY;  // wavefront maximum known so far
+
+  __device__ __forceinline__ uint4 philox(uint32_t c0) const { return philox4x32_10(c0, row, fam, offset, k0, k1); }
+
+  // (thr - margin) log2e folded into the bound's constant.  The margin
+  // 2e-3 + 2e-6 |thr| exceeds every rounding involved for elements with
+  // |x/T| <= |thr| + 100; an element with x/T < thr - 100 cannot reach thr
+  // because G < 16.7.
+  __device__ __forceinline__ static float bound_offset(float thr) {
+    return 24.0f - (thr - (2e-3f + 2e-6f * fabsf(thr))) * kLog2e;
+  }
+
+  // Bound test of the 4 elements that share one Philox counter: bit k set
+  // where v * log2e/T + off >= log2(j').
+  __device__ __forceinline__ static uint32_t cand4(const uint4& w, const float* v, float c2, float off) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool c = fmaf(v[k], c2, off) >= __builtin_amdgcn_logf((float)((~word_of(w, k)) >> 8));
+      m |= c ? (1u << k) : 0u;
+    }
+    return m;
+  }
+
+  // Draw the lane's 8 elements at `base` (values v, the first nvalid valid).
+  __device__ __forceinline__ void draw(int base, const float (&v)[8], int nvalid) {
+    const uint32_t c0 = (uint32_t)base >> 2;
+    const float off = bound_offset(fmaxf(best.key, wave_best));
+    uint32_t cand = cand4(philox(c0), v, c2, off) | (cand4(philox(c0 + 1), v + 4, c2, off) << 4);
+    cand &= (1u << nvalid) - 1u;
+    if (__ballot(cand != 0u) == 0ull) return;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if (cand & (1u << k)) {  // rare: the exact key, Philox word recomputed
+        const float key = gumbel_key(v[k], inv_t, word_of(philox(c0 + (k >> 2)), k & 3));
+        if (key > best.key) {
+          best.key = key;
+          best.idx = base + k;
+        }
+      }
+    }
+    if (__ballot(best.key > wave_best) != 0ull) wave_best = wave_max(best.key);
+  }
+};
+
+}  // namespace vsd

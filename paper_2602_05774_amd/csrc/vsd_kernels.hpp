@@ -54,6 +54,24 @@ struct SampleStepArgs {
   uint32_t k0, k1, offset;
 };
 
+// Decode-time verification of the draft paths (vsd_verify_paths).
+struct VerifyArgs {
+  const void* X;             // [R, ld_d]
+  const void* Y;             // [R, ld_t]
+  const int32_t* inv;        // [Vt] draft index of target column t, -1 unmapped; null = identity
+  const int32_t* depth;      // [paths] or null
+  const float* la;           // [R, 3] log alpha of the three families (column 0: z~)
+  const float* lse_q;        // [R]
+  const float* lse_p;        // [R]
+  int32_t* accept_len;       // [paths]
+  int32_t* resample;         // [paths] target index, -1 when every token is kept
+  int32_t* err;
+  int64_t paths, ld_d, ld_t;
+  int32_t L, Vd, Vt;
+  float inv_tq, inv_tp;
+  uint32_t k0, k1, offset;
+};
+
 struct ScoreRowArgs {
   const void* X;
   const void* Y;
@@ -207,6 +225,7 @@ hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_sample_step(const SampleStepArgs& a, bool bf16, hipStream_t s);
+hipError_t launch_verify(const VerifyArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s);

@@ -28,7 +28,7 @@ from ._lib import (VSD_BF16, VSD_CAR_LOGPROB, VSD_CAR_PROB, VSD_F32, VSD_GRAD_AR
 
 __all__ = ["Problem", "Params", "LmHead", "LmHeadGrad", "SampleResult", "ScoreResult", "sample_paths",
            "score_paths", "sample_score_paths", "weighted_loss_bwd", "sample_step", "score_paths_ctx",
-           "weighted_loss_bwd_ctx", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
+           "weighted_loss_bwd_ctx", "verify_paths", "VerifyResult", "score_workspace_bytes", "VsdError", "VSD_GRAD_BASIC", "VSD_GRAD_ARW",
            "VSD_GRAD_ARW_CAR", "VSD_CAR_PROB", "VSD_CAR_LOGPROB"]
 
 
@@ -87,6 +87,12 @@ class SampleResult(NamedTuple):
     tok_draft: torch.Tensor
     tok_target: torch.Tensor
     tok_greedy: torch.Tensor
+    device_error: torch.Tensor
+
+
+class VerifyResult(NamedTuple):
+    accept_len: torch.Tensor     # [P*N] int32: kept draft tokens per path
+    resample_tok: torch.Tensor   # [P*N] int32: replacement (target index), -1 when all kept
     device_error: torch.Tensor
 
 
@@ -463,3 +469,38 @@ def weighted_loss_bwd_ctx(prob, params, Xs, lse_draft, lse_draft_corr, tok_draft
                                              _ptr(kl_grad), _ptr(grads[0]), _ptr(grads[1]), _ptr(device_error),
                                              _stream(dev)))
     return grads
+
+
+def verify_paths(prob, params, X, Y, score: ScoreResult, d2t=None, valid_depth=None, seed=0, offset=0,
+                 workspace=None, device_error=None):
+    """Decode-time verification of the draft paths scored in `score` (which
+    must hold log_alpha, lse_draft and lse_target): per path the number of
+    kept draft tokens and the replacement drawn at the first rejection."""
+    lib = _lib.load()
+    if isinstance(X, LmHead) or isinstance(Y, LmHead):
+        raise ValueError("verify_paths takes materialised logits")
+    _check_logits("X", X, prob, prob.v_draft)
+    _check_logits("Y", Y, prob, prob.v_target)
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    for name in ("log_alpha", "lse_draft", "lse_target"):
+        if getattr(score, name) is None:
+            raise ValueError(f"score.{name} is required (score with full outputs)")
+    dev = X.device
+    n = prob.P * prob.N
+    acc = torch.empty(n, dtype=torch.int32, device=dev)
+    res = torch.empty(n, dtype=torch.int32, device=dev)
+    if device_error is None:
+        device_error = torch.zeros(1, dtype=torch.int32, device=dev)
+    if d2t is not None:
+        nbytes = score_workspace_bytes(prob, X.dtype)
+        if workspace is None or workspace.numel() < nbytes:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dims = _dims(prob, X, Y)
+    pr = params.c()
+    _lib.check(lib.vsd_verify_paths(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)), ctypes.byref(_src(Y)),
+                                    _ptr(d2t), _ptr(valid_depth), _ptr(score.log_alpha), _ptr(score.lse_draft),
+                                    _ptr(score.lse_target), int(seed), int(offset), _ptr(acc), _ptr(res),
+                                    _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                    _ptr(device_error), _stream(dev)))
+    return VerifyResult(acc, res, device_error)

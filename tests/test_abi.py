@@ -36,7 +36,7 @@ def test_every_declared_function_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.vsd_abi_version() == 3
+    assert lib.vsd_abi_version() == 4
     for code, name in _lib.STATUS_NAMES.items():
         assert lib.vsd_status_string(code).decode() == name
     assert lib.vsd_status_string(99).decode() == "VSD_ERR_UNKNOWN"
@@ -284,3 +284,22 @@ def test_exact_context_validation(lib):
     assert bwd(gd=None) == 1 and bwd(corr=None) == 1 and bwd(ca=None) == 1 and bwd(err=None) == 1
     assert bwd(gc=FAKE + 8) == 4
     assert bwd(dims=_dims(hidden_dim=128, dtype=_lib.VSD_BF16)) == 6
+
+
+def test_verify_validation(lib):
+    """vsd_verify_paths rejects invalid arguments before any launch."""
+    src = _lib.VsdSrc(FAKE, None, None)
+
+    def verify(dims=None, d2t=None, la=FAKE, acc=FAKE, ws=None, nbytes=0, err=FAKE):
+        d = dims if dims is not None else _dims()
+        p = _params()
+        return lib.vsd_verify_paths(ctypes.byref(d), ctypes.byref(p), ctypes.byref(src), ctypes.byref(src), d2t,
+                                    None, la, FAKE, FAKE, 0, 0, acc, FAKE, ws, nbytes, err, None)
+
+    assert verify(la=None) == 1 and verify(acc=None) == 1 and verify(err=None) == 1
+    assert verify(dims=_dims(hidden_dim=128, dtype=_lib.VSD_BF16)) == 6
+    mapped = _dims(v_target=2000, ld_target=2000)
+    assert verify(dims=mapped) == 5                                  # map required
+    assert verify(dims=mapped, d2t=FAKE) == 7                        # workspace required with a map
+    assert verify(dims=mapped, d2t=FAKE, ws=FAKE + 8, nbytes=1 << 30) == 4
+    assert verify(dims=_dims(ld_draft=999)) == 2
