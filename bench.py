@@ -11,7 +11,9 @@ The same step through the three separate calls (vsd_sample_paths,
 vsd_score_paths, vsd_weighted_loss_bwd) is timed too and reported beside it,
 and the step once more, both ways, with the top-K renormalised KL term on
 (K = 10, "kl_variant"), and with exact context ("exact_context": each family
-on its own rows, drawn depth by depth).
+on its own rows, drawn depth by depth); "verification" times the decode-time
+verification of the step's draft paths (vsd_verify_paths) and reports its
+mean accepted length beside the mean expected accepted length.
 W untimed steps, then exactly K steps timed between stream synchronisations;
 per-call durations come from HIP events recorded on the stream the kernels
 run on.
@@ -429,6 +431,7 @@ def main():
         "kernels": kernels, "three_calls": three_calls, "kl_variant": kl_variant, "roofline": roof,
         "cpu_baseline": base,
     }
+    line["verification"] = bench_verify(cfg, prob, params, inp, out, ws, timed, dev)
     if not args.no_ctx:
         line["exact_context"] = bench_ctx(cfg, prob, params, inp, ws, timed, live, dev)
     if not args.no_lm_head:
@@ -436,6 +439,38 @@ def main():
         torch.cuda.empty_cache()
         line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
     print(json.dumps(line), flush=True)
+
+
+def bench_verify(cfg, prob, params, inp, out, ws, timed, dev):
+    """Decode-time verification of the step's draft paths (vsd_verify_paths
+    on the scores `out` holds).  Bytes: each rejected path's row is read once
+    (target logits es V_t, draft logits es V_d through the inverse map)."""
+    import torch
+
+    import paper_2602_05774_amd as vsd
+    X, Y, d2t, depth = inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    res = {}
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        res["v"] = vsd.verify_paths(prob, params, X, Y, out, d2t, depth, cfg.philox_seed, cfg.philox_offset,
+                                    workspace=ws, device_error=err)
+        if ev:
+            ev[1].record()
+
+    (t_verify,), _, _ = timed(step, 2)
+    if int(err.item()) != 0:
+        raise RuntimeError("device error reported during the verification benchmark")
+    acc = res["v"].accept_len
+    d = torch.full_like(acc, cfg.L) if depth is None else depth.reshape(-1)
+    rejected = int((acc < d).sum().item())
+    es = X.element_size()
+    nbytes = rejected * es * (cfg.v_draft + cfg.v_target)
+    return {"ms": t_verify, "paths": acc.numel(), "rejected_paths": rejected, "bytes": nbytes,
+            "GB/s": nbytes / (t_verify * 1e-3) / 1e9, "mean_accept_len": float(acc.double().mean().item()),
+            "mean_expected_accept_len": float(out.exp_accept_len.double().mean().item())}
 
 
 def bench_ctx(cfg, prob, params, inp, ws, timed, live, dev):
