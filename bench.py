@@ -206,7 +206,8 @@ def bench_lm_head(cfg, steps, warmup, dev):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
-KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_device.hpp"], "bwd": ["k_bwd.hip", "vsd_device.hpp"]}
+KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_draw.hpp", "vsd_topk.hpp", "vsd_device.hpp"],
+                  "bwd": ["k_bwd.hip", "vsd_topk.hpp", "vsd_device.hpp"]}
 
 
 def source_hash(kernel):

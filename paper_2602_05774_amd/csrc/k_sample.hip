@@ -69,7 +69,7 @@ struct LaneLse {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
 
   __device__ __forceinline__ void add8(const float (&v)[8], float c) {
-    const float cm = fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])), fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7])));
+    const float cm = max8(v);
     if (cm > mraw) {
       const float nmc = cm * c;
       s *= __builtin_amdgcn_exp2f(mc - nmc);
@@ -161,6 +161,9 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
   auto same = [](int col) { return col; };
   const int nfull = Vd / kChunk;
   auto greedy = [&](int base, const float (&y)[8], int nvalid) {
+    // a full chunk that no lane's maximum lifts above its running maximum
+    // changes nothing (the common case once a few chunks are seen)
+    if (nvalid == 8 && __ballot(max8(y) > bg.key) == 0ull) return;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const bool better = k < nvalid && y[k] > bg.key;
@@ -171,20 +174,16 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
   if (nfull > 0) {
     uint32_t t[8];
     T g[8];
-    uint32_t bad = 0;
     Raw8<T> yr;
     auto load_map = [&](int chunk, uint32_t (&tt)[8]) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) tt[k] = (uint32_t)d2t[chunk + k * kWave + lane];
     };
-    auto gather = [&](const uint32_t (&tt)[8]) {  // out-of-range entries read element 0, flagged
-      bad = 0;
+    // map entries are range-checked before the launch (k_map_check reports
+    // an out-of-range entry); the clamp only keeps every access in bounds
+    auto gather = [&](const uint32_t (&tt)[8]) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const bool ok = tt[k] < (uint32_t)Vt;
-        bad |= ok ? 0u : (1u << k);
-        g[k] = Y[ok ? tt[k] : 0u];
-      }
+      for (int k = 0; k < 8; ++k) g[k] = Y[min(tt[k], (uint32_t)Vt - 1u)];
     };
     if (MAPPED) {
       load_map(0, t);
@@ -212,9 +211,8 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       if (MAPPED) {
         // transpose the gathered values through the LDS tile; LDS operations
         // of one wavefront execute in order, so no barrier is needed
-        map_bad |= bad != 0u;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) tile[k * kWave + lane] = (bad & (1u << k)) ? neg_inf<T>() : g[k];
+        for (int k = 0; k < 8; ++k) tile[k * kWave + lane] = g[k];
         load8(tile + lane * 8, y);
       } else {
         yr.unpack(y);
@@ -450,8 +448,24 @@ __global__ __launch_bounds__(192) void k_sample_step(SampleStepArgs a) {
   if (lane == 0) out[r] = wave == 1 ? f.best.idx : bg.idx;
 }
 
+// Range check of the map (the sampling kernels clamp map entries instead of
+// testing each one): the first entry outside [0, Vt) is reported.
+__global__ __launch_bounds__(256) void k_map_check(const int32_t* d2t, int Vd, int Vt, int32_t* err) {
+  const int v = blockIdx.x * 256 + threadIdx.x;
+  if (v < Vd && (uint32_t)d2t[v] >= (uint32_t)Vt) report_error(err, VSD_DEVERR_MAP_RANGE);
+}
+
+hipError_t launch_map_check(const int32_t* d2t, int Vd, int Vt, int32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_map_check, dim3((unsigned)((Vd + 255) / 256)), dim3(256), 0, s, d2t, Vd, Vt, err);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_step_t(const SampleStepArgs& a, hipStream_t s) {
+  if (a.d2t != nullptr) {
+    const hipError_t e = launch_map_check(a.d2t, a.Vd, a.Vt, a.err, s);
+    if (e != hipSuccess) return e;
+  }
   const dim3 grid((unsigned)a.paths);
   if (a.d2t != nullptr)
     hipLaunchKernelGGL((k_sample_step<T, true>), grid, dim3(3 * kWave), 0, s, a);
@@ -462,6 +476,10 @@ hipError_t launch_step_t(const SampleStepArgs& a, hipStream_t s) {
 
 template <typename T, bool FUSED, bool KL>
 hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
+  if (a.d2t != nullptr) {
+    const hipError_t e = launch_map_check(a.d2t, a.Vd, a.Vt, a.err, s);
+    if (e != hipSuccess) return e;
+  }
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
   if (a.d2t != nullptr)
     hipLaunchKernelGGL((k_sample<T, true, FUSED, KL>), grid, dim3(256), 0, s, a);

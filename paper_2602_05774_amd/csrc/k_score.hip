@@ -57,8 +57,7 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
     for (int u = 0; u < U; ++u) load8(row + base + u * step, x[u]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float cm = fmaxf(fmaxf(fmaxf(x[u][0], x[u][1]), fmaxf(x[u][2], x[u][3])),
-                             fmaxf(fmaxf(x[u][4], x[u][5]), fmaxf(x[u][6], x[u][7])));
+      const float cm = max8(x[u]);
       if (cm > mraw) {
         const float nmc = cm * c;
         s *= __builtin_amdgcn_exp2f(mc - nmc);
@@ -72,9 +71,7 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
   for (; base + 8 <= V; base += step) {
     float x[8];
     load8(row + base, x);
-    float cm = x[0];
-#pragma unroll
-    for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
+    const float cm = max8(x);
     if (cm > mraw) {
       const float nmc = cm * c;
       s *= __builtin_amdgcn_exp2f(mc - nmc);
@@ -120,9 +117,7 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     return MAPPED ? ((mask[base >> 5] >> (base & 31)) & keep) : keep;
   };
   auto fold = [&](int base, const float (&x)[8], uint32_t bits) {
-    float cm = x[0];
-#pragma unroll
-    for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
+    const float cm = max8(x);
     if (cm > mraw) {
       const float nmc = cm * c;
       s *= __builtin_amdgcn_exp2f(mc - nmc);

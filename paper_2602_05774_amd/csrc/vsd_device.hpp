@@ -152,6 +152,19 @@ __device__ __forceinline__ void store1(bf16_t* p, float v) {
   *p = __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
+// ------------------------------------------------------------ lane math ---
+// max(a, b, c) in one instruction (v_max3_f32).
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Largest of 8 values in four instructions.
+__device__ __forceinline__ float max8(const float (&v)[8]) {
+  return fmaxf(max3f(v[3], v[4], v[5]), max3f(v[6], v[7], max3f(v[0], v[1], v[2])));
+}
+
 // ------------------------------------------------------ wave reductions ---
 // (key, index) maximum; equal keys resolve to the smaller index.
 __device__ __forceinline__ void wave_argmax(float& key, int& idx) {
