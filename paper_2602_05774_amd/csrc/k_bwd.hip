@@ -57,7 +57,7 @@ struct KlRow {
 template <typename T, bool KL>
 __global__ __launch_bounds__(256) void k_bwd(BwdArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + wave_id();
   if (r >= a.R) return;
   T* G = static_cast<T*>(a.G) + r * a.ld;
   const float ca = a.coef_a != nullptr ? a.coef_a[r] : 0.0f;

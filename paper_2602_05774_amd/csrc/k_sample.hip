@@ -274,7 +274,7 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
   __shared__ float kl_bv[KL ? kRowsPerBlock * kTopKCap : 1];
   __shared__ int kl_bi[KL ? kRowsPerBlock * kTopKCap : 1];
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x >> 6;
+  const int wave = wave_id();
   const int slot = wave >> 1;       // row within the block
   const bool draft_role = (wave & 1) == 0;
   const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + slot;
@@ -405,7 +405,7 @@ template <typename T, bool MAPPED>
 __global__ __launch_bounds__(192) void k_sample_step(SampleStepArgs a) {
   __shared__ __align__(16) T ytile[2][kChunk];
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x >> 6;  // 0: z~, 1: z', 2: z-bar
+  const int wave = wave_id();  // 0: z~, 1: z', 2: z-bar
   const int64_t path = blockIdx.x;     // the grid has exactly one workgroup per path
   int d = a.L;
   if (a.depth != nullptr) {

@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   __shared__ float kl_bv[KL ? kRowsPerBlock * kTopKCap : 1];
   __shared__ int kl_bi[KL ? kRowsPerBlock * kTopKCap : 1];
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + wave_id();
   if (r >= a.R) return;
   const int i = (int)(r % a.L);
   const int64_t path = r / a.L;
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   WaveTopK tk;
   RowLse p;
   if (KL) {
-    const int slot = threadIdx.x >> 6;
+    const int slot = wave_id();
     tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
     p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.map_mask, a.inv);
   } else {

@@ -29,7 +29,7 @@ constexpr int kPathsPerBlock = 4;
 template <typename T, bool MAPPED>
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t path = (int64_t)blockIdx.x * kPathsPerBlock + (threadIdx.x >> 6);
+  const int64_t path = (int64_t)blockIdx.x * kPathsPerBlock + wave_id();
   if (path >= a.paths) return;
   int d = a.L;
   if (a.depth != nullptr) {

@@ -152,6 +152,11 @@ __device__ __forceinline__ void store1(bf16_t* p, float v) {
   *p = __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
+// Index of the calling wavefront within its workgroup, as a wavefront-uniform
+// (scalar) value: everything derived from it (row indices, row pointers,
+// Philox counter words) then lives in scalar registers.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 // ------------------------------------------------------------ lane math ---
 // max(a, b, c) in one instruction (v_max3_f32).
 __device__ __forceinline__ float max3f(float a, float b, float c) {
