@@ -124,12 +124,13 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
       if (it + 1 < nfull) xn.load(X + base + kChunk);
       float x[8];
       xr.unpack(x);
-      if (FUSED) lq.add8(x, f.c2);
-      f.draw(base, x, 8);
-      if (FUSED && MAPPED) {
+      if (FUSED && MAPPED) {  // before the draws: the target wavefront's gathers of this
+        // block's mapped elements then find its lines in L2 more often
         const int lo = it * 2 * kStream;
         stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
       }
+      if (FUSED) lq.add8(x, f.c2);
+      f.draw(base, x, 8);
       xr = xn;
     }
   }
