@@ -213,6 +213,12 @@ EDGES = {
     "same_models": dict(B=1, T=2, N=5, L=4, Vd=3000, Vt=3000, dtype=torch.bfloat16, seed=6, same=True, ragged=True),
     "const_logits": dict(B=1, T=2, N=4, L=2, Vd=600, Vt=600, dtype=torch.bfloat16, seed=7, const=True),
     "N70_wide_block": dict(B=1, T=1, N=70, L=2, Vd=300, Vt=300, dtype=torch.float32, seed=8, ragged=True),
+    # the largest path count and depth the ABI accepts, and one-token vocabularies
+    "N1024_max_paths": dict(B=1, T=1, N=1024, L=2, Vd=64, Vt=64, dtype=torch.float32, seed=9, ragged=True),
+    "L64_max_depth": dict(B=1, T=1, N=3, L=64, Vd=300, Vt=700, dtype=torch.bfloat16, seed=10, mapped=True,
+                          ragged=True),
+    "V1": dict(B=1, T=2, N=3, L=2, Vd=1, Vt=1, dtype=torch.float32, seed=11),
+    "V1_map": dict(B=1, T=2, N=2, L=3, Vd=1, Vt=17, dtype=torch.bfloat16, seed=12, mapped=True),
 }
 
 
@@ -304,7 +310,8 @@ def test_fused_sample_score_every_position(name):
         assert torch.equal(a, b), "fused and three-call tokens differ"
 
 
-@pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models"])
+@pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models", "N1024_max_paths",
+                                  "L64_max_depth", "V1_map"])
 def test_fused_edge_cases(name):
     spec = dict(EDGES[name])
     log(f"[fused-edge] {name}")

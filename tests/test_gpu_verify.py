@@ -98,7 +98,8 @@ def test_ragged_peaked():
     assert np.all(ver.accept_len.cpu().numpy() <= depth)
 
 
-@pytest.mark.parametrize("name", ["V1003_f32", "V1003_bf16_map", "V2_map", "N1_L1", "same_models"])
+@pytest.mark.parametrize("name", ["V1003_f32", "V1003_bf16_map", "V2_map", "N1_L1", "same_models", "N1024_max_paths",
+                                  "L64_max_depth", "V1_map"])
 def test_edge_cases(name):
     cfg, inp = _custom(**EDGES[name])
     ver, gpu = check_verify(cfg, inp, list(range(cfg.P)), params_of(cfg), f"edge {name} verify")
