@@ -43,13 +43,15 @@ constexpr int kThreads = 512;                // eight wavefronts
 constexpr int LDK = TK + 8;                  // K-contiguous LDS row (bf16): 144 B, conflict-free 16-B reads
 constexpr int LDN = TN + 32;                 // N-contiguous LDS row (bf16) of a K-major operand: 576 B
 constexpr int LDT = TN + 4;                  // fp32 epilogue row
-constexpr int kStageElems = 2 * TM * LDK;    // A and B of one stage (bf16)
+constexpr int kStageElems = 2 * TM * LDK;    // A and B of one stage (bf16), padded rows
+constexpr int kStageNT = 2 * TM * TK;        // A and B of one stage, direct-loaded NT operands
 constexpr int kLdsBytes = 2 * kStageElems * 2;
 constexpr int kXcds = 8;                     // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr int kGroupRows = 4;                // row tiles per L2 reuse group
 static_assert(TM * LDK == TK * LDN, "both B layouts fill the same stage slot");
 static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit the operand buffers");
 static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
+static_assert(2 * kStageNT * 2 <= kLdsBytes, "two direct-loaded NT stages fit");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -72,6 +74,9 @@ __device__ __forceinline__ void tile_of(int pid, int nrt, int ncol, int& rt, int
   rt = first + in % rows;
   col = in / rows;
 }
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_void;
 
 // ------------------------------------------------------------- GEMM core ---
 // acc = A[row0 .. +TM, 0 .. K) * B, accumulated over K in order.  A is bf16
@@ -136,9 +141,40 @@ struct Core {
     }
   }
 
+  // NT: both operands K-contiguous.  A stage goes from global memory to LDS
+  // directly (global_load_lds_dwordx4: lane i's 16 bytes land at the
+  // instruction's LDS base + 16 i), 8 rows of 64 K values per instruction;
+  // rows are unpadded (128 B) and lane i of a row loads global 16-byte chunk
+  // (i ^ row) & 7, so chunk c of row r sits at position c ^ (r & 7): the
+  // fragment reads of 8 consecutive rows then cover all banks.  Rows past
+  // nrow / ncol read the last valid row (their results are never used); K is
+  // a multiple of TK.
+  __device__ __forceinline__ void issue(int k0, bf16_t* L) const {
+    const int lane = threadIdx.x & 63, w = wave_id();
+    const int lr = lane >> 3, lc = lane & 7;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = w * 32 + j * 8 + lr;
+      const int cg = (lc ^ r) & 7;
+      const int64_t ar = min(row0 + r, nrow - 1);
+      const int br = min(col0 + r, ncol - 1);
+      __builtin_amdgcn_global_load_lds((const global_void*)(A + ar * lda + k0 + cg * 8),
+                                       (lds_void*)(L + (w * 32 + j * 8) * TK), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const global_void*)(B + (int64_t)br * ldb + k0 + cg * 8),
+                                       (lds_void*)(L + TM * TK + (w * 32 + j * 8) * TK), 16, 0, 0);
+    }
+  }
+
+  // Fragment of rows r0 .. r0+31 (one per lane & 31) at K offset ks*16 of a
+  // direct-loaded NT operand block.
+  __device__ __forceinline__ static bf16x8 frag_nt(const bf16_t* L, int r0, int ks, int lane) {
+    const int r = r0 + (lane & 31), c = ks * 2 + (lane >> 5);
+    return *reinterpret_cast<const bf16x8*>(L + r * TK + (((c ^ r) & 7) << 3));
+  }
+
   // The B fragment of tile column n0 (32 wide) at K offset ks*16.
   __device__ __forceinline__ static bf16x8 frag_b(const bf16_t* L, int n0, int ks, int lane) {
-    if (!NN) return *reinterpret_cast<const bf16x8*>(L + TM * LDK + (n0 + (lane & 31)) * LDK + ks * 16 + (lane >> 5) * 8);
+    if (!NN) return frag_nt(L + TM * TK, n0, ks, lane);
     // Transpose load: in each 16-lane group, source lane s names row
     // k = base + s/4 and columns 4(s%4) .. +3; lane i of the group then holds
     // rows base .. base+3 of column i.  Group g covers rows (g >> 1)*8 and
@@ -161,7 +197,9 @@ struct Core {
       bf16x8 a[4], b[2];
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti)
-        a[ti] = *reinterpret_cast<const bf16x8*>(L + (wr * 128 + ti * 32 + (lane & 31)) * LDK + ks * 16 + (lane >> 5) * 8);
+        a[ti] = NN ? *reinterpret_cast<const bf16x8*>(L + (wr * 128 + ti * 32 + (lane & 31)) * LDK + ks * 16 +
+                                                      (lane >> 5) * 8)
+                   : frag_nt(L, wr * 128 + ti * 32, ks, lane);
 #pragma unroll
       for (int tj = 0; tj < 2; ++tj) b[tj] = frag_b(L, wc * 64 + tj * 32, ks, lane);
 #pragma unroll
@@ -175,6 +213,17 @@ struct Core {
   __device__ void run(bf16_t* lds, f32x16 (&acc)[8]) const {
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = f32x16{};
+    if (!NN) {  // direct loads: the next stage streams into the other buffer during this one
+      const int nst = K / TK;
+      issue(0, lds);
+      __syncthreads();
+      for (int st = 0; st < nst; ++st) {
+        if (st + 1 < nst) issue((st + 1) * TK, lds + ((st + 1) & 1) * kStageNT);
+        compute(lds + (st & 1) * kStageNT, acc);
+        __syncthreads();  // waits for the direct loads too
+      }
+      return;
+    }
     uint4 ra[4], rb[4];
     const int nst = (K + TK - 1) / TK;
     load(0, ra, rb);
