@@ -11,11 +11,14 @@ to the unchanged per-position oracle.
 
 The gradient of the loss with respect to the hidden states follows by the
 chain rule through logits = h W^T: dLoss/dh_r = sum_v g_r[v] W[v, :], with g
-the gradient with respect to the logits (derivative of Eq. advance).
+the gradient with respect to the logits (derivative of Eq. advance); the
+gradient with respect to the draft head's weight is dLoss/dW[v, :] =
+sum_r g_r[v] h_r.
 
 Pinned by tests/test_oracle_lmhead.py: unit-vector weights reduce the product
 to selecting hidden entries; central finite differences of the whole loss as a
-function of the hidden states check the chain rule and the operand order.
+function of the hidden states and of the draft weight check the chain rule and
+the operand order.
 """
 import numpy as np
 
@@ -34,16 +37,23 @@ def grad_hidden(grad_logits, weight):
     return np.asarray(grad_logits, dtype=np.float64) @ np.asarray(weight, dtype=np.float64)
 
 
+def grad_weight(grad_logits, hidden):
+    """dLoss/dW [V, H] from dLoss/dlogits [n, V] and hidden [n, H]."""
+    return np.asarray(grad_logits, dtype=np.float64).T @ np.asarray(hidden, dtype=np.float64)
+
+
 def run_positions(Hd, Ht, Wd, Wt, d2t, depth, positions, N, L, params, seed=0, offset=0,
                   tokens=None, want_grad=True):
     """reference.run_positions on the logits of the given hidden rows
     ([len(positions)*N*L, H] each, in row order), plus "grad_hidden" when
-    want_grad.  The logits themselves are returned as "X" and "Y"."""
+    want_grad (and "grad_weight", the draft weight's gradient over these
+    rows).  The logits themselves are returned as "X" and "Y"."""
     X = logits(Hd, Wd)
     Y = logits(Ht, Wt)
     res = reference.run_positions(X, Y, d2t, depth, positions, N, L, params, seed, offset, tokens, want_grad)
     if want_grad:
         res["grad_hidden"] = grad_hidden(res["grad"], Wd)
+        res["grad_weight"] = grad_weight(res["grad"], Hd)
     res["X"] = X
     res["Y"] = Y
     return res

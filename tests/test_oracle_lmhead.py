@@ -67,6 +67,37 @@ def test_hidden_gradient_matches_central_finite_differences(mode):
     assert np.abs(fd).max() > 1e-3  # the case is not degenerate
 
 
+@pytest.mark.parametrize("mode", [paths.MODE_BASIC, paths.MODE_ARW_CAR])
+def test_weight_gradient_matches_central_finite_differences(mode):
+    rng = np.random.default_rng(5)
+    N, L, H, V = 3, 2, 4, 6
+    hd = rng.normal(size=(N * L, H))
+    ht = rng.normal(size=(N * L, H))
+    Wd = rng.normal(size=(V, H))
+    Wt = rng.normal(size=(V, H))
+    depth = np.array([L, 2, 1])
+    toks = [rng.integers(0, V, N * L) for _ in range(3)]
+    params = dict(mode=mode, temp_draft=0.8, loss_scale=0.7)
+    res = lmhead.run_positions(hd, ht, Wd, Wt, None, depth[None, :], [0], N, L, params, tokens=toks)
+    Y = res["Y"].reshape(N, L, V)
+    t3 = [t.reshape(N, L) for t in toks]
+    frozen = paths.score_position(res["X"].reshape(N, L, V), Y, None, depth, *t3, params)
+
+    def loss_of(W):
+        Xw = lmhead.logits(hd, W).reshape(N, L, V)
+        return params["loss_scale"] * paths.loss_from_logits(Xw, Y, None, depth, *t3, frozen, params)
+
+    eps = 1e-6
+    fd = np.zeros_like(Wd)
+    for idx in np.ndindex(Wd.shape):
+        wp, wm = Wd.copy(), Wd.copy()
+        wp[idx] += eps
+        wm[idx] -= eps
+        fd[idx] = (loss_of(wp) - loss_of(wm)) / (2 * eps)
+    np.testing.assert_allclose(res["grad_weight"], fd, atol=1e-8, rtol=1e-6)
+    assert np.abs(fd).max() > 1e-3
+
+
 def test_driver_equals_materialised_driver_and_gumbel_max():
     rng = np.random.default_rng(3)
     N, L, H, Vd, Vt = 2, 3, 8, 10, 16
