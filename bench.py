@@ -179,6 +179,19 @@ def bench_lm_head(cfg, steps, warmup, dev):
     wall = time.perf_counter() - t0
     t_fwd = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
     t_bwd = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+    # the backward once more with the draft weight's gradient (g^T H_d, fp32)
+    gw = vsd.LmHeadGrad(grad.grad_hidden, grad.grad_logits,
+                        torch.empty(cfg.v_draft, cfg.hidden, dtype=torch.float32, device=dev))
+    ew = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    vsd.weighted_loss_bwd(prob, params, Xs, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=gw,
+                          device_error=err)
+    ew[0].record()
+    vsd.weighted_loss_bwd(prob, params, Xs, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=gw,
+                          device_error=err)
+    ew[1].record()
+    torch.cuda.synchronize()
+    t_bwd_w = ew[0].elapsed_time(ew[1])
+    del gw
     if int(err.item()) != 0 or int(out.device_error.item()) != 0:
         raise RuntimeError("device error reported during the LM-head benchmark")
     live = prob.R if inp["valid_depth"] is None else int((tok[0] >= 0).sum().item())
@@ -194,7 +207,9 @@ def bench_lm_head(cfg, steps, warmup, dev):
         "path_tokens_per_step": live, "ms_per_step": t_fwd + t_bwd, "wall_ms_per_step": wall * 1e3 / steps,
         "value": live / ((t_fwd + t_bwd) * 1e-3), "unit": "path-tokens/s",
         "kernels": {"sample_score": {"ms": t_fwd, "flop": fwd_flop, "TFLOP/s": tf(fwd_flop, t_fwd)},
-                    "bwd": {"ms": t_bwd, "flop": bwd_flop, "TFLOP/s": tf(bwd_flop, t_bwd)}},
+                    "bwd": {"ms": t_bwd, "flop": bwd_flop, "TFLOP/s": tf(bwd_flop, t_bwd)},
+                    "bwd_with_weight_grad": {"ms": t_bwd_w, "flop": bwd_flop * 1.5,
+                                             "TFLOP/s": tf(bwd_flop * 1.5, t_bwd_w)}},
         "step_TFLOP/s": tf(fwd_flop + bwd_flop, t_fwd + t_bwd),
         "roofline": {"bound": "mfma", "kernel": "k_lm_fwd (forward call: GEMM tiles + sampling epilogue)",
                      "achieved": tf(fwd_flop, t_fwd), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -143,7 +143,9 @@
  *   Backward: grad->grad_logits (bf16, row stride dims->ld_draft, a multiple
  *   of 8 >= v_draft) receives g as defined at vsd_weighted_loss_bwd, and
  *   grad->grad_hidden [R, H] (bf16) receives g . weight_d.
- *   grad->grad_weight must be NULL (the weight gradient is not computed).
+ *   grad->grad_weight [V_d, H] fp32, optional (NULL: not computed), receives
+ *   the gradient with respect to the draft head's weight, g^T . hidden_d
+ *   (fp32 accumulation of the bf16 g; written, not accumulated into).
  *   dims->ld_target is unused.
  *
  * VSD (KL): the top-K renormalised KL term (params->kl_weight > 0)
@@ -298,7 +300,7 @@ typedef struct vsd_ctx_rows {
 typedef struct vsd_grad {
   void* grad_logits;      /* [R, ld_draft]: dtype of X; fused: bf16 */
   void* grad_hidden;      /* fused: [R, H] bf16, required */
-  float* grad_weight;     /* fused: must be NULL (not computed) */
+  float* grad_weight;     /* fused, optional: [V_d, H] fp32, g^T . hidden_d */
 } vsd_grad;
 
 /* E-step sampling (Alg. 1: z~ ~ q and z' ~ p; Alg. 2: z-bar greedy).

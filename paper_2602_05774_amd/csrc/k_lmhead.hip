@@ -25,7 +25,7 @@
 // Backward (derivative of Eq. advance through the LM head).  The draft
 // logits are recomputed tile by tile; g = loss_scale/T_q ((a+b) q - a e_z~ -
 // b e_z') is written in bf16 (the gradient with respect to the logits); then
-// dH_d = g W_d.
+// dH_d = g W_d and, when asked for, dW_d = g^T H_d (fp32).
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
 
@@ -48,7 +48,7 @@ constexpr int kStageNT = 2 * TM * TK;        // A and B of one stage, direct-loa
 constexpr int kLdsBytes = 2 * kStageElems * 2;
 constexpr int kXcds = 8;                     // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr int kGroupRows = 4;                // row tiles per L2 reuse group
-static_assert(TM * LDK == TK * LDN, "both B layouts fill the same stage slot");
+static_assert(TM * LDK == TK * LDN, "both operand layouts fill the same stage slot");
 static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit the operand buffers");
 static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
 static_assert(2 * kStageNT * 2 <= kLdsBytes, "two direct-loaded NT stages fit");
@@ -80,14 +80,16 @@ typedef __attribute__((address_space(1))) const void global_void;
 
 // ------------------------------------------------------------- GEMM core ---
 // acc = A[row0 .. +TM, 0 .. K) * B, accumulated over K in order.  A is bf16
-// [*, K] row-major (stride lda).  NN = false: B is [N, K] row-major (stride
-// ldb) and the tile takes rows col0 .. +TN of it; NN = true: B is [K, N]
-// row-major and the tile takes columns col0 .. +TN.  Rows >= nrow, columns
+// [*, K] row-major (stride lda), or with TA = true [K, *] row-major (the
+// tile takes its columns row0 .. +TM).  NN = false: B is [N, K] row-major
+// (stride ldb) and the tile takes rows col0 .. +TN of it; NN = true: B is
+// [K, N] row-major and the tile takes columns col0 .. +TN.  K-major operands
+// are staged N-contiguous and read with transpose loads.  Rows >= nrow, columns
 // >= ncol and K >= K read as zero; NN needs ncol % 8 == 0, NT needs K % 8 ==
 // 0 (A's K tail is read element-wise when K % TK != 0).
 // Wavefront w = (wr, wc) = (w >> 2, w & 3) accumulates acc[ti*2 + tj] =
 // rows wr*128 + ti*32 .. +31, columns wc*64 + tj*32 .. +31.
-template <bool NN>
+template <bool NN, bool TA = false>
 struct Core {
   const bf16_t* A;
   const bf16_t* B;
@@ -105,13 +107,30 @@ struct Core {
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
 
+  // 8 consecutive columns m .. m+7 of K row k of a K-major A (zeros past
+  // the matrix).
+  __device__ __forceinline__ uint4 load_ta(int k, int64_t m) const {
+    if (k >= K || m >= nrow) return make_uint4(0, 0, 0, 0);
+    const bf16_t* p = A + (int64_t)k * lda + m;
+    if (m + 8 <= nrow) return *reinterpret_cast<const uint4*>(p);
+    uint32_t w[4] = {0, 0, 0, 0};
+    for (int e = 0; e < 8; ++e)
+      if (m + e < nrow) w[e >> 1] |= (uint32_t)p[e] << (16 * (e & 1));
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+
   __device__ __forceinline__ void load(int k0, uint4 (&ra)[4], uint4 (&rb)[4]) const {
     const int t = threadIdx.x;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = t + kThreads * j;  // 16-byte chunk of the 256 x 64 tile
       const int r = c >> 3, kc = (c & 7) * 8;
-      ra[j] = load_a(row0 + r, k0 + kc);
+      if (TA) {
+        const int kr = c >> 5, mc = (c & 31) * 8;  // 64 K rows x 256 columns
+        ra[j] = load_ta(k0 + kr, row0 + mc);
+      } else {
+        ra[j] = load_a(row0 + r, k0 + kc);
+      }
       if (!NN) {
         rb[j] = (col0 + r < ncol && k0 + kc < K)
                     ? *reinterpret_cast<const uint4*>(B + (int64_t)(col0 + r) * ldb + k0 + kc)
@@ -131,7 +150,10 @@ struct Core {
     for (int j = 0; j < 4; ++j) {
       const int c = t + kThreads * j;
       const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(L + r * LDK + kc) = ra[j];
+      if (TA)
+        *reinterpret_cast<uint4*>(L + (c >> 5) * LDN + (c & 31) * 8) = ra[j];
+      else
+        *reinterpret_cast<uint4*>(L + r * LDK + kc) = ra[j];
       if (!NN) {
         *reinterpret_cast<uint4*>(L + TM * LDK + r * LDK + kc) = rb[j];
       } else {
@@ -175,12 +197,20 @@ struct Core {
   // The B fragment of tile column n0 (32 wide) at K offset ks*16.
   __device__ __forceinline__ static bf16x8 frag_b(const bf16_t* L, int n0, int ks, int lane) {
     if (!NN) return frag_nt(L + TM * TK, n0, ks, lane);
+    return frag_tr(L + TM * LDK, n0, ks, lane);
+  }
+
+  // Fragment of columns n0 .. n0+31 at K offset ks*16 of an N-contiguous
+  // (K-major) operand block: lane l gets rows (l / 32) * 8 .. +7 of column
+  // n0 + l % 32, which is the layout of the MFMA's B operand and, read as
+  // rows of A^T, of its A operand.
+  __device__ __forceinline__ static bf16x8 frag_tr(const bf16_t* Lk, int n0, int ks, int lane) {
     // Transpose load: in each 16-lane group, source lane s names row
     // k = base + s/4 and columns 4(s%4) .. +3; lane i of the group then holds
     // rows base .. base+3 of column i.  Group g covers rows (g >> 1)*8 and
     // columns (g & 1)*16 of the 16 x 32 fragment; two loads give 8 rows.
     const int g = lane >> 4, s = lane & 15;
-    const bf16_t* p = L + TM * LDK + (ks * 16 + (g >> 1) * 8 + (s >> 2)) * LDN + n0 + (g & 1) * 16 + 4 * (s & 3);
+    const bf16_t* p = Lk + (ks * 16 + (g >> 1) * 8 + (s >> 2)) * LDN + n0 + (g & 1) * 16 + 4 * (s & 3);
     typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
     // (whole-vector casts: the two loads feed the MFMA registers directly)
     const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
@@ -197,9 +227,10 @@ struct Core {
       bf16x8 a[4], b[2];
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti)
-        a[ti] = NN ? *reinterpret_cast<const bf16x8*>(L + (wr * 128 + ti * 32 + (lane & 31)) * LDK + ks * 16 +
+        a[ti] = TA ? frag_tr(L, wr * 128 + ti * 32, ks, lane)
+             : NN ? *reinterpret_cast<const bf16x8*>(L + (wr * 128 + ti * 32 + (lane & 31)) * LDK + ks * 16 +
                                                       (lane >> 5) * 8)
-                   : frag_nt(L, wr * 128 + ti * 32, ks, lane);
+                  : frag_nt(L, wr * 128 + ti * 32, ks, lane);
 #pragma unroll
       for (int tj = 0; tj < 2; ++tj) b[tj] = frag_b(L, wc * 64 + tj * 32, ks, lane);
 #pragma unroll
@@ -695,6 +726,33 @@ __global__ __launch_bounds__(kThreads, 1) void k_lm_gemm_nn(LmGemmNNArgs a) {
       }
 }
 
+// dW = A^T B (fp32): A = g [R, ldg] (K = R rows, M = V_d columns), B = H_d
+// [R, H]; both K-major, staged N-contiguous and read with transpose loads.
+__global__ __launch_bounds__(kThreads, 1) void k_lm_gemm_tn(LmGemmTNArgs a) {
+  __shared__ __align__(16) bf16_t lds[2 * kStageElems];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wr = w >> 2, wc = w & 3;
+  const int nrt = (int)((a.M + TM - 1) / TM);
+  int rt, ct;
+  tile_of(blockIdx.x, nrt, (a.N + TN - 1) / TN, rt, ct);
+  const int64_t row0 = (int64_t)rt * TM;
+  const int n0 = ct * TN;
+  Core<true, true> g{static_cast<const bf16_t*>(a.A), static_cast<const bf16_t*>(a.B), a.lda, a.ldb, row0, a.M, n0,
+                     a.N, a.K};
+  f32x16 acc[8];
+  g.run(lds, acc);
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int64_t row = row0 + wr * 128 + ti * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+        const int col = n0 + wc * 64 + tj * 32 + (lane & 31);
+        if (row < a.M && col < a.N) a.C[row * a.ldc + col] = acc[ti * 2 + tj][i];
+      }
+}
+
 }  // namespace
 
 hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32_t* err, hipStream_t s) {
@@ -721,6 +779,11 @@ hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   LmGemmNNArgs gm{a.G, a.Wd, a.dH, a.R, a.ldg, a.H, a.H, a.H, a.Vd};
   hipLaunchKernelGGL(k_lm_gemm_nn, dim3((unsigned)(nrt * ((a.H + TN - 1) / TN))), dim3(kThreads), 0, s, gm);
+  e = hipGetLastError();
+  if (e != hipSuccess || a.dW == nullptr) return e;
+  LmGemmTNArgs tn{a.G, a.Hd, a.dW, a.Vd, a.ldg, a.H, a.H, a.H, (int32_t)a.R};
+  const int64_t nvt = (a.Vd + TM - 1) / TM;
+  hipLaunchKernelGGL(k_lm_gemm_tn, dim3((unsigned)(nvt * ((a.H + TN - 1) / TN))), dim3(kThreads), 0, s, tn);
   return hipGetLastError();
 }
 

@@ -611,13 +611,14 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
                   (long long)dims->ld_draft);
     if (grad->grad_hidden == nullptr) return fail(VSD_ERR_NULL_POINTER, "fused: grad->grad_hidden is NULL");
     if (!aligned16(grad->grad_hidden)) return fail(VSD_ERR_MISALIGNED, "grad_hidden not 16-byte aligned");
-    if (grad->grad_weight != nullptr)
-      return fail(VSD_ERR_UNSUPPORTED, "fused: the weight gradient is not computed (pass grad_weight = NULL)");
+    if (grad->grad_weight != nullptr && !aligned16(grad->grad_weight))
+      return fail(VSD_ERR_MISALIGNED, "grad_weight not 16-byte aligned");
     vsd::LmBwdArgs b{};
     b.Hd = draft->hidden;
     b.Wd = draft->weight;
     b.G = grad->grad_logits;
     b.dH = grad->grad_hidden;
+    b.dW = grad->grad_weight;
     b.lse_q = lse_draft;
     b.tok_d = tok_draft;
     b.tok_t = tok_target;

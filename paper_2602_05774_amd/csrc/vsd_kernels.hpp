@@ -199,6 +199,7 @@ struct LmBwdArgs {
   const void* Wd;
   void* G;                   // [R, ldg] bf16: gradient w.r.t. the draft logits
   void* dH;                  // [R, H] bf16
+  float* dW;                 // [Vd, H] fp32 or null: gradient w.r.t. the draft head's weight
   const float* lse_q;
   const int32_t* tok_d;
   const int32_t* tok_t;
@@ -207,6 +208,16 @@ struct LmBwdArgs {
   int64_t R, ldg;
   int32_t H, Vd;
   float inv_tq, scale;
+};
+
+// C = A^T B with A [K, M] and B [K, N] row-major bf16, C [M, N] fp32.
+struct LmGemmTNArgs {
+  const void* A;
+  const void* B;
+  float* C;
+  int64_t M, lda;
+  int64_t ldb, ldc;
+  int32_t N, K;
 };
 
 struct LmGemmNNArgs {

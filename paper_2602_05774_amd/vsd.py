@@ -81,6 +81,7 @@ class LmHead:
 class LmHeadGrad(NamedTuple):
     grad_hidden: torch.Tensor  # [R, H] bf16
     grad_logits: torch.Tensor  # [R, ld] bf16 (columns [0, v_draft) written)
+    grad_weight: Optional[torch.Tensor] = None  # [v_draft, H] fp32: gradient w.r.t. the draft head's weight
 
 
 class SampleResult(NamedTuple):
@@ -313,12 +314,14 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
 
 
 def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,
-                      grad=None, device_error=None, kl_idx=None, kl_grad=None):
+                      grad=None, device_error=None, kl_idx=None, kl_grad=None, weight_grad=False):
     """Gradient of loss_scale * sum_x L_x with respect to the draft logits
     (same shape, stride and dtype as X).  For an LmHead source, returns
-    LmHeadGrad(grad_hidden [R, H], grad_logits [R, ld]): the logit gradient is
-    written in bf16 and then contracted with the weight; `grad`, if given, is
-    such a pair to fill.  kl_idx / kl_grad (from score_paths' output) add the
+    LmHeadGrad(grad_hidden [R, H], grad_logits [R, ld], grad_weight): the
+    logit gradient is written in bf16 and then contracted with the weight
+    (and, with weight_grad=True or a grad_weight given in `grad`, with the
+    hidden states: grad_weight [v_draft, H] fp32); `grad`, if given, holds
+    the buffers to fill.  kl_idx / kl_grad (from score_paths' output) add the
     top-K KL term's gradient when params.kl_weight > 0."""
     lib = _lib.load()
     _check_src("X", X, prob, prob.v_draft)
@@ -330,15 +333,19 @@ def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a,
         H = X.hidden.shape[1]
         if grad is None:
             grad = LmHeadGrad(torch.empty(prob.R, H, dtype=torch.bfloat16, device=dev),
-                              torch.empty(prob.R, _ld8(prob.v_draft), dtype=torch.bfloat16, device=dev))
-        gh, gl = grad
+                              torch.empty(prob.R, _ld8(prob.v_draft), dtype=torch.bfloat16, device=dev),
+                              torch.empty(prob.v_draft, H, dtype=torch.float32, device=dev) if weight_grad else None)
+        gh, gl, gw = grad
+        if gw is not None and (gw.shape != (prob.v_draft, H) or gw.dtype != torch.float32 or not gw.is_contiguous()
+                               or not gw.is_cuda):
+            raise ValueError(f"grad_weight must be a contiguous float32 [{prob.v_draft}, {H}] device tensor")
         if gh.shape != (prob.R, H) or gh.dtype != torch.bfloat16 or not gh.is_contiguous():
             raise ValueError(f"grad_hidden must be a contiguous bfloat16 [{prob.R}, {H}] tensor")
         if (gl.dim() != 2 or gl.shape[0] != prob.R or gl.shape[1] < prob.v_draft or gl.stride(1) != 1
                 or gl.dtype != torch.bfloat16):
             raise ValueError(f"grad_logits must be a bfloat16 [{prob.R}, ld>={prob.v_draft}] tensor")
         dims = _dims(prob, X, None, ld_grad=gl.stride(0))
-        g = _lib.VsdGrad(gl.data_ptr(), gh.data_ptr(), None)
+        g = _lib.VsdGrad(gl.data_ptr(), gh.data_ptr(), None if gw is None else gw.data_ptr())
     else:
         if grad is None:
             grad = torch.empty_like(X)

@@ -200,7 +200,7 @@ def test_fused_lm_head_validation(lib):
                                          FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(grad), FAKE, None)
     assert bwd(fdims(), _lib.VsdGrad(FAKE, None, None)) == 1
     assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE + 8, None)) == 4
-    assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE, FAKE)) == 6
+    assert bwd(fdims(), _lib.VsdGrad(FAKE, FAKE, FAKE + 8)) == 4            # grad_weight misaligned
     assert bwd(fdims(ld_draft=999), _lib.VsdGrad(FAKE, FAKE, None)) == 2
     assert bwd(fdims(ld_draft=1004), _lib.VsdGrad(FAKE, FAKE, None)) == 2   # 2008 bytes: not 16-B rows
     assert bwd(fdims(), _lib.VsdGrad(None, FAKE, None)) == 1

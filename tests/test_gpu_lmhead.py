@@ -9,7 +9,8 @@ LM head (exact float64 logits handed to the per-position oracle).
 * Scoring and backward: run on the oracle's tokens (vsd_score_paths with
   given tokens, then the backward) and compared under the materialised path's
   bars; the hidden-state gradient to 1e-2 relative Frobenius error and 2e-3
-  absolute.  The one-pass draw-and-score outputs are also compared on every
+  absolute; where every position is compared, the draft weight's gradient
+  g^T H_d to 1e-2 relative Frobenius error and 1e-2 of its largest entry.  The one-pass draw-and-score outputs are also compared on every
   position whose tokens all agree.
 * Sizes: a small batch checked on every position (two row tiles, the last
   ragged; vocabularies that span several slices and end mid-tile), edge cases
@@ -35,12 +36,13 @@ def _heads(inp):
     return vsd.LmHead(inp["Hd"], inp["Wd"]), vsd.LmHead(inp["Ht"], inp["Wt"])
 
 
-def _bwd(prob, params, Xs, sc, toks):
+def _bwd(prob, params, Xs, sc, toks, weight=False):
     gl = torch.full((prob.R, (prob.v_draft + 7) // 8 * 8), SENTINEL, dtype=torch.bfloat16, device=DEV)
     gh = torch.empty(prob.R, Xs.hidden.shape[1], dtype=torch.bfloat16, device=DEV)
+    gw = torch.full((prob.v_draft, Xs.hidden.shape[1]), SENTINEL, dtype=torch.float32, device=DEV) if weight else None
     vsd.weighted_loss_bwd(prob, params, Xs, sc.lse_draft, toks[0], toks[1], sc.coef_a, sc.coef_b,
-                          grad=vsd.LmHeadGrad(gh, gl))
-    return gh, gl
+                          grad=vsd.LmHeadGrad(gh, gl, gw))
+    return (gh, gl, gw) if weight else (gh, gl)
 
 
 def _rows_of(cfg, positions):
@@ -114,7 +116,8 @@ def check_lmhead(cfg, inp, positions, params=None, label=""):
     for t, name in zip(full_tok, ("tok_draft", "tok_target", "tok_greedy")):
         t.index_copy_(0, idx, torch.as_tensor(ora[name].astype(np.int32), device=DEV))
     sc2 = vsd.score_paths(prob, params, Xs, Ys, *full_tok, inp["d2t"], inp["valid_depth"])
-    gh2, gl2 = _bwd(prob, params, Xs, sc2, full_tok)
+    every = len(positions) == cfg.P  # the weight gradient sums over every row: checked when all are compared
+    gh2, gl2, gw2 = _bwd(prob, params, Xs, sc2, full_tok, weight=True)
     torch.cuda.synchronize()
     assert int(sc2.device_error.item()) == 0
     summary = compare(cfg, dict(tokens=full_tok, score=sc2, grad=gl2), rows, ora, positions, label=label)
@@ -132,6 +135,16 @@ def check_lmhead(cfg, inp, positions, params=None, label=""):
     fro = np.linalg.norm((got - ref)[keep_rows]) / max(np.linalg.norm(ref[keep_rows]), 1e-30)
     assert fro <= 1e-2, f"{label} grad_hidden relative Frobenius error {fro}"
     summary["grad_hidden_fro"] = float(fro)
+    # 5. weight gradient g^T H_d (every row contributes; rows of near-tie
+    #    positions would too, so the check needs none)
+    if every and not summary["near_tie_positions"]:
+        gw = gw2.cpu().numpy()
+        refw = ora["grad_weight"]
+        fro_w = np.linalg.norm(gw - refw) / max(np.linalg.norm(refw), 1e-30)
+        assert fro_w <= 1e-2, f"{label} grad_weight relative Frobenius error {fro_w}"
+        assert np.abs(gw - refw).max() <= 1e-2 * np.abs(refw).max() + 1e-6, f"{label} grad_weight max abs err"
+        summary["grad_weight_fro"] = float(fro_w)
+        log(f"[{label}] dW rel fro {fro_w:.2e}")
     summary["near"] = near
     log(f"[{label}] ok: worst {summary['worst']}, dH rel fro {fro:.2e}")
     return summary
@@ -143,7 +156,8 @@ SMALL = scaled("C5", B=2, T=8, N=4, L=3, v_draft=4500, v_target=9000, hidden=256
 def test_small_batch_every_position():
     cfg = SMALL
     inp = make_inputs(cfg, DEV)
-    check_lmhead(cfg, inp, list(range(cfg.P)), label="C5s")
+    summary = check_lmhead(cfg, inp, list(range(cfg.P)), label="C5s")
+    assert "grad_weight_fro" in summary  # the weight gradient was compared
 
 
 @pytest.mark.parametrize("case", ["identity", "ragged_temp", "one_kstep_odd_vocab"])
