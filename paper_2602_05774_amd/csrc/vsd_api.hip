@@ -557,11 +557,6 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   a.lse_p = out->lse_target;
   a.la = la;
   a.lq = lq;
-  // target elements streamed per draft chunk: the whole target row split
-  // into as many blocks as there are 512-element draft chunks, each block a
-  // multiple of 512 elements
-  const int64_t nchunks = ((int64_t)dims->v_draft + 511) / 512;
-  a.tblock = (int32_t)(512 * ((dims->v_target + 512 * nchunks - 1) / (512 * nchunks)));
   float* kl_row = nullptr;
   if (kl_on(params)) {
     kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);

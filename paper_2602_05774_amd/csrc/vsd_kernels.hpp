@@ -26,7 +26,6 @@ struct SampleArgs {
   float* lse_p;              // [R] optional
   float* la;                 // [R,3]
   float* lq;                 // [R,3]
-  int32_t tblock;            // mapped: target elements streamed per 512-element chunk
   // top-K renormalised KL term (fused only; kl_k > 0 turns it on)
   int32_t kl_k;
   int32_t* kl_idx;           // [R, kl_k]
