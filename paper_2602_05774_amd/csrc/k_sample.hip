@@ -63,10 +63,32 @@ template <>
 __device__ __forceinline__ bf16_t neg_inf<bf16_t>() { return (bf16_t)0xFF80u; }
 
 // Per-lane online log-sum-exp of v/T in the scorer's exactly consistent form:
-// mraw = largest raw value, mc = float(mraw * c), s = sum of
+// mraw = a raw reference value, mc = float(mraw * c), s = sum of
 // exp2(fma(v, c, -mc)), c = log2(e)/T.  Elements equal to -inf add nothing.
+// add8 moves the reference up to the running maximum.  add8_fixed keeps the
+// reference that start8 took from the lane's first slice and tracks no
+// maximum: one fma, exp2 and add per element.  Every identity used after the
+// row (the reduction, the rounding correction of mc, log q) holds for any
+// reference; a lane whose sum leaves [0, 2^100] (an element about 100 / c
+// above its reference, or a NaN) is recomputed with add8 (bad()).
 struct LaneLse {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
+
+  __device__ __forceinline__ void start8(const float (&v)[8], float c) {
+    const float cm = max8(v);
+    if (cm > mraw) {
+      s *= __builtin_amdgcn_exp2f(mc - cm * c);
+      mc = cm * c;
+      mraw = cm;
+    }
+  }
+
+  __device__ __forceinline__ void add8_fixed(const float (&v)[8], float c) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(v[k], c, -mc));
+  }
+
+  __device__ __forceinline__ bool bad() const { return !(s <= 0x1p100f); }
 
   __device__ __forceinline__ void add8(const float (&v)[8], float c) {
     const float cm = max8(v);
@@ -94,18 +116,63 @@ struct RowShared {
   float p_mraw[2], p_mc[2], p_s[2];  // target log-sum-exp partials of the two wavefronts
 };
 
-// Log-sum-exp of target elements [lo, hi) of a row (guarded at both ends).
+// The lane's slice of a row at g (elements past n read as -inf).
 template <typename T>
+__device__ __forceinline__ void load_slice(const T* Y, int g, int n, float (&v)[8]) {
+  if (g + 8 <= n) {
+    load8(Y + g, v);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = (g + k < n) ? load1(Y + g + k) : -INFINITY;
+  }
+}
+
+// Log-sum-exp of target elements [lo, hi) of a row (guarded at both ends);
+// FIXED: against the lane's fixed reference, a whole range without guards.
+template <bool FIXED, typename T>
 __device__ __forceinline__ void stream_lse(const T* Y, int lo, int hi, int lane, float c2, LaneLse& acc) {
+  if (FIXED && hi - lo == kStream) {
+    float v0[8], v1[8];
+    load8(Y + lo + lane * 8, v0);
+    load8(Y + lo + kChunk + lane * 8, v1);
+    acc.add8_fixed(v0, c2);
+    acc.add8_fixed(v1, c2);
+    return;
+  }
   for (int g = lo + lane * 8; g - lane * 8 < hi; g += kChunk) {
     float v[8];
-    if (g + 8 <= hi) {
-      load8(Y + g, v);
-    } else {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = (g + k < hi) ? load1(Y + g + k) : -INFINITY;
-    }
-    acc.add8(v, c2);
+    load_slice(Y, g, hi, v);
+    if (FIXED)
+      acc.add8_fixed(v, c2);
+    else
+      acc.add8(v, c2);
+  }
+}
+
+// Wavefront w of a row streams the target ranges [lo, lo + kStream) with
+// lo = w kStream + j 2 kStream: the reference of its accumulator comes from
+// its lane's first slice, and the careful recomputation repeats every range.
+template <typename T>
+__device__ __forceinline__ void stream_start(const T* Y, int w, int Vt, int lane, float c2, LaneLse& acc) {
+  float v[8];
+  load_slice(Y, w * kStream + lane * 8, min(w * kStream + kStream, Vt), v);
+  acc.start8(v, c2);
+}
+template <typename T>
+__device__ void stream_redo(const T* Y, int w, int Vt, int lane, float c2, LaneLse& acc) {
+  acc = LaneLse{};
+  for (int lo = w * kStream; lo < Vt; lo += 2 * kStream) stream_lse<false>(Y, lo, min(lo + kStream, Vt), lane, c2, acc);
+}
+
+// Careful recomputation over the lane's slices g = lane 8 + j kChunk of a row
+// of n elements (the chunk layout of both wavefronts).
+template <typename T>
+__device__ void row_redo(const T* X, int n, int lane, float c, LaneLse& acc) {
+  acc = LaneLse{};
+  for (int g = lane * 8; g < n; g += kChunk) {
+    float v[8];
+    load_slice(X, g, n, v);
+    acc.add8(v, c);
   }
 }
 
@@ -115,9 +182,15 @@ template <typename T, bool MAPPED, bool FUSED>
 __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f, LaneLse& lq, LaneLse& lp,
                            float cp2, int lane) {
   const int nfull = Vd / kChunk;
+  if (FUSED && MAPPED) stream_start(Y, 0, Vt, lane, cp2, lp);
   if (nfull > 0) {
     Raw8<T> xr;
     xr.load(X + lane * 8);
+    if (FUSED) {
+      float x0[8];
+      xr.unpack(x0);
+      lq.start8(x0, f.c2);
+    }
     for (int it = 0; it < nfull; ++it) {
       const int base = it * kChunk + lane * 8;
       Raw8<T> xn;
@@ -127,9 +200,9 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
       if (FUSED && MAPPED) {  // before the draws: the target wavefront's gathers of this
         // block's mapped elements then find its lines in L2 more often
         const int lo = it * 2 * kStream;
-        stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
+        stream_lse<true>(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
       }
-      if (FUSED) lq.add8(x, f.c2);
+      if (FUSED) lq.add8_fixed(x, f.c2);
       f.draw(base, x, 8);
       xr = xn;
     }
@@ -144,13 +217,13 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
     f.draw(base, x, nvalid);
     if (FUSED && MAPPED) {
       const int lo = nfull * 2 * kStream;
-      stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
+      stream_lse<true>(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
     }
   }
   if (FUSED && MAPPED) {  // target elements past the last chunk's block: even half-blocks
     const int nchunks = (Vd + kChunk - 1) / kChunk;
     for (int lo = nchunks * 2 * kStream; lo < Vt; lo += 2 * kStream)
-      stream_lse(Y, lo, min(lo + kStream, Vt), lane, cp2, lp);
+      stream_lse<true>(Y, lo, min(lo + kStream, Vt), lane, cp2, lp);
   }
 }
 
@@ -172,6 +245,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       bg.idx = better ? base + k : bg.idx;
     }
   };
+  if (FUSED && MAPPED) stream_start(Y, 1, Vt, lane, f.c2, lp);
   if (nfull > 0) {
     uint32_t t[8];
     T g[8];
@@ -191,6 +265,11 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       gather(t);
     } else {
       yr.load(Y + lane * 8);
+      if (FUSED) {
+        float y0[8];
+        yr.unpack(y0);
+        lp.start8(y0, f.c2);
+      }
     }
     for (int it = 0; it < nfull; ++it) {
       const int chunk = it * kChunk;
@@ -206,7 +285,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       }
       if (FUSED && MAPPED) {  // this chunk's target block, second half
         const int lo = it * 2 * kStream + kStream;
-        stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
+        stream_lse<true>(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
       }
       float y[8];
       if (MAPPED) {
@@ -217,7 +296,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
         load8(tile + lane * 8, y);
       } else {
         yr.unpack(y);
-        if (FUSED) lp.add8(y, f.c2);
+        if (FUSED) lp.add8_fixed(y, f.c2);
       }
       greedy(base, y, 8);
       if (DRAW) f.draw(base, y, 8);
@@ -236,7 +315,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
     const int nvalid = min(8, max(0, Vd - base));
     if (FUSED && MAPPED) {
       const int lo = nfull * 2 * kStream + kStream;
-      stream_lse(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
+      stream_lse<true>(Y, min(lo, Vt), min(lo + kStream, Vt), lane, f.c2, lp);
     }
     if (MAPPED) {
 #pragma unroll
@@ -264,7 +343,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
   if (FUSED && MAPPED) {  // target elements past the last chunk's block: odd half-blocks
     const int nchunks = (Vd + kChunk - 1) / kChunk;
     for (int lo = nchunks * 2 * kStream + kStream; lo < Vt; lo += 2 * kStream)
-      stream_lse(Y, lo, min(lo + kStream, Vt), lane, f.c2, lp);
+      stream_lse<true>(Y, lo, min(lo + kStream, Vt), lane, f.c2, lp);
   }
 }
 
@@ -301,6 +380,8 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     if (draft_role) {
       FamilyDraw f{(uint32_t)r, 0u, a.offset, a.k0, a.k1, a.inv_tq, cq2};
       draft_wave<T, MAPPED, FUSED>(X, Y, a.Vd, a.Vt, f, lq, lp, cp2, lane);
+      if (FUSED && lq.bad()) row_redo(X, a.Vd, lane, cq2, lq);
+      if (FUSED && MAPPED && lp.bad()) stream_redo(Y, 0, a.Vt, lane, cp2, lp);
       wave_argmax(f.best.key, f.best.idx);
       if (FUSED) {
         lq.reduce();
@@ -322,6 +403,12 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
       WaveTopK tk;
       if (KL) tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
       target_wave<T, MAPPED, FUSED, KL>(Y, a.d2t, ytile[slot], a.Vd, a.Vt, f, bg, lp, map_bad, tk, lane);
+      if (FUSED && lp.bad()) {
+        if (MAPPED)
+          stream_redo(Y, 1, a.Vt, lane, cp2, lp);
+        else
+          row_redo(Y, a.Vt, lane, cp2, lp);
+      }
       if (map_bad) report_error(a.err, VSD_DEVERR_MAP_RANGE);
       if (KL) {
         tk.finish(lane);

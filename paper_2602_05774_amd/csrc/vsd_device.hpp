@@ -165,9 +165,10 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   return r;
 }
 
-// Largest of 8 values in four instructions.
+// Largest of 8 values in four instructions (all v_max3_f32: a plain fmaxf of
+// the asm results would first quiet both operands).
 __device__ __forceinline__ float max8(const float (&v)[8]) {
-  return fmaxf(max3f(v[3], v[4], v[5]), max3f(v[6], v[7], max3f(v[0], v[1], v[2])));
+  return max3f(max3f(v[0], v[1], v[2]), max3f(v[3], v[4], v[5]), max3f(v[6], v[7], v[7]));
 }
 
 // ------------------------------------------------------ wave reductions ---

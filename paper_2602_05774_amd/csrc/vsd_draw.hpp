@@ -74,11 +74,23 @@ struct FamilyDraw {
   }
 
   // Draw the lane's 8 elements at `base` (values v, the first nvalid valid).
+  // A full slice is first tested as a whole: the largest value against the
+  // largest Philox word (the smallest j').  If that pair fails the bound, every
+  // element fails it: v_k c2 + off <= vmax c2 + off < log2(j'_min) <= log2(j'_k)
+  // up to the same rounding of the one log that the margin already covers.
   __device__ __forceinline__ void draw(int base, const float (&v)[8], int nvalid) {
     const uint32_t c0 = (uint32_t)base >> 2;
     const float off = bound_offset(fmaxf(best.key, wave_best));
-    uint32_t cand = cand4(philox(c0), v, c2, off) | (cand4(philox(c0 + 1), v + 4, c2, off) << 4);
-    cand &= (1u << nvalid) - 1u;
+    const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
+    uint32_t cand;
+    if (nvalid == 8) {
+      const uint32_t wmax = max(max(max(p0.x, p0.y), max(p0.z, p0.w)), max(max(p1.x, p1.y), max(p1.z, p1.w)));
+      const bool maybe = fmaf(max8(v), c2, off) >= __builtin_amdgcn_logf((float)((~wmax) >> 8));
+      if (__ballot(maybe) == 0ull) return;
+      cand = maybe ? cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4) : 0u;
+    } else {
+      cand = (cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4)) & ((1u << nvalid) - 1u);
+    }
     if (__ballot(cand != 0u) == 0ull) return;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {

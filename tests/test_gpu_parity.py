@@ -178,7 +178,7 @@ def test_full_size_sampled_positions(name):
 
 
 # ------------------------------------------------------------ edge cases
-def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False):
+def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False, ramp=0.0):
     g = torch.Generator(device="cpu").manual_seed(seed)
     R = B * T * N * L
     es = 4 if dtype == torch.float32 else 2
@@ -196,6 +196,9 @@ def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=Fa
     if const:
         X = torch.zeros(R, Vd)
         Y = torch.zeros(R, Vt)
+    if ramp:  # logits rising along the row: each lane's first slice lies far below its later ones
+        X = X + ramp * torch.arange(Vd) / Vd
+        Y = Y + ramp * torch.arange(Vt) / Vt
     depth = torch.randint(1, L + 1, (B * T * N,), generator=g).to(torch.int32) if ragged else None
     inp = {"X": _pad_rows(X.numpy(), ldd, dtype), "Y": _pad_rows(Y.numpy(), ldt, dtype),
            "d2t": None if d2t is None else d2t.to(DEV), "valid_depth": None if depth is None else depth.to(DEV)}
@@ -219,6 +222,12 @@ EDGES = {
                           ragged=True),
     "V1": dict(B=1, T=2, N=3, L=2, Vd=1, Vt=1, dtype=torch.float32, seed=11),
     "V1_map": dict(B=1, T=2, N=2, L=3, Vd=1, Vt=17, dtype=torch.bfloat16, seed=12, mapped=True),
+    # rows whose logits rise by 60 or 200 along the vocabulary (sums far above
+    # the first slice's maximum, and beyond the float range without rescaling)
+    "ramp60_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=9000, dtype=torch.bfloat16, seed=13, mapped=True, ramp=60.0),
+    "ramp200_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=9000, dtype=torch.bfloat16, seed=14, mapped=True,
+                        ramp=200.0),
+    "ramp200": dict(B=1, T=2, N=3, L=2, Vd=2500, Vt=2500, dtype=torch.float32, seed=15, ramp=200.0),
 }
 
 
@@ -311,7 +320,7 @@ def test_fused_sample_score_every_position(name):
 
 
 @pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models", "N1024_max_paths",
-                                  "L64_max_depth", "V1_map"])
+                                  "L64_max_depth", "V1_map", "ramp60_map", "ramp200_map", "ramp200"])
 def test_fused_edge_cases(name):
     spec = dict(EDGES[name])
     log(f"[fused-edge] {name}")
