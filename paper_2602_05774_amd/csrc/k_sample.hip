@@ -234,16 +234,24 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
                             LaneLse& lp, bool& map_bad, WaveTopK& tk, int lane) {
   auto same = [](int col) { return col; };
   const int nfull = Vd / kChunk;
-  auto greedy = [&](int base, const float (&y)[8], int nvalid) {
-    // a full chunk that no lane's maximum lifts above its running maximum
-    // changes nothing (the common case once a few chunks are seen)
-    if (nvalid == 8 && __ballot(max8(y) > bg.key) == 0ull) return;
+  // Greedy maximum: each lane keeps the first of its largest values, gw is the
+  // wavefront's largest so far.  A chunk in which no lane's maximum ymax
+  // (elements past nvalid hold -inf) exceeds gw changes nothing: an element
+  // below gw cannot be the row's maximum, and one equal to gw comes after the
+  // element that reached gw (every earlier chunk holds smaller indices), so it
+  // loses the tie.  gw rises a few times per row (each a new record of the
+  // row so far), whereas some lane of 64 improves on its own maximum in
+  // almost every chunk.
+  float gw = -INFINITY;
+  auto greedy = [&](int base, const float (&y)[8], int nvalid, float ymax) {
+    if (__ballot(ymax > gw) == 0ull) return;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const bool better = k < nvalid && y[k] > bg.key;
       bg.key = better ? y[k] : bg.key;
       bg.idx = better ? base + k : bg.idx;
     }
+    gw = wave_max(bg.key);
   };
   if (FUSED && MAPPED) stream_start(Y, 1, Vt, lane, f.c2, lp);
   if (nfull > 0) {
@@ -298,8 +306,9 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
         yr.unpack(y);
         if (FUSED) lp.add8_fixed(y, f.c2);
       }
-      greedy(base, y, 8);
-      if (DRAW) f.draw(base, y, 8);
+      const float ymax = max8(y);
+      greedy(base, y, 8, ymax);
+      if (DRAW) f.draw8(base, y, ymax);
       if (KL) tk.offer8(y, base, 0xFFu, same, lane);
       if (next) {
         if (MAPPED)
@@ -336,7 +345,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       y[k] = in ? (MAPPED ? load1(tile + lane * 8 + k) : load1(Y + base + k)) : -INFINITY;
     }
     if (FUSED && !MAPPED) lp.add8(y, f.c2);
-    greedy(base, y, nvalid);
+    greedy(base, y, nvalid, max8(y));
     if (DRAW) f.draw(base, y, nvalid);
     if (KL) tk.offer8(y, base, nvalid > 0 ? (1u << nvalid) - 1u : 0u, same, lane);
   }

@@ -50,6 +50,10 @@ struct FamilyDraw {
   float inv_t, c2;  // 1/T and log2(e)/T
   Best best{-INFINITY, 0x7FFFFFFF};
   float wave_best = -INFINITY;  // wavefront maximum known so far
+  // bound_offset(wave_best): after every draw no lane's best exceeds
+  // wave_best, so the threshold is wave_best itself and the offset changes
+  // only when wave_best is refreshed
+  float off = INFINITY;
 
   __device__ __forceinline__ uint4 philox(uint32_t c0) const { return philox4x32_10(c0, row, fam, offset, k0, k1); }
 
@@ -74,27 +78,38 @@ struct FamilyDraw {
   }
 
   // Draw the lane's 8 elements at `base` (values v, the first nvalid valid).
-  // A full slice is first tested as a whole: the largest value against the
-  // largest Philox word (the smallest j').  If that pair fails the bound, every
-  // element fails it: v_k c2 + off <= vmax c2 + off < log2(j'_min) <= log2(j'_k)
-  // up to the same rounding of the one log that the margin already covers.
+  // A full slice is first tested as a whole: the largest value vmax against
+  // the largest Philox word (the smallest j').  If that pair fails the bound,
+  // every element fails it: v_k c2 + off <= vmax c2 + off < log2(j'_min) <=
+  // log2(j'_k) up to the same rounding of the one log that the margin already
+  // covers.
   __device__ __forceinline__ void draw(int base, const float (&v)[8], int nvalid) {
-    const uint32_t c0 = (uint32_t)base >> 2;
-    const float off = bound_offset(fmaxf(best.key, wave_best));
-    const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
-    uint32_t cand;
     if (nvalid == 8) {
-      const uint32_t wmax = max(max(max(p0.x, p0.y), max(p0.z, p0.w)), max(max(p1.x, p1.y), max(p1.z, p1.w)));
-      const bool maybe = fmaf(max8(v), c2, off) >= __builtin_amdgcn_logf((float)((~wmax) >> 8));
-      if (__ballot(maybe) == 0ull) return;
-      cand = maybe ? cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4) : 0u;
-    } else {
-      cand = (cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4)) & ((1u << nvalid) - 1u);
+      draw8(base, v, max8(v));
+      return;
     }
+    const uint32_t c0 = (uint32_t)base >> 2;
+    const uint32_t cand = (cand4(philox(c0), v, c2, off) | (cand4(philox(c0 + 1), v + 4, c2, off) << 4)) &
+                          ((1u << nvalid) - 1u);
+    exact(base, v, c0, cand);
+  }
+  __device__ __forceinline__ void draw8(int base, const float (&v)[8], float vmax) {
+    const uint32_t c0 = (uint32_t)base >> 2;
+    const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
+    const uint32_t wmax = max(max(max(p0.x, p0.y), max(p0.z, p0.w)), max(max(p1.x, p1.y), max(p1.z, p1.w)));
+    const bool maybe = fmaf(vmax, c2, off) >= __builtin_amdgcn_logf((float)((~wmax) >> 8));
+    if (__ballot(maybe) == 0ull) return;
+    exact(base, v, c0, maybe ? cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4) : 0u);
+  }
+  // Exact keys of the candidates (bit k of cand: element base + k).
+  __device__ __forceinline__ void exact(int base, const float (&v)[8], uint32_t c0, uint32_t cand) {
     if (__ballot(cand != 0u) == 0ull) return;
+    // the candidate's Philox word is recomputed (the counter made opaque), so
+    // no word of the slice stays alive through the exact keys
+    asm volatile("" : "+v"(c0));
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      if (cand & (1u << k)) {  // rare: the exact key, Philox word recomputed
+      if (cand & (1u << k)) {  // rare
         const float key = gumbel_key(v[k], inv_t, word_of(philox(c0 + (k >> 2)), k & 3));
         if (key > best.key) {
           best.key = key;
@@ -102,7 +117,10 @@ struct FamilyDraw {
         }
       }
     }
-    if (__ballot(best.key > wave_best) != 0ull) wave_best = wave_max(best.key);
+    if (__ballot(best.key > wave_best) != 0ull) {
+      wave_best = wave_max(best.key);
+      off = bound_offset(wave_best);
+    }
   }
 };
 
