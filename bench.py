@@ -411,11 +411,13 @@ def main():
     # The one-pass sampler is bound by VALU issue (its counters show the SIMDs
     # issuing at their peak rate): its roofline counts the method's essential
     # lane operations per live row -- 4 per logit for the two log-sum-exps
-    # (max, fma, exp2, add), 40 per Philox4x32-10 call (10 rounds of two
+    # (unpack, fma, exp2, add), 40 per Philox4x32-10 call (10 rounds of two
     # 32x32->64 products and two 3-way XORs; ceil(V_d/4) calls per family, two
-    # families) and 6 per key for the candidate bound (not, shift, convert,
-    # log2, fma, compare).  The backward is bound by HBM.
-    ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4) + 6.0 * 2 * cfg.v_draft)
+    # families) and 14 per 8-key slice for the candidate bound (largest of 8
+    # values and of 8 Philox words, 4 three-way maxima each; not, shift,
+    # convert, log2, fma, compare).  The backward is bound by HBM.
+    ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4)
+                     + 14.0 * 2 * ((cfg.v_draft + 7) // 8))
     kernels["sample_score"]["valu_lane_ops"] = ss_ops
     kernels["sample_score"]["TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
     kl_variant = {"kl_topk": params_kl.kl_topk, "kl_weight": params_kl.kl_weight,
