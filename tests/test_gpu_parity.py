@@ -178,7 +178,8 @@ def test_full_size_sampled_positions(name):
 
 
 # ------------------------------------------------------------ edge cases
-def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False, ramp=0.0):
+def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False, ramp=0.0,
+            masked_prefix=0):
     g = torch.Generator(device="cpu").manual_seed(seed)
     R = B * T * N * L
     es = 4 if dtype == torch.float32 else 2
@@ -199,6 +200,10 @@ def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=Fa
     if ramp:  # logits rising along the row: each lane's first slice lies far below its later ones
         X = X + ramp * torch.arange(Vd) / Vd
         Y = Y + ramp * torch.arange(Vt) / Vt
+    if masked_prefix:  # a vocabulary mask: the first columns of every row are -inf (the target's up to the
+        # first unmasked draft column's image, so every drawn token keeps a finite log p)
+        X[:, :masked_prefix] = -float("inf")
+        Y[:, :int(d2t[masked_prefix]) if mapped else masked_prefix] = -float("inf")
     depth = torch.randint(1, L + 1, (B * T * N,), generator=g).to(torch.int32) if ragged else None
     inp = {"X": _pad_rows(X.numpy(), ldd, dtype), "Y": _pad_rows(Y.numpy(), ldt, dtype),
            "d2t": None if d2t is None else d2t.to(DEV), "valid_depth": None if depth is None else depth.to(DEV)}
@@ -228,6 +233,9 @@ EDGES = {
     "ramp200_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=9000, dtype=torch.bfloat16, seed=14, mapped=True,
                         ramp=200.0),
     "ramp200": dict(B=1, T=2, N=3, L=2, Vd=2500, Vt=2500, dtype=torch.float32, seed=15, ramp=200.0),
+    # -inf over the first 1100 draft columns and ~4400 target columns: every lane's first slice is masked
+    "masked_prefix_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=12000, dtype=torch.bfloat16, seed=16, mapped=True,
+                              masked_prefix=1100),
 }
 
 
@@ -320,7 +328,8 @@ def test_fused_sample_score_every_position(name):
 
 
 @pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models", "N1024_max_paths",
-                                  "L64_max_depth", "V1_map", "ramp60_map", "ramp200_map", "ramp200"])
+                                  "L64_max_depth", "V1_map", "ramp60_map", "ramp200_map", "ramp200",
+                                  "masked_prefix_map"])
 def test_fused_edge_cases(name):
     spec = dict(EDGES[name])
     log(f"[fused-edge] {name}")
