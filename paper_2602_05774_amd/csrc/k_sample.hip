@@ -65,12 +65,18 @@ __device__ __forceinline__ bf16_t neg_inf<bf16_t>() { return (bf16_t)0xFF80u; }
 // Per-lane online log-sum-exp of v/T in the scorer's exactly consistent form:
 // mraw = a raw reference value, mc = float(mraw * c), s = sum of
 // exp2(fma(v, c, -mc)), c = log2(e)/T.  Elements equal to -inf add nothing.
-// add8 moves the reference up to the running maximum.  add8_fixed keeps the
-// reference that start8 took from the lane's first slice and tracks no
-// maximum: one fma, exp2 and add per element.  Every identity used after the
-// row (the reduction, the rounding correction of mc, log q) holds for any
-// reference; a lane whose sum leaves [0, 2^100] (an element about 100 / c
-// above its reference, or a NaN) is recomputed with add8 (bad()).
+// Every identity used after the row (the reduction, the rounding correction
+// of mc, log q) holds for any reference, so the reference need not be the
+// maximum:
+//   add8        moves it up to the running maximum (the careful form);
+//   add8_lazy   moves it only when the slice's maximum (already known to the
+//               caller) exceeds it by more than 64 / c, so terms stay below
+//               2^64: one compare per slice;
+//   add8_fixed  keeps the reference start8 took from the lane's first slice
+//               and tracks nothing: one fma, exp2 and add per element.
+// A lane whose sum leaves [0, 2^120] (an element about 120 / c above its
+// reference, or a NaN) is recomputed with add8 (bad()); 64 lanes and two
+// wavefronts of such sums still merge below the float range.
 struct LaneLse {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
 
@@ -88,7 +94,22 @@ struct LaneLse {
     for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(v[k], c, -mc));
   }
 
-  __device__ __forceinline__ bool bad() const { return !(s <= 0x1p100f); }
+  // add8_lazy's threshold in raw units, mraw + 64 / c (-inf while empty); only
+  // add8_lazy moves the reference of an accumulator it is used on
+  float lim = -INFINITY;
+  __device__ __forceinline__ void add8_lazy(const float (&v)[8], float vmax, float c) {
+    // a wavefront-uniform test first keeps the common case a scalar branch
+    if (__ballot(vmax > lim) != 0ull && vmax > lim) {  // then vmax > mraw: mc does not decrease
+      const float nmc = vmax * c;
+      s *= __builtin_amdgcn_exp2f(mc - nmc);
+      mc = nmc;
+      mraw = vmax;
+      lim = vmax + 64.0f / c;
+    }
+    add8_fixed(v, c);
+  }
+
+  __device__ __forceinline__ bool bad() const { return !(s <= 0x1p120f); }
 
   __device__ __forceinline__ void add8(const float (&v)[8], float c) {
     const float cm = max8(v);
@@ -186,11 +207,6 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
   if (nfull > 0) {
     Raw8<T> xr;
     xr.load(X + lane * 8);
-    if (FUSED) {
-      float x0[8];
-      xr.unpack(x0);
-      lq.start8(x0, f.c2);
-    }
     for (int it = 0; it < nfull; ++it) {
       const int base = it * kChunk + lane * 8;
       Raw8<T> xn;
@@ -202,8 +218,9 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
         const int lo = it * 2 * kStream;
         stream_lse<true>(Y, min(lo, Vt), min(lo + kStream, Vt), lane, cp2, lp);
       }
-      if (FUSED) lq.add8_fixed(x, f.c2);
-      f.draw(base, x, 8);
+      const float xmax = max8(x);
+      if (FUSED) lq.add8_lazy(x, xmax, f.c2);
+      f.draw8(base, x, xmax);
       xr = xn;
     }
   }
@@ -273,11 +290,6 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       gather(t);
     } else {
       yr.load(Y + lane * 8);
-      if (FUSED) {
-        float y0[8];
-        yr.unpack(y0);
-        lp.start8(y0, f.c2);
-      }
     }
     for (int it = 0; it < nfull; ++it) {
       const int chunk = it * kChunk;
@@ -304,9 +316,9 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
         load8(tile + lane * 8, y);
       } else {
         yr.unpack(y);
-        if (FUSED) lp.add8_fixed(y, f.c2);
       }
       const float ymax = max8(y);
+      if (FUSED && !MAPPED) lp.add8_lazy(y, ymax, f.c2);
       greedy(base, y, 8, ymax);
       if (DRAW) f.draw8(base, y, ymax);
       if (KL) tk.offer8(y, base, 0xFFu, same, lane);
