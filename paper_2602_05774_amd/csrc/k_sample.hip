@@ -220,7 +220,7 @@ __device__ void draft_wave(const T* X, const T* Y, int Vd, int Vt, FamilyDraw& f
       }
       const float xmax = max8(x);
       if (FUSED) lq.add8_lazy(x, xmax, f.c2);
-      f.draw8(base, x, xmax);
+      f.draw8(base, x, xmax, it == 0);
       xr = xn;
     }
   }
@@ -320,7 +320,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       const float ymax = max8(y);
       if (FUSED && !MAPPED) lp.add8_lazy(y, ymax, f.c2);
       greedy(base, y, 8, ymax);
-      if (DRAW) f.draw8(base, y, ymax);
+      if (DRAW) f.draw8(base, y, ymax, it == 0);
       if (KL) tk.offer8(y, base, 0xFFu, same, lane);
       if (next) {
         if (MAPPED)

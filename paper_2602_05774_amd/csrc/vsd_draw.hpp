@@ -49,10 +49,12 @@ struct FamilyDraw {
   uint32_t row, fam, offset, k0, k1;
   float inv_t, c2;  // 1/T and log2(e)/T
   Best best{-INFINITY, 0x7FFFFFFF};
-  float wave_best = -INFINITY;  // wavefront maximum known so far
+  // A lower bound of the row's best key: the wavefront maximum of the keys
+  // found so far, or the seeded bound of draw8 while that is larger.
+  float wave_best = -INFINITY;
   // bound_offset(wave_best): after every draw no lane's best exceeds
   // wave_best, so the threshold is wave_best itself and the offset changes
-  // only when wave_best is refreshed
+  // only when wave_best changes
   float off = INFINITY;
 
   __device__ __forceinline__ uint4 philox(uint32_t c0) const { return philox4x32_10(c0, row, fam, offset, k0, k1); }
@@ -93,28 +95,65 @@ struct FamilyDraw {
                           ((1u << nvalid) - 1u);
     exact(base, v, c0, cand);
   }
-  __device__ __forceinline__ void draw8(int base, const float (&v)[8], float vmax) {
+  // seed = true (the row's first full slice): before the test, raise the
+  // wavefront threshold to a lower bound of the row's best key taken from
+  // these elements.  With d = 1 - u (exact on the 2^-24 grid), -ln u <= d / u,
+  // so G = -ln(-ln u) >= ln u - ln d; x/T + ln u - ln d less a margin that
+  // covers the hardware logarithms and the key's two roundings is below the
+  // element's normative key, hence below the row's best.  The element that
+  // attains the wavefront maximum of that bound still passes the filter, so
+  // the best key found afterwards reaches the seeded threshold.  Without the
+  // seed every element of a row's first chunk would take the exact key.
+  __device__ __forceinline__ void draw8(int base, const float (&v)[8], float vmax, bool seed = false) {
     const uint32_t c0 = (uint32_t)base >> 2;
     const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
+    if (seed) {
+      float lo[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float u = uniform_from_word(word_of(k < 4 ? p0 : p1, k & 3));
+        const float g = (__builtin_amdgcn_logf(u) - __builtin_amdgcn_logf(1.0f - u)) * kLn2;
+        lo[k] = v[k] * inv_t + g;
+      }
+      float thr = wave_max(max8(lo));
+      thr -= 1e-3f + 1e-5f * fabsf(thr);
+      if (thr > wave_best && thr < INFINITY) {
+        wave_best = thr;
+        off = bound_offset(thr);
+      }
+    }
     const uint32_t wmax = max(max(max(p0.x, p0.y), max(p0.z, p0.w)), max(max(p1.x, p1.y), max(p1.z, p1.w)));
     const bool maybe = fmaf(vmax, c2, off) >= __builtin_amdgcn_logf((float)((~wmax) >> 8));
     if (__ballot(maybe) == 0ull) return;
     exact(base, v, c0, maybe ? cand4(p0, v, c2, off) | (cand4(p1, v + 4, c2, off) << 4) : 0u);
   }
-  // Exact keys of the candidates (bit k of cand: element base + k).
+  // Exact keys of the candidates (bit k of cand: element base + k).  Each
+  // round takes every lane's lowest remaining candidate, so a round evaluates
+  // one key per lane that has one and the rounds number the largest count in
+  // a lane (a single key's code, not one per slice position).  A lane's
+  // candidates come in increasing index order, after the smaller indices of
+  // its earlier chunks, so the strict comparison keeps the first of equal
+  // keys.
   __device__ __forceinline__ void exact(int base, const float (&v)[8], uint32_t c0, uint32_t cand) {
     if (__ballot(cand != 0u) == 0ull) return;
     // the candidate's Philox word is recomputed (the counter made opaque), so
     // no word of the slice stays alive through the exact keys
     asm volatile("" : "+v"(c0));
+    while (cand != 0u) {
+      const int k = __builtin_ctz(cand);
+      cand &= cand - 1u;
+      // v[k] by selects; the empty asm keeps the compiler from turning the
+      // chain into an indexed stack array
+      float x = v[0];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      if (cand & (1u << k)) {  // rare
-        const float key = gumbel_key(v[k], inv_t, word_of(philox(c0 + (k >> 2)), k & 3));
-        if (key > best.key) {
-          best.key = key;
-          best.idx = base + k;
-        }
+      for (int j = 1; j < 8; ++j) {
+        x = k == j ? v[j] : x;
+        asm volatile("" : "+v"(x));
+      }
+      const float key = gumbel_key(x, inv_t, word_of(philox(c0 + ((uint32_t)k >> 2)), k & 3));
+      if (key > best.key) {
+        best.key = key;
+        best.idx = base + k;
       }
     }
     if (__ballot(best.key > wave_best) != 0ull) {
