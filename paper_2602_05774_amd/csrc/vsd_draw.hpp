@@ -67,6 +67,15 @@ struct FamilyDraw {
     return 24.0f - (thr - (2e-3f + 2e-6f * fabsf(thr))) * kLog2e;
   }
 
+  // Whether any lane's slice with maximum vmax can reach the threshold at
+  // all: every word gives G < 24 ln 2 (u <= 1 - 2^-24), which is the bound
+  // (24 - log2 j') ln 2 at j' = 1, so a slice failing it for log2 j' = 0
+  // fails for every word and needs no Philox draw.  Peaked rows skip most of
+  // their slices this way once their top elements are known.
+  __device__ __forceinline__ bool reachable(float vmax) const {
+    return __ballot(fmaf(vmax, c2, off) >= 0.0f) != 0ull;
+  }
+
   // Bound test of the 4 elements that share one Philox counter: bit k set
   // where v * log2e/T + off >= log2(j').
   __device__ __forceinline__ static uint32_t cand4(const uint4& w, const float* v, float c2, float off) {
@@ -90,6 +99,7 @@ struct FamilyDraw {
       draw8(base, v, max8(v));
       return;
     }
+    if (!reachable(max8(v))) return;  // elements past nvalid hold -inf
     const uint32_t c0 = (uint32_t)base >> 2;
     const uint32_t cand = (cand4(philox(c0), v, c2, off) | (cand4(philox(c0 + 1), v + 4, c2, off) << 4)) &
                           ((1u << nvalid) - 1u);
@@ -106,8 +116,8 @@ struct FamilyDraw {
   // seed every element of a row's first chunk would take the exact key.
   __device__ __forceinline__ void draw8(int base, const float (&v)[8], float vmax, bool seed = false) {
     const uint32_t c0 = (uint32_t)base >> 2;
-    const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
     if (seed) {
+      const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
       float lo[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -122,6 +132,8 @@ struct FamilyDraw {
         off = bound_offset(thr);
       }
     }
+    if (!reachable(vmax)) return;
+    const uint4 p0 = philox(c0), p1 = philox(c0 + 1);
     const uint32_t wmax = max(max(max(p0.x, p0.y), max(p0.z, p0.w)), max(max(p1.x, p1.y), max(p1.z, p1.w)));
     const bool maybe = fmaf(vmax, c2, off) >= __builtin_amdgcn_logf((float)((~wmax) >> 8));
     if (__ballot(maybe) == 0ull) return;
