@@ -179,7 +179,7 @@ def test_full_size_sampled_positions(name):
 
 # ------------------------------------------------------------ edge cases
 def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False, ramp=0.0,
-            masked_prefix=0):
+            masked_prefix=0, scale=1.0):
     g = torch.Generator(device="cpu").manual_seed(seed)
     R = B * T * N * L
     es = 4 if dtype == torch.float32 else 2
@@ -197,6 +197,8 @@ def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=Fa
     if const:
         X = torch.zeros(R, Vd)
         Y = torch.zeros(R, Vt)
+    if scale != 1.0:  # logits in the thousands: the bounds' relative margins and the keys' rounding dominate
+        X, Y = X * scale, Y * scale
     if ramp:  # logits rising along the row: each lane's first slice lies far below its later ones
         X = X + ramp * torch.arange(Vd) / Vd
         Y = Y + ramp * torch.arange(Vt) / Vt
@@ -236,6 +238,9 @@ EDGES = {
     # -inf over the first 1100 draft columns and ~4400 target columns: every lane's first slice is masked
     "masked_prefix_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=12000, dtype=torch.bfloat16, seed=16, mapped=True,
                               masked_prefix=1100),
+    "huge_logits_f32": dict(B=1, T=2, N=3, L=2, Vd=2000, Vt=2000, dtype=torch.float32, seed=17, scale=330.0),
+    "huge_logits_bf16_map": dict(B=1, T=2, N=3, L=2, Vd=2000, Vt=7000, dtype=torch.bfloat16, seed=18, mapped=True,
+                                 scale=330.0),
 }
 
 
@@ -329,7 +334,7 @@ def test_fused_sample_score_every_position(name):
 
 @pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models", "N1024_max_paths",
                                   "L64_max_depth", "V1_map", "ramp60_map", "ramp200_map", "ramp200",
-                                  "masked_prefix_map"])
+                                  "masked_prefix_map", "huge_logits_f32", "huge_logits_bf16_map"])
 def test_fused_edge_cases(name):
     spec = dict(EDGES[name])
     log(f"[fused-edge] {name}")
