@@ -69,8 +69,12 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
       v[k] = res > 0.0f ? __builtin_amdgcn_logf(res) * kLn2 : -INFINITY;
     }
   };
-  int base = lane * 8;
-  for (; base + 8 <= a.Vt; base += 8 * kWave) {
+  // whole 512-element chunks with every lane active (the draw's wavefront
+  // reductions, including the seed of the first chunk, need all lanes), then
+  // one partial chunk in which every lane takes part with its valid count
+  const int nfull = a.Vt / (8 * kWave);
+  for (int it = 0; it < nfull; ++it) {
+    const int base = it * 8 * kWave + lane * 8;
     float y[8], x[8], v[8];
     bool mapped[8];
     load8(Y + base, y);
@@ -88,10 +92,11 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
       for (int k = 0; k < 8; ++k) mapped[k] = true;
     }
     residual(y, x, mapped, v);
-    f.draw(base, v, 8);
+    f.draw8(base, v, max8(v), it == 0);
   }
-  if (base < a.Vt) {  // the partial last chunk
-    const int nvalid = a.Vt - base;
+  if (nfull * 8 * kWave < a.Vt) {  // the partial last chunk
+    const int base = nfull * 8 * kWave + lane * 8;
+    const int nvalid = min(8, max(0, a.Vt - base));
     float y[8], x[8], v[8];
     bool mapped[8];
 #pragma unroll
@@ -103,6 +108,8 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
       x[k] = mapped[k] ? load1(X + iv) : 0.0f;
     }
     residual(y, x, mapped, v);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = k < nvalid ? v[k] : -INFINITY;
     f.draw(base, v, nvalid);
   }
   wave_argmax(f.best.key, f.best.idx);
