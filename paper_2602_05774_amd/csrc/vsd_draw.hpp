@@ -44,7 +44,9 @@ struct Best {
 };
 
 // State and steps common to both wavefronts of a row: the Philox draws and
-// the exact filter of one family.
+// the exact filter of one family.  Every call must be made by all 64 lanes
+// of the wavefront (lanes without elements pass values of -inf): the seed and
+// the threshold's refresh are wavefront reductions.
 struct FamilyDraw {
   uint32_t row, fam, offset, k0, k1;
   float inv_t, c2;  // 1/T and log2(e)/T
