@@ -449,6 +449,9 @@ def main():
         "kernels": kernels, "three_calls": three_calls, "kl_variant": kl_variant, "roofline": roof,
         "cpu_baseline": base,
     }
+    ref = hbm_reference(dev)
+    ref["score_frac_of_read"] = three_calls["score_GB/s"] / ref["read_GB/s"]
+    line["hbm_reference"] = ref
     line["verification"] = bench_verify(cfg, prob, params, inp, out, ws, timed, dev)
     if not args.no_ctx:
         line["exact_context"] = bench_ctx(cfg, prob, params, inp, ws, timed, live, dev)
@@ -457,6 +460,40 @@ def main():
         torch.cuda.empty_cache()
         line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
     print(json.dumps(line), flush=True)
+
+
+def hbm_reference(dev, gib=4):
+    """Measured HBM rates of plain library kernels on this machine, as reference
+    points for the roofline fractions: a streaming read (the faster of two
+    integer reductions over a buffer of `gib` GiB, which read at the box's
+    practical rate) and a device copy of half that size (read + write)."""
+    import torch
+
+    n = (gib << 30) // 2
+    buf = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty(n // 2, dtype=torch.bfloat16, device=dev)
+
+    def median_ms(fn, reps=7):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[reps // 2]
+
+    t_read = min(median_ms(lambda: buf.view(torch.int64).sum()),
+                 median_ms(lambda: buf.view(torch.int32).view(-1, 1 << 15).amax(dim=1)))
+    t_copy = median_ms(lambda: dst.copy_(buf[: n // 2]))
+    res = {"read_GB/s": 2 * n / (t_read * 1e-3) / 1e9, "copy_GB/s": 2 * (2 * (n // 2)) / (t_copy * 1e-3) / 1e9,
+           "read_bytes": 2 * n, "kernels": "torch int64 sum / int32 row amax (read), copy_ (read + write)"}
+    del buf, dst
+    torch.cuda.empty_cache()
+    return res
 
 
 def bench_verify(cfg, prob, params, inp, out, ws, timed, dev):
