@@ -452,6 +452,10 @@ def main():
     ref = hbm_reference(dev)
     ref["score_frac_of_read"] = three_calls["score_GB/s"] / ref["read_GB/s"]
     line["hbm_reference"] = ref
+    if roof.get("traffic"):  # the dominant kernel's measured fetch rate against the box's streaming read
+        t_dom = kernels[dominant]["ms"]
+        roof["traffic_GB/s"] = roof["traffic"] / (t_dom * 1e-3) / 1e9
+        roof["traffic_frac_of_measured_read"] = roof["traffic_GB/s"] / ref["read_GB/s"]
     line["verification"] = bench_verify(cfg, prob, params, inp, out, ws, timed, dev)
     if not args.no_ctx:
         line["exact_context"] = bench_ctx(cfg, prob, params, inp, ws, timed, live, dev)
