@@ -3,13 +3,14 @@
 // Order: the larger value first, equal values by the smaller index.  An offer
 // takes part only if it is not below the current K-th best (a
 // wavefront-uniform threshold, -inf until K entries are known); such offers
-// are appended to a per-wavefront LDS buffer at positions given by a
-// wavefront prefix sum.  Whenever more than 64 entries are buffered the
+// are appended to a per-wavefront LDS buffer at positions counted from one
+// ballot per slice position.  Whenever more than 64 entries are buffered the
 // wavefront selects the K best (K rounds of wavefront argmax), keeps them at
 // the front in order and raises the threshold.  An element below the
 // threshold is worse than K known elements, so it cannot be in the final top
 // K: the result is exact.  After finish() the K best are at the front of the
 // buffer, in order.  Values must not be -inf (sentinel of empty slots).
+// Every call must be made by all 64 lanes of the wavefront.
 #pragma once
 
 #include "vsd_device.hpp"
@@ -40,6 +41,28 @@ struct WaveTopK {
     thi = 0x7FFFFFFF;
   }
 
+  // Before the first offer: raise the threshold to the K-th largest of the
+  // lanes' slice maxima vmax.  K lanes hold an element at least that large,
+  // so an element below it is worse than K elements that the first offer
+  // appends: the selection stays exact, and the first chunk appends about K
+  // entries instead of all of them.
+  __device__ void seed_lane_max(float vmax, int lane) {
+    if (K > kWave) return;
+    float v = vmax, kth = -INFINITY;
+    int r = 0;
+    for (; r < K; ++r) {
+      const float m = wave_max(v);
+      if (m == -INFINITY) break;
+      const uint64_t b = __ballot(v == m);
+      if (lane == __builtin_ctzll(b)) v = -INFINITY;  // one occurrence
+      kth = m;
+    }
+    if (r == K && kth > thv) {
+      thv = kth;
+      thi = 0x7FFFFFFF;
+    }
+  }
+
   // Offer a lane's 8 values x of columns base .. base+7 (bit k of `bits`:
   // column base+k takes part).  A value equal to the threshold is appended
   // too (its index decides at the next compaction).  Returns at once when no
@@ -58,22 +81,27 @@ struct WaveTopK {
     uint32_t q = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) q |= (((bits >> k) & 1u) && x[k] >= thv) ? (1u << k) : 0u;
-    const int cnt = __builtin_popcount(q);
-    int incl = cnt;  // inclusive prefix sum of cnt over the lanes
+    // positions by slice position k, then by lane: one ballot per k and the
+    // count of lower lanes in it (the buffer's order is irrelevant to the
+    // selection, which orders by value and index)
+    uint64_t bal[8];
+    int total = 0;
 #pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int o = __shfl_up(incl, off, kWave);
-      if (lane >= off) incl += o;
+    for (int k = 0; k < 8; ++k) {
+      bal[k] = __ballot((q >> k) & 1u);
+      total += __builtin_popcountll(bal[k]);
     }
-    const int total = __shfl(incl, kWave - 1, kWave);
     if (n + total > kTopKCap) compact(lane);
-    int pos = n + incl - cnt;
+    int pos0 = n;
+#pragma unroll
     for (int k = 0; k < 8; ++k) {
       if ((q >> k) & 1u) {
+        const int pos = pos0 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal[k] >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal[k], 0u));
         bv[pos] = x[k];
         bi[pos] = idx_of(base + k);
-        ++pos;
       }
+      pos0 += __builtin_popcountll(bal[k]);
     }
     n += total;
     if (n > kWave) compact(lane);  // keeps the threshold close to the K-th best so far
