@@ -172,47 +172,97 @@ __device__ __forceinline__ float max8(const float (&v)[8]) {
 }
 
 // ------------------------------------------------------ wave reductions ---
+// Every lane must be active.  Within each row of 16 lanes the values meet
+// through DPP lane permutations (quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror: after them every lane holds its row's
+// result); the four row results are then read with readlane and combined in
+// a fixed order, so every lane ends with the same, run-to-run identical
+// value and no LDS permute is needed.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ int lane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+constexpr int kDppQuad1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kDppQuad2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // row_half_mirror
+constexpr int kDppMirror = 0x140;     // row_mirror
+
 // (key, index) maximum; equal keys resolve to the smaller index.
-__device__ __forceinline__ void wave_argmax(float& key, int& idx) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ok = __shfl_xor(key, off, kWave);
-    const int oi = __shfl_xor(idx, off, kWave);
-    if (ok > key || (ok == key && oi < idx)) {
-      key = ok;
-      idx = oi;
-    }
+__device__ __forceinline__ void argmax_merge(float& key, int& idx, float ok, int oi) {
+  if (ok > key || (ok == key && oi < idx)) {
+    key = ok;
+    idx = oi;
   }
+}
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(float& key, int& idx) {
+  argmax_merge(key, idx, dpp_f<CTRL>(key), dpp_i<CTRL>(idx));
+}
+__device__ __forceinline__ void wave_argmax(float& key, int& idx) {
+  argmax_step<kDppQuad1>(key, idx);
+  argmax_step<kDppQuad2>(key, idx);
+  argmax_step<kDppHalfMirror>(key, idx);
+  argmax_step<kDppMirror>(key, idx);
+  float k = lane_f(key, 0);
+  int i = lane_i(idx, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) argmax_merge(k, i, lane_f(key, 16 * r), lane_i(idx, 16 * r));
+  key = k;
+  idx = i;
 }
 
 // Combine per-lane (max, sum of exp2(x - max)) pairs in the log2 domain.
+__device__ __forceinline__ void lse2_merge(float& m, float& s, float om, float os) {
+  const float nm = fmaxf(m, om);
+  s = s * __builtin_amdgcn_exp2f(m - nm) + os * __builtin_amdgcn_exp2f(om - nm);
+  m = nm;
+}
+template <int CTRL>
+__device__ __forceinline__ void lse2_step(float& m, float& s) {
+  lse2_merge(m, s, dpp_f<CTRL>(m), dpp_f<CTRL>(s));
+}
 __device__ __forceinline__ void wave_lse2(float& m, float& s) {
+  lse2_step<kDppQuad1>(m, s);
+  lse2_step<kDppQuad2>(m, s);
+  lse2_step<kDppHalfMirror>(m, s);
+  lse2_step<kDppMirror>(m, s);
+  float rm = lane_f(m, 0), rs = lane_f(s, 0);
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float om = __shfl_xor(m, off, kWave);
-    const float os = __shfl_xor(s, off, kWave);
-    const float nm = fmaxf(m, om);
-    s = s * __builtin_amdgcn_exp2f(m - nm) + os * __builtin_amdgcn_exp2f(om - nm);
-    m = nm;
-  }
+  for (int r = 1; r < 4; ++r) lse2_merge(rm, rs, lane_f(m, 16 * r), lane_f(s, 16 * r));
+  m = rm;
+  s = rs;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  v += dpp_f<kDppQuad1>(v);
+  v += dpp_f<kDppQuad2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
-  return v;
+  v = fmaxf(v, dpp_f<kDppQuad1>(v));
+  v = fmaxf(v, dpp_f<kDppQuad2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
 }
 
 __device__ __forceinline__ int wave_sum_int(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  v += dpp_i<kDppQuad1>(v);
+  v += dpp_i<kDppQuad2>(v);
+  v += dpp_i<kDppHalfMirror>(v);
+  v += dpp_i<kDppMirror>(v);
+  return (lane_i(v, 0) + lane_i(v, 16)) + (lane_i(v, 32) + lane_i(v, 48));
 }
 
 // First device-side data error wins; later ones are dropped.

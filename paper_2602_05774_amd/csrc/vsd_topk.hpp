@@ -132,15 +132,7 @@ struct WaveTopK {
       }
       float wv = lv;
       int wi = li;
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const float ov = __shfl_xor(wv, off, kWave);
-        const int oi = __shfl_xor(wi, off, kWave);
-        if (beats(ov, oi, wv, wi)) {
-          wv = ov;
-          wi = oi;
-        }
-      }
+      wave_argmax(wv, wi);
       if (wv == -INFINITY) break;
       if (lj >= 0 && li == wi && lv == wv) bv[lj] = -INFINITY;  // indices are unique: one owner
       if (lane == r) {
@@ -155,8 +147,8 @@ struct WaveTopK {
     }
     n = cnt;
     if (cnt == K) {
-      thv = __shfl(kv, K - 1, kWave);
-      thi = __shfl(ki, K - 1, kWave);
+      thv = lane_f(kv, K - 1);
+      thi = lane_i(ki, K - 1);
     }
   }
 
@@ -170,15 +162,7 @@ struct WaveTopK {
     for (int r = 0; r < K; ++r) {
       float wv = ev;
       int wi = ei;
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const float ov = __shfl_xor(wv, off, kWave);
-        const int oi = __shfl_xor(wi, off, kWave);
-        if (beats(ov, oi, wv, wi)) {
-          wv = ov;
-          wi = oi;
-        }
-      }
+      wave_argmax(wv, wi);
       if (wv == -INFINITY) break;
       if (ei == wi && ev == wv) {
         ev = -INFINITY;
@@ -196,8 +180,8 @@ struct WaveTopK {
     }
     n = cnt;
     if (cnt == K) {
-      thv = __shfl(kv, K - 1, kWave);
-      thi = __shfl(ki, K - 1, kWave);
+      thv = lane_f(kv, K - 1);
+      thi = lane_i(ki, K - 1);
     }
   }
 
