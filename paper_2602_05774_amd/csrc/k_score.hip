@@ -116,7 +116,7 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     const uint32_t keep = nvalid >= 8 ? 0xFFu : ((1u << nvalid) - 1u);
     return MAPPED ? ((mask[base >> 5] >> (base & 31)) & keep) : keep;
   };
-  auto fold = [&](int base, const float (&x)[8], uint32_t bits) {
+  auto fold = [&](int base, const float (&x)[8], uint32_t bits, bool first = false) {
     const float cm = max8(x);
     if (cm > mraw) {
       const float nmc = cm * c;
@@ -126,6 +126,12 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -mc));
+    if (first) {  // the threshold from the lanes' largest offered values of the first slice
+      float best = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) best = ((bits >> k) & 1u) ? fmaxf(best, x[k]) : best;
+      tk.seed_lane_max(best, lane);
+    }
     tk.offer8(x, base, bits, idx_of, lane);
   };
   int chunk = 0;
@@ -139,7 +145,7 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
       bits[u] = bits_of(base, 8);
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) fold(chunk + u * step + lane * 8, x[u], bits[u]);
+    for (int u = 0; u < U; ++u) fold(chunk + u * step + lane * 8, x[u], bits[u], chunk == 0 && u == 0);
   }
   for (; chunk < V; chunk += step) {
     const int base = chunk + lane * 8;
