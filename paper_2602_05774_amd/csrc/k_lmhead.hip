@@ -170,19 +170,32 @@ struct Core {
   // (i ^ row) & 7, so chunk c of row r sits at position c ^ (r & 7): the
   // fragment reads of 8 consecutive rows then cover all banks.  Rows past
   // nrow / ncol read the last valid row (their results are never used); K is
-  // a multiple of TK.
-  __device__ __forceinline__ void issue(int k0, bf16_t* L) const {
+  // a multiple of TK.  The lane's source addresses at K offset 0 are formed
+  // once per tile (row clamp and row stride); a stage only adds k0.
+  struct NtSrc {
+    const bf16_t* a[4];
+    const bf16_t* b[4];
+  };
+  __device__ __forceinline__ NtSrc nt_src() const {
     const int lane = threadIdx.x & 63, w = wave_id();
     const int lr = lane >> 3, lc = lane & 7;
+    NtSrc s;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = w * 32 + j * 8 + lr;
       const int cg = (lc ^ r) & 7;
-      const int64_t ar = min(row0 + r, nrow - 1);
-      const int br = min(col0 + r, ncol - 1);
-      __builtin_amdgcn_global_load_lds((const global_void*)(A + ar * lda + k0 + cg * 8),
-                                       (lds_void*)(L + (w * 32 + j * 8) * TK), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const global_void*)(B + (int64_t)br * ldb + k0 + cg * 8),
+      s.a[j] = A + min(row0 + r, nrow - 1) * lda + cg * 8;
+      s.b[j] = B + (int64_t)min(col0 + r, ncol - 1) * ldb + cg * 8;
+    }
+    return s;
+  }
+  __device__ __forceinline__ static void issue(const NtSrc& s, int k0, bf16_t* L) {
+    const int w = wave_id();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      __builtin_amdgcn_global_load_lds((const global_void*)(s.a[j] + k0), (lds_void*)(L + (w * 32 + j * 8) * TK),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const global_void*)(s.b[j] + k0),
                                        (lds_void*)(L + TM * TK + (w * 32 + j * 8) * TK), 16, 0, 0);
     }
   }
@@ -246,10 +259,11 @@ struct Core {
     for (int q = 0; q < 8; ++q) acc[q] = f32x16{};
     if (!NN) {  // direct loads: the next stage streams into the other buffer during this one
       const int nst = K / TK;
-      issue(0, lds);
+      const NtSrc src = nt_src();
+      issue(src, 0, lds);
       __syncthreads();
       for (int st = 0; st < nst; ++st) {
-        if (st + 1 < nst) issue((st + 1) * TK, lds + ((st + 1) & 1) * kStageNT);
+        if (st + 1 < nst) issue(src, (st + 1) * TK, lds + ((st + 1) & 1) * kStageNT);
         compute(lds + (st & 1) * kStageNT, acc);
         __syncthreads();  // waits for the direct loads too
       }
