@@ -179,7 +179,7 @@ def test_full_size_sampled_positions(name):
 
 # ------------------------------------------------------------ edge cases
 def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=False, const=False, ramp=0.0,
-            masked_prefix=0, scale=1.0):
+            masked_prefix=0, scale=1.0, map_swaps=0):
     g = torch.Generator(device="cpu").manual_seed(seed)
     R = B * T * N * L
     es = 4 if dtype == torch.float32 else 2
@@ -188,7 +188,13 @@ def _custom(B, T, N, L, Vd, Vt, dtype, seed, mapped=False, ragged=False, same=Fa
     Y = 3.0 * torch.randn(R, Vt, generator=g)
     d2t = None
     if mapped:
-        d2t = torch.sort(torch.randperm(Vt, generator=g)[:Vd]).values.to(torch.int32)
+        d2t = torch.randperm(Vt, generator=g)[:Vd]
+        if map_swaps >= 0:  # ascending, then map_swaps exchanges of two entries (-1: random order)
+            d2t = torch.sort(d2t).values
+            for _ in range(map_swaps):
+                i, j = torch.randint(0, Vd, (2,), generator=g).tolist()
+                d2t[i], d2t[j] = d2t[j].clone(), d2t[i].clone()
+        d2t = d2t.to(torch.int32)
         X = 0.7 * Y[:, d2t.long()] + 2.0 * torch.randn(R, Vd, generator=g)
     else:
         X = 0.8 * Y + 1.5 * torch.randn(R, Vd, generator=g)
@@ -241,6 +247,11 @@ EDGES = {
     "huge_logits_f32": dict(B=1, T=2, N=3, L=2, Vd=2000, Vt=2000, dtype=torch.float32, seed=17, scale=330.0),
     "huge_logits_bf16_map": dict(B=1, T=2, N=3, L=2, Vd=2000, Vt=7000, dtype=torch.bfloat16, seed=18, mapped=True,
                                  scale=330.0),
+    # injective maps that are not ascending: in random order, and ascending but for four exchanges
+    "random_order_map": dict(B=1, T=2, N=3, L=2, Vd=1003, Vt=4099, dtype=torch.bfloat16, seed=19, mapped=True,
+                             map_swaps=-1),
+    "swapped_map": dict(B=1, T=2, N=3, L=2, Vd=3000, Vt=9000, dtype=torch.bfloat16, seed=20, mapped=True,
+                        map_swaps=4),
 }
 
 
@@ -334,7 +345,8 @@ def test_fused_sample_score_every_position(name):
 
 @pytest.mark.parametrize("name", ["V1003_bf16_map", "V2_map", "N1_L1", "V5", "same_models", "N1024_max_paths",
                                   "L64_max_depth", "V1_map", "ramp60_map", "ramp200_map", "ramp200",
-                                  "masked_prefix_map", "huge_logits_f32", "huge_logits_bf16_map"])
+                                  "masked_prefix_map", "huge_logits_f32", "huge_logits_bf16_map", "random_order_map",
+                                  "swapped_map"])
 def test_fused_edge_cases(name):
     spec = dict(EDGES[name])
     log(f"[fused-edge] {name}")

@@ -8,7 +8,8 @@ counted and left out) or the residual draw's two best keys are closer than
 1e-3 (float32 p - q cancels).  Cases: C1 in full (fp32, shared vocabulary),
 C3-recipe positions at the full vocabularies (the residual runs over the whole
 target vocabulary, unmapped tokens included), C4-recipe positions (ragged,
-peaked, T_q = 0.5), ragged and odd vocabulary sizes, equal models (every token
+peaked, T_q = 0.5), ragged and odd vocabulary sizes, maps that are not ascending (in random
+order, and ascending but for a few exchanges), equal models (every token
 kept).  At the full C3 size the mean accepted length over all paths matches
 the mean expected accepted length sum_k S_k from scoring (the Monte-Carlo
 cross-check of Eq. accepted_len_cond), and the draws are deterministic.
@@ -99,7 +100,7 @@ def test_ragged_peaked():
 
 
 @pytest.mark.parametrize("name", ["V1003_f32", "V1003_bf16_map", "V2_map", "N1_L1", "same_models", "N1024_max_paths",
-                                  "L64_max_depth", "V1_map"])
+                                  "L64_max_depth", "V1_map", "random_order_map", "swapped_map"])
 def test_edge_cases(name):
     cfg, inp = _custom(**EDGES[name])
     ver, gpu = check_verify(cfg, inp, list(range(cfg.P)), params_of(cfg), f"edge {name} verify")
