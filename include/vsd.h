@@ -235,7 +235,7 @@ typedef enum vsd_car_input {
 } vsd_car_input;
 
 typedef struct vsd_dims {
-  int32_t B, T, N, L;  /* 1 <= B,T; 1 <= N <= 1024; 1 <= L <= 64 */
+  int32_t B, T, N, L;  /* 1 <= B,T; 1 <= N <= 1024; 1 <= L <= 64; R = B*T*N*L < 2^24 */
   int32_t v_draft;     /* draft vocabulary size, >= 1 */
   int32_t v_target;    /* target vocabulary size, >= v_draft */
   int32_t dtype;       /* vsd_dtype of the logit (or hidden/weight) arrays */

@@ -33,7 +33,12 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 
-constexpr int64_t kMaxRows = (int64_t)1 << 31;
+// A grid's size is a 32-bit count of work-items; the largest launch per row
+// is one 192-thread workgroup per path (per-depth sampling, L = 1), so rows
+// stay below 2^24, and the fused LM head's workgroups of 512 threads below
+// 2^23.
+constexpr int64_t kMaxRows = (int64_t)1 << 24;
+constexpr int64_t kMaxLmWorkgroups = (int64_t)1 << 23;
 constexpr int32_t kMaxHidden = 65536;
 
 size_t align_up(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -52,18 +57,18 @@ vsd_status check_dims(const vsd_dims* d) {
                 d->v_draft);
   if (d->dtype != VSD_F32 && d->dtype != VSD_BF16) return fail(VSD_ERR_INVALID_VALUE, "dtype=%d", d->dtype);
   const int64_t R = rows_of(d);
-  if (R >= kMaxRows) return fail(VSD_ERR_INVALID_SHAPE, "R=B*T*N*L=%lld must be < 2^31", (long long)R);
+  if (R >= kMaxRows) return fail(VSD_ERR_INVALID_SHAPE, "R=B*T*N*L=%lld must be < 2^24", (long long)R);
   if (d->hidden_dim < 0 || d->hidden_dim > kMaxHidden || d->hidden_dim % 64 != 0)
     return fail(VSD_ERR_INVALID_SHAPE, "hidden_dim=%d must be 0 or a multiple of 64 up to %d", d->hidden_dim,
                 kMaxHidden);
   if (d->hidden_dim > 0) {
     if (d->dtype != VSD_BF16) return fail(VSD_ERR_UNSUPPORTED, "the fused LM head takes bf16 operands only");
-    // workgroup ids of the fused kernels are 32-bit: row tiles x vocabulary tiles
+    // the fused kernels launch row tiles x vocabulary tiles workgroups
     const int64_t nrt = (R + vsd::kLmTile - 1) / vsd::kLmTile;
     const int64_t vt = std::max<int64_t>(
         std::max<int64_t>((d->v_draft + vsd::kLmTile - 1) / vsd::kLmTile, (d->hidden_dim + vsd::kLmTile - 1) / vsd::kLmTile),
         vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
-    if (nrt * vt >= kMaxRows)
+    if (nrt * vt >= kMaxLmWorkgroups)
       return fail(VSD_ERR_INVALID_SHAPE, "fused LM head: R=%lld rows x %lld vocabulary tiles too large",
                   (long long)R, (long long)vt);
   }

@@ -131,6 +131,16 @@ def test_bwd_rejects_bad_arguments(lib):
     assert call(_dims(), _params(kl_weight=0.5, kl_topk=10), g) == 1            # KL on: kl_idx / kl_grad required
 
 
+def test_row_limit_keeps_every_grid_within_32_bit_work_item_counts(lib):
+    # R = B*T*N*L < 2^24: the largest launch per row is one 192-thread workgroup per path
+    size = ctypes.c_size_t()
+    assert _sample(lib, _dims(B=1 << 12, T=1 << 12, N=1, L=1)) == 2
+    assert "2^24" in lib.vsd_last_error().decode()
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims(B=(1 << 24) - 1, T=1, N=1, L=1)),
+                                         ctypes.byref(size)) == 0
+    assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims(B=1 << 24, T=1, N=1, L=1)), ctypes.byref(size)) == 2
+
+
 def test_workspace_query_scales_with_rows(lib):
     small, big = ctypes.c_size_t(), ctypes.c_size_t()
     assert lib.vsd_score_workspace_bytes(ctypes.byref(_dims()), ctypes.byref(small)) == 0
