@@ -91,7 +91,7 @@ def score_position(X, Y, d2t, depth, tok_d, tok_t, tok_g, params=None):
     lse_q = np.zeros((nrow, N, L))
     lse_p = np.zeros((nrow, N, L))
     log_q = np.zeros((3, N, L))
-    log_p = np.zeros((3, N, L))
+    log_ratio = np.zeros((3, N, L))
     for s in range(N):
         for i in range(depth[s]):
             for k in range(nrow):
@@ -100,10 +100,15 @@ def score_position(X, Y, d2t, depth, tok_d, tok_t, tok_g, params=None):
             for f in range(3):
                 k = f if ctx else 0
                 z = toks[f][s, i]
-                log_q[f, s, i] = float(X[k, s, i, z]) / Tq - lse_q[k, s, i]
-                log_p[f, s, i] = float(Y[k, s, i, d2t[z]]) / Tp - lse_p[k, s, i]
+                x, y = float(X[k, s, i, z]), float(Y[k, s, i, d2t[z]])
+                log_q[f, s, i] = x / Tq - lse_q[k, s, i]
+                # log p - log q, grouped as (y/T_p - x/T_q) - (lse_p - lse_q):
+                # tokens of one row with equal y/T_p - x/T_q (common with
+                # bf16 logits) then get bitwise equal values, so the gate
+                # below sees their exact tie (equality accepts)
+                log_ratio[f, s, i] = (y / Tp - x / Tq) - (lse_p[k, s, i] - lse_q[k, s, i])
     # Eq. acc: alpha = min(1, p/q)  <=>  log alpha = min(0, log p - log q).
-    log_alpha = np.where(live[None], np.minimum(0.0, log_p - log_q), 0.0)
+    log_alpha = np.where(live[None], np.minimum(0.0, log_ratio), 0.0)
 
     # Prefix sums over depth: log S_k (Eq. survival_def) and log-likelihoods.
     LS = np.zeros((3, N, L))

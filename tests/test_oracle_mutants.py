@@ -182,6 +182,26 @@ def _check_ctx(P):
     return True
 
 
+def _check_exact_ties(P):
+    """Different tokens with equal y - x tie exactly and are accepted (the
+    pin of tests/test_oracle_paths.py, on a mutant module)."""
+    rng = np.random.default_rng(11)
+    for _ in range(100):
+        V = 64
+        y = np.round(rng.normal(0.0, 3.0, V) * 16) / 16
+        x = np.round(rng.normal(0.0, 3.0, V) * 16) / 16
+        g = int(np.argmax(y))
+        d = np.round(rng.normal(-1.0, 1.0) * 32) / 32
+        x[g] = y[g] - d
+        other = (g + 1 + int(rng.integers(V - 1))) % V
+        x[other] = y[other] - d
+        sc = P.score_position(x.reshape(1, 1, V), y.reshape(1, 1, V), None, [1], np.array([[other]]),
+                              np.array([[g]]), np.array([[g]]))
+        if not sc["accept_flag"][0, 0]:
+            return False
+    return True
+
+
 def _check_sampler(S):
     w = (np.arange(2 ** 23, dtype=np.uint64) << np.uint64(9)).astype(np.uint32)
     ug = S.uniform_from_word(w)
@@ -254,8 +274,12 @@ VERIFY_MUTANTS = [
 
 
 PATH_MUTANTS = [
-    ("np.minimum(0.0, log_p - log_q)", "np.maximum(0.0, log_p - log_q)"),
-    ("np.minimum(0.0, log_p - log_q)", "np.minimum(0.0, log_q - log_p)"),
+    ("np.minimum(0.0, log_ratio)", "np.maximum(0.0, log_ratio)"),
+    ("(y / Tp - x / Tq) - (lse_p[k, s, i] - lse_q[k, s, i])", "(x / Tq - y / Tp) - (lse_q[k, s, i] - lse_p[k, s, i])"),
+    ("(y / Tp - x / Tq) - (lse_p[k, s, i] - lse_q[k, s, i])", "(y / Tp - x / Tq) - (lse_p[k, s, i] + lse_q[k, s, i])"),
+    ("(y / Tp - x / Tq) - (lse_p[k, s, i] - lse_q[k, s, i])", "(y / Tp - x) - (lse_p[k, s, i] - lse_q[k, s, i])"),
+    # the regrouping lost: per-token log probabilities first, so exact ties break in their rounding
+    ("(y / Tp - x / Tq) - (lse_p[k, s, i] - lse_q[k, s, i])", "(y / Tp - lse_p[k, s, i]) - (x / Tq - lse_q[k, s, i])"),
     ("acc_flag[s, i] = LS[0, s, i] >= LS[2, s, i]", "acc_flag[s, i] = LS[0, s, i] > LS[2, s, i]"),
     ("corrected_ok = LS[1, s, i] >= LS[2, s, i]", "corrected_ok = LS[1, s, i] >= LS[0, s, i]"),
     ("val_flag[s, i] = acc_flag[s, i] or corrected_ok", "val_flag[s, i] = corrected_ok"),
@@ -274,10 +298,9 @@ PATH_MUTANTS = [
     ("coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] - c[s, lev])", "coef_a[s, i] += o_prime[s, lev] * (acc_flag[s, lev] + c[s, lev])"),
     ("g[s, i] = loss_scale / temp_draft * row", "g[s, i] = loss_scale * row"),
     ("row[tok_t[s, i]] -= b", "row[tok_d[s, i]] -= b"),
-    ("log_p[f, s, i] = float(Y[k, s, i, d2t[z]]) / Tp - lse_p[k, s, i]",
-     "log_p[f, s, i] = float(Y[k, s, i, z]) / Tp - lse_p[k, s, i]"),
+    ("x, y = float(X[k, s, i, z]), float(Y[k, s, i, d2t[z]])", "x, y = float(X[k, s, i, z]), float(Y[k, s, i, z])"),
     ("lse_p[k, s, i] = log_softmax_normaliser(Y[k, s, i], Tp)", "lse_p[k, s, i] = log_softmax_normaliser(Y[k, s, i, d2t], Tp)"),
-    ("log_q[f, s, i] = float(X[k, s, i, z]) / Tq - lse_q[k, s, i]", "log_q[f, s, i] = float(X[k, s, i, z]) - lse_q[k, s, i]"),
+    ("log_q[f, s, i] = x / Tq - lse_q[k, s, i]", "log_q[f, s, i] = x - lse_q[k, s, i]"),
     # exact context: a family scored on another family's rows, gradients on the wrong rows
     ("k = f if ctx else 0", "k = 0"),
     ("k = f if ctx else 0", "k = (f + 1) % 3 if ctx else 0"),
@@ -322,7 +345,7 @@ def test_verify_mutant_is_caught(old, new):
 def test_path_mutant_is_caught(golden_dir, old, new):
     P = _mutant(paths_mod, old, new)
     caught = (not _check_golden(P, golden_dir)) or (not _check_closed_form(P)) \
-        or (not _check_fd(P)) or (not _check_map(P)) or (not _check_ctx(P))
+        or (not _check_fd(P)) or (not _check_map(P)) or (not _check_ctx(P)) or (not _check_exact_ties(P))
     assert caught, f"no pin caught mutant {new!r}"
 
 

@@ -347,3 +347,32 @@ def test_sampled_tokens_are_minus_one_on_masked_slots():
     for t in toks:
         assert list(t[1, 2:]) == [-1, -1] and list(t[2, 1:]) == [-1, -1, -1]
         assert np.all(t[0] >= 0)
+
+
+def test_exact_ties_between_different_tokens_accept():
+    """Two different tokens of a row whose logits differ by the same amount
+    (y - x equal, as bf16 grids make common) have the same log alpha exactly
+    (Eq. acc: log p - log q = (y - x) - (lse_p - lse_q) at T = 1), so the
+    gate compares equal values and accepts (Alg. 2 accepts on equality).
+    The row normalisers are generic values, so the two per-token log
+    probabilities round differently; only their difference ties."""
+    rng = np.random.default_rng(11)
+    accepted = 0
+    for trial in range(200):
+        V = 64
+        y = np.round(rng.normal(0.0, 3.0, V) * 16) / 16
+        x = np.round(rng.normal(0.0, 3.0, V) * 16) / 16
+        g = int(np.argmax(y))
+        d = np.round(rng.normal(-1.0, 1.0) * 32) / 32
+        x[g] = y[g] - d                      # the greedy token: y - x = d
+        other = (g + 1 + int(rng.integers(V - 1))) % V
+        x[other] = y[other] - d              # a different token with the same difference
+        X = np.broadcast_to(x, (1, 1, V)).copy()
+        Y = np.broadcast_to(y, (1, 1, V)).copy()
+        tok = lambda z: np.array([[z]])
+        sc = paths.score_position(X, Y, None, [1], tok(other), tok(g), tok(g))
+        la = sc["log_alpha"][0, 0]
+        assert la[0] == la[2], trial          # bitwise equal
+        assert sc["accept_flag"][0, 0], trial
+        accepted += 1
+    assert accepted == 200
