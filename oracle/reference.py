@@ -132,7 +132,8 @@ def run_positions(X, Y, d2t, depth, positions, N, L, params, seed=0, offset=0,
             if lam > 0.0:
                 for s in range(N):
                     for i in range(int(depth[k][s])):
-                        g[s, i, omega[s, i]] += kl_grad[s, i]
+                        members = omega[s, i] >= 0
+                        g[s, i, omega[s, i][members]] += kl_grad[s, i][members]
             out["grad"].append(g.reshape(N * L, Vd))
     res = {k: np.concatenate(v) for k, v in acc.items()}
     for k in ("tok_draft", "tok_target", "tok_greedy", "exp_accept_len"):

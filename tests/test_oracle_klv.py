@@ -115,3 +115,34 @@ def test_position_average_over_paths_with_ragged_depths():
     assert L_row[1, 1] == 0.0 and np.all(omega[1, 1:] == -1)
     # each live row's gradient coefficients sum to zero (q_hat and p_hat both sum to one)
     np.testing.assert_allclose(dx.sum(axis=-1), 0.0, atol=1e-14)
+
+
+def test_non_finite_target_logits_are_not_members():
+    """A row with fewer than K finite mapped target logits: Omega holds only
+    the finite ones (a token of zero target probability is not among the
+    target's likely tokens), so the term equals the term with K = their
+    number; with none the term is 0."""
+    rng = np.random.default_rng(3)
+    x = rng.normal(0, 2, size=30)
+    y = np.full(30, -np.inf)
+    finite = np.array([4, 11, 17, 25])
+    y[finite] = [1.0, 2.5, 2.5, -0.5]
+    om, p_hat, q_hat, L = klv.row_term(x, y, 10)
+    assert list(om) == [11, 17, 4, 25]
+    om4, p4, q4, L4 = klv.row_term(x[finite], y[finite], 4)
+    np.testing.assert_allclose(p_hat, p4, rtol=1e-15)
+    np.testing.assert_allclose(q_hat, q4, rtol=1e-15)
+    assert L == L4
+    # brute force: q renormalised over the four finite members only
+    b = x[[11, 17, 4, 25]]
+    q_ref = np.exp(b) / np.exp(b).sum()
+    np.testing.assert_allclose(q_hat, q_ref, rtol=1e-13)
+    om0, _, _, L0 = klv.row_term(x, np.full(30, -np.inf), 10)
+    assert om0.size == 0 and L0 == 0.0
+    # per position: the members' slots hold the indices, the rest -1 and 0
+    X = x.reshape(1, 1, 30)
+    Y = y.reshape(1, 1, 30)
+    L_row, omega, dx, KL = klv.position_terms(X, Y, None, [1], 10)
+    assert list(omega[0, 0]) == [11, 17, 4, 25] + [-1] * 6
+    assert np.all(dx[0, 0, 4:] == 0.0) and abs(dx[0, 0, :4].sum()) < 1e-15
+    assert KL == L
