@@ -523,6 +523,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_lm_fwd(LmFwdArgs a) {
 }
 
 // Inverse of the draft->target map: inv[t] = v where d2t[v] = t, else -1.
+// The map must be injective: a second draft index claiming a target slot
+// finds it taken (compare-and-swap against the fill value) and reports
+// VSD_DEVERR_MAP_DUPLICATE instead of overwriting it.
 __global__ void k_lm_inv_fill(int32_t* inv, int Vt) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t < Vt) inv[t] = -1;
@@ -536,7 +539,7 @@ __global__ void k_lm_inv_scatter(const int32_t* d2t, int Vd, int Vt, int32_t* in
     report_error(err, VSD_DEVERR_MAP_RANGE);
     return;
   }
-  inv[t] = v;
+  if (atomicCAS(inv + t, -1, v) != -1) report_error(err, VSD_DEVERR_MAP_DUPLICATE);
 }
 
 // Dot product of two bf16 rows of length H (H % 8 == 0), one wavefront; the
@@ -615,6 +618,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
   const bf16_t* ht = static_cast<const bf16_t*>(a.Ht) + r * a.H;
   const bf16_t* Wd = static_cast<const bf16_t*>(a.Wd);
   const bf16_t* Wt = static_cast<const bf16_t*>(a.Wt);
+  const float gap = lse_gap(pmraw, pt, a.inv_tp, qmraw, qt, a.inv_tq);
   float lqv[3], lav[3];
 #pragma unroll
   for (int f = 0; f < 3; ++f) {
@@ -633,7 +637,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     const float xz = wave_dot(hd, Wd + (int64_t)z * a.H, a.H, lane);
     const float yz = wave_dot(ht, Wt + (int64_t)zt * a.H, a.H, lane);
     lqv[f] = (xz - qmraw) * a.inv_tq - qt;
-    lav[f] = fminf(0.0f, (yz - pmraw) * a.inv_tp - pt - lqv[f]);
+    lav[f] = log_alpha_of(xz, yz, a.inv_tq, a.inv_tp, gap);
   }
   if (lane < 3) {
     a.la[r * 3 + lane] = lane == 0 ? lav[0] : lane == 1 ? lav[1] : lav[2];

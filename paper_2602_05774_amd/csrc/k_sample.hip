@@ -495,13 +495,14 @@ __global__ __launch_bounds__(256) void k_sample(SampleArgs a) {
     const float pmraw = fmaxf(s.p_mraw[0], s.p_mraw[1]);
     const float pt = (log2f(ps) - fmaf(pmraw, cp2, -pmc)) * kLn2;
     const int z = lane == 0 ? s.d.idx : lane == 1 ? s.t.idx : s.g.idx;
+    const float gap = lse_gap(pmraw, pt, a.inv_tp, s.q_mraw, qt, a.inv_tq);
     float lqv = 0.0f, lav = 0.0f;
     if ((uint32_t)z < (uint32_t)a.Vd) {
       const int32_t zt = MAPPED ? a.d2t[z] : z;
       if ((uint32_t)zt < (uint32_t)a.Vt) {
-        lqv = (load1(X + z) - s.q_mraw) * a.inv_tq - qt;
-        const float lpv = (load1(Y + zt) - pmraw) * a.inv_tp - pt;
-        lav = fminf(0.0f, lpv - lqv);
+        const float xz = load1(X + z);
+        lqv = (xz - s.q_mraw) * a.inv_tq - qt;
+        lav = log_alpha_of(xz, load1(Y + zt), a.inv_tq, a.inv_tp, gap);
       }
     }
     a.la[r * 3 + lane] = lav;

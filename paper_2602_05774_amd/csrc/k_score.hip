@@ -214,6 +214,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   }
   const float lse_q = q.mraw * a.inv_tq + q.tail;
   const float lse_p = p.mraw * a.inv_tp + p.tail;
+  const float gap = lse_gap(p.mraw, p.tail, a.inv_tp, q.mraw, q.tail, a.inv_tq);
   if (lane >= a.fam_lo && lane < a.fam_hi) {  // lane f gathers family f
     const int32_t z = a.tok[lane][r];
     float lq = 0.0f, la = 0.0f;
@@ -224,9 +225,9 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
       if ((uint32_t)zt >= (uint32_t)a.Vt) {
         report_error(a.err, VSD_DEVERR_MAP_RANGE);
       } else {
-        lq = (load1(X + z) - q.mraw) * a.inv_tq - q.tail;
-        const float lp = (load1(Y + zt) - p.mraw) * a.inv_tp - p.tail;
-        la = fminf(0.0f, lp - lq);
+        const float xz = load1(X + z);
+        lq = (xz - q.mraw) * a.inv_tq - q.tail;
+        la = log_alpha_of(xz, load1(Y + zt), a.inv_tq, a.inv_tp, gap);
       }
     }
     a.la[r * 3 + lane] = la;

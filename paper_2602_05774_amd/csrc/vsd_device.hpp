@@ -152,6 +152,25 @@ __device__ __forceinline__ void store1(bf16_t* p, float v) {
   *p = __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
+// log alpha = min(0, log p(z) - log q(z)) (Eq. acc) of a token with draft
+// logit x and target logit y, grouped as (y/T_p - x/T_q) - gap with the row
+// constant gap = lse_p - lse_q.  At temperatures that are powers of two the
+// first difference is exact for bf16 logits, so tokens of one row with equal
+// y/T_p - x/T_q (common on bf16 grids) get bitwise equal values and the
+// oracle gate sees their tie exactly (equality accepts).
+__device__ __forceinline__ float log_alpha_of(float x, float y, float inv_tq, float inv_tp, float gap) {
+#pragma clang fp contract(off)
+  return fminf(0.0f, (y * inv_tp - x * inv_tq) - gap);
+}
+
+// gap = lse_p - lse_q from each log-sum-exp's raw maximum m and tail t (lse =
+// m/T + t): the maxima are logit values, so their tempered difference is
+// exact wherever y/T_p - x/T_q is, and only the small tails round.
+__device__ __forceinline__ float lse_gap(float pm, float pt, float inv_tp, float qm, float qt, float inv_tq) {
+#pragma clang fp contract(off)
+  return (pm * inv_tp - qm * inv_tq) + (pt - qt);
+}
+
 // Index of the calling wavefront within its workgroup, as a wavefront-uniform
 // (scalar) value: everything derived from it (row indices, row pointers,
 // Philox counter words) then lives in scalar registers.
