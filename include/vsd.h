@@ -138,7 +138,7 @@
  *   vsd_sample_paths does not accept fused sources (it has no workspace);
  *   vsd_sample_score_paths draws and scores, vsd_score_paths scores given
  *   tokens.  The map d2t, when given, must be injective (it is inverted on
- *   the device).  The workspace (vsd_score_workspace_bytes with the same
+ *   the device; a duplicate entry sets VSD_DEVERR_MAP_DUPLICATE).  The workspace (vsd_score_workspace_bytes with the same
  *   dims) then also holds per-slice partial row statistics.
  *   Backward: grad->grad_logits (bf16, row stride dims->ld_draft, a multiple
  *   of 8 >= v_draft) receives g as defined at vsd_weighted_loss_bwd, and
@@ -153,8 +153,12 @@
  *   The paper's KL variant (Eq. klv) adds a token-level distillation term
  *   over the K target tokens of highest probability.  Per live row r, with
  *   y_v = Y[r][d2t[v]] over the draft vocabulary:
- *     Omega_r  = the K draft indices with the largest y_v (equal values: the
- *                smaller index first), in that order;
+ *     Omega_r  = the K draft indices with the largest finite y_v (equal
+ *                values: the smaller index first), in that order; a row
+ *                with fewer than K finite y_v (entries of zero target
+ *                probability, y_v = -inf) has that many members, its
+ *                kl_idx / kl_grad slots past them hold -1 / 0 (none: the
+ *                row's term is 0);
  *     p_hat(v) = exp(y_v/T_p) / sum_{u in Omega_r} exp(y_u/T_p),
  *     q_hat(v) = exp(X[r][v]/T_q) / sum_{u in Omega_r} exp(X[r][u]/T_q);
  *     kl_row[r] = - sum_{v in Omega_r} p_hat(v) log q_hat(v).
@@ -216,7 +220,11 @@ enum {
   VSD_DEVERR_NONE = 0,
   VSD_DEVERR_TOKEN_RANGE = 1, /* token outside [-1, v_draft) or -1 on a live slot */
   VSD_DEVERR_MAP_RANGE = 2,   /* d2t entry outside [0, v_target) */
-  VSD_DEVERR_DEPTH_RANGE = 3  /* valid_depth entry outside [1, L] */
+  VSD_DEVERR_DEPTH_RANGE = 3, /* valid_depth entry outside [1, L] */
+  VSD_DEVERR_MAP_DUPLICATE = 4 /* two d2t entries name the same target token
+                                  (detected where the map is inverted: the KL
+                                  term, the fused LM head's draws,
+                                  verification) */
 };
 
 typedef enum vsd_dtype { VSD_F32 = 0, VSD_BF16 = 1 } vsd_dtype;

@@ -15,7 +15,8 @@ VSD_OK = 0
 STATUS_NAMES = {0: "VSD_OK", 1: "VSD_ERR_NULL_POINTER", 2: "VSD_ERR_INVALID_SHAPE",
                 3: "VSD_ERR_INVALID_VALUE", 4: "VSD_ERR_MISALIGNED", 5: "VSD_ERR_MAP_REQUIRED",
                 6: "VSD_ERR_UNSUPPORTED", 7: "VSD_ERR_WORKSPACE", 8: "VSD_ERR_HIP"}
-DEVERR_NAMES = {0: "none", 1: "token out of range", 2: "map entry out of range", 3: "depth out of range"}
+DEVERR_NAMES = {0: "none", 1: "token out of range", 2: "map entry out of range", 3: "depth out of range",
+                4: "duplicate map entry"}
 
 VSD_F32, VSD_BF16 = 0, 1
 VSD_GRAD_BASIC, VSD_GRAD_ARW, VSD_GRAD_ARW_CAR = 0, 1, 2

@@ -9,7 +9,8 @@
 // the front in order and raises the threshold.  An element below the
 // threshold is worse than K known elements, so it cannot be in the final top
 // K: the result is exact.  After finish() the K best are at the front of the
-// buffer, in order.  Values must not be -inf (sentinel of empty slots).
+// buffer, in order.  -inf marks empty slots: a -inf offer never becomes an
+// entry.
 // Every call must be made by all 64 lanes of the wavefront.
 #pragma once
 
@@ -193,8 +194,11 @@ struct WaveTopK {
 // q_hat (from y / T_p and X[v] / T_q) are renormalised over the K, the row
 // term -sum p_hat log q_hat goes to *row_out (lane 0) and the gradient
 // coefficients gscale (q_hat - p_hat) with the indices to idx_out / grad_out.
-// Slots past the entries found (only NaN logits leave fewer than K) get index
-// -1 and coefficient 0; an index is read from X only if it lies in [0, Vd).
+// Only finite values become entries (a -inf offer is dropped at the next
+// compaction), so a row with fewer than K finite mapped target logits has
+// fewer than K entries: the distributions are renormalised over those, and
+// the slots past them get index -1 and coefficient 0.  An index is read from
+// X only if it lies in [0, Vd).
 template <typename T>
 __device__ void kl_row_term(const WaveTopK& tk, const T* X, int Vd, float inv_tq, float inv_tp, float gscale,
                             int32_t* idx_out, float* grad_out, float* row_out, int lane) {

@@ -195,10 +195,11 @@ def _src(t):
 
 
 def sample_paths(prob, X, Y, d2t=None, valid_depth=None, temp_draft=1.0, temp_target=1.0,
-                 seed=0, offset=0, device_error=None):
+                 seed=0, offset=0, device_error=None, tokens=None):
     """E-step draws: tokens of the draft proposal, target correction and greedy
-    reference families ([R] int32 each, -1 on masked rows).  Materialised
-    logits only: the fused LM head draws through sample_score_paths."""
+    reference families ([R] int32 each, -1 on masked rows; written into
+    `tokens`, three int32 [R] tensors, when given).  Materialised logits
+    only: the fused LM head draws through sample_score_paths."""
     lib = _lib.load()
     if isinstance(X, LmHead) or isinstance(Y, LmHead):
         raise ValueError("sample_paths takes logits; draw from LmHead sources with sample_score_paths")
@@ -207,7 +208,12 @@ def sample_paths(prob, X, Y, d2t=None, valid_depth=None, temp_draft=1.0, temp_ta
     _check_i32("d2t", d2t, prob.v_draft)
     _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
     dev = X.device
-    toks = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    if tokens is None:
+        toks = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    else:
+        toks = list(tokens)
+        for t in toks:
+            _check_i32("tokens", t, prob.R)
     if device_error is None:
         device_error = torch.zeros(1, dtype=torch.int32, device=dev)
     dims = _dims(prob, X, Y)

@@ -5,16 +5,27 @@ Bars (floating point against the float64 oracle):
   log-domain values (log alpha, log q, log-sum-exp)   |d| <= 1e-3 * max(1, |ref|)
   linear values (survival, E[A], o', beta, zeta, a, b,
                  per-position loss, total loss)       |d| <= 1e-3 * |ref| + 1e-6
-  gradients, fp32 output                              |d| <= 2e-3
-  gradients, bf16 output                              |d| <= 2e-3, or <= one bf16
-                                                      ulp of ref where |ref| >= 1
+  gradients                                           tests/grad_bar.py: |d| <= 2e-3,
+                                                      and |d| <= 2^-8 |ref| (bf16) plus
+                                                      the float32 error of the
+                                                      summands, element by element,
+                                                      and a 1e-2 relative L2 per row
 Integers (tokens, oracle flags) are compared exactly.  A flag may differ only
 where the oracle's float64 margin between the compared log-survivals is below
 1e-4 * max(1, |LS of the greedy path|) (a near-tie that float32 accumulation can
-resolve either way); such positions are reported and left out of the float
+resolve either way); such positions are reported, capped (at most
+max(2, 0.2 %) of the compared positions) and left out of the float
 comparisons that follow from the flags.
+
+oracle_positions_threaded runs the oracle over many positions (every one of a
+batch by default), the inputs copied to the host in chunks of positions, the
+positions of a chunk spread over a thread pool (numpy releases the
+interpreter lock inside its array operations, so the threads run in
+parallel; no process is forked from one that holds the GPU).
 """
+import os
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import torch
@@ -22,8 +33,10 @@ import torch
 import paper_2602_05774_amd as vsd
 from oracle import reference
 from synth.gen import rows_to_host
+from tests import grad_bar
 
 TIE_REL = 1e-4
+TIE_CAP_FRAC = 2e-3
 SENTINEL = -7.0   # pre-filled into gradient buffers: padding columns must keep it
 
 
@@ -87,7 +100,67 @@ def oracle_positions(cfg, inp, positions, params=None, tokens=None, want_grad=Tr
              kl_weight=params.kl_weight, kl_topk=params.kl_topk)
     ora = reference.run_positions(X, Y, d2t, depth, list(positions), cfg.N, cfg.L, p, seed=cfg.philox_seed,
                                   offset=cfg.philox_offset, tokens=tok, want_grad=want_grad)
+    if want_grad:  # for the gradient bar's summand magnitudes
+        ora["X_rows"] = X
+    ora["_params"] = p
     return rows, ora
+
+
+def oracle_params(params):
+    return dict(temp_draft=params.temp_draft, temp_target=params.temp_target, w_base=params.w_base,
+                car_tau=params.car_tau, mode=params.mode, car_input=params.car_input, loss_scale=params.loss_scale,
+                kl_weight=params.kl_weight, kl_topk=params.kl_topk)
+
+
+def oracle_threads():
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _merge(parts):
+    """Concatenate per-group oracle results (every array along axis 0)."""
+    out = {}
+    for k, v in parts[0].items():
+        if isinstance(v, np.ndarray) and v.ndim >= 1:
+            out[k] = np.concatenate([p[k] for p in parts])
+        elif k == "loss_total":
+            out[k] = sum(p[k] for p in parts)
+        else:
+            out[k] = v
+    return out
+
+
+def oracle_positions_threaded(cfg, inp, positions=None, params=None, want_grad=False, chunk_positions=128,
+                              group=2, threads=None):
+    """Yield (positions, rows, oracle result) over `positions` (default: every
+    position of the batch), chunk by chunk; with want_grad the result also
+    holds the gradient rows and the host copy of X (for the gradient bar)."""
+    params = params or params_of(cfg)
+    p = oracle_params(params)
+    threads = threads or oracle_threads()
+    positions_all = list(range(cfg.P)) if positions is None else list(positions)
+    d2t = None if inp["d2t"] is None else inp["d2t"].cpu().numpy()
+    depth_all = None if inp["valid_depth"] is None else inp["valid_depth"].reshape(-1, cfg.N).cpu().numpy()
+    per = cfg.N * cfg.L
+    with ThreadPoolExecutor(threads) as ex:
+        for c0 in range(0, len(positions_all), chunk_positions):
+            chunk = positions_all[c0:c0 + chunk_positions]
+            rows = (np.asarray(chunk)[:, None] * per + np.arange(per)[None]).reshape(-1)
+            X = rows_to_host(inp["X"], rows, cfg.v_draft)
+            Y = rows_to_host(inp["Y"], rows, cfg.v_target)
+
+            def run(k0, chunk=chunk, X=X, Y=Y):
+                k1 = min(len(chunk), k0 + group)
+                depth = None if depth_all is None else depth_all[chunk[k0:k1]]
+                return reference.run_positions(X[k0 * per:k1 * per], Y[k0 * per:k1 * per], d2t, depth, chunk[k0:k1],
+                                               cfg.N, cfg.L, p, seed=cfg.philox_seed, offset=cfg.philox_offset,
+                                               want_grad=want_grad)
+
+            ora = _merge(list(ex.map(run, range(0, len(chunk), group))))
+            if want_grad:
+                ora["X_rows"] = X
+            ora["_params"] = p
+            del Y
+            yield chunk, rows, ora
 
 
 def _lin_ok(got, ref):
@@ -98,13 +171,10 @@ def _log_ok(got, ref):
     return np.abs(got - ref) <= 1e-3 * np.maximum(1.0, np.abs(ref))
 
 
-def _bf16_ulp(x):
-    e = np.floor(np.log2(np.maximum(np.abs(x), 1e-30)))
-    return np.exp2(e - 7)
-
-
-def compare(cfg, gpu, rows, ora, positions, check_grad=True, label=""):
-    """Assert GPU == oracle on the given rows/positions; returns a summary dict."""
+def compare(cfg, gpu, rows, ora, positions, check_grad=True, label="", tie_cap=None):
+    """Assert GPU == oracle on the given rows/positions; returns a summary dict.
+    tie_cap: the most positions allowed a near-tie flag difference (default
+    max(2, 0.2 % of the positions))."""
     N, L = cfg.N, cfg.L
     npos = len(positions)
     sc = gpu["score"]
@@ -128,6 +198,8 @@ def compare(cfg, gpu, rows, ora, positions, check_grad=True, label=""):
     for k in np.nonzero(val_g != val_o)[0]:
         assert tie_cor[k] or acc_g[k] != acc_o[k], f"{label} valid flag mismatch at row {rows[k]}"
         tied_pos.add(k // (N * L))
+    cap = max(2, int(np.ceil(TIE_CAP_FRAC * npos))) if tie_cap is None else tie_cap
+    assert len(tied_pos) <= cap, f"{label}: {len(tied_pos)} near-tie positions with differing flags (cap {cap})"
     keep_rows = np.array([k // (N * L) not in tied_pos for k in range(npos * N * L)])
     keep_pos = np.array([p not in tied_pos for p in range(npos)])
     keep_paths = np.repeat(keep_pos, N)
@@ -155,26 +227,57 @@ def compare(cfg, gpu, rows, ora, positions, check_grad=True, label=""):
         ok = ok | ~np.broadcast_to(keep, ok.shape)
         bad = np.argwhere(~ok)
         assert bad.size == 0, f"{label} {name}: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {got[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
-        worst[name] = float(np.max(np.abs(got - ref))) if got.size else 0.0
+        kept = np.broadcast_to(keep, ok.shape)
+        worst[name] = float(np.max(np.abs(got - ref)[kept])) if kept.any() else 0.0
     # 4. gradient (exact context: also the one on the rows along z')
+    margins = {}
     for name in ("grad", "grad_corr"):
         if check_grad and name in ora and name in gpu:
-            worst[name] = check_grad_rows(cfg, gpu[name], ora[name], rows, keep_rows, f"{label} {name}")
-    return dict(worst=worst, near_tie_positions=sorted(tied_pos))
+            mag = grad_magnitude(cfg, ora, name)
+            worst[name], margins[name] = check_grad_rows(cfg, gpu[name], ora[name], rows, keep_rows,
+                                                         f"{label} {name}", mag)
+    return dict(worst=worst, near_tie_positions=sorted(tied_pos), grad_margin=margins)
 
 
-def check_grad_rows(cfg, grad, ref, rows, keep_rows, label):
+def grad_magnitude(cfg, ora, name):
+    """(m, rel) of the gradient bar for the oracle's `name` gradient
+    ("grad": the rows along z~; "grad_corr": exact context, along z')."""
+    p = ora["_params"]
+    rows_n = len(ora["coef_a"])
+    zero = np.zeros(rows_n)
+    none = np.full(rows_n, -1)
+    if "X_ctx" in ora:  # exact context: each part on its own rows
+        f = 0 if name == "grad" else 1
+        X, lse = ora["X_ctx"][f], ora["lse_q_ctx"][:, f]
+        a = ora["coef_a"] if f == 0 else zero
+        b = zero if f == 0 else ora["coef_b"]
+        td = ora["tok_draft"] if f == 0 else none
+        tt = none if f == 0 else ora["tok_target"]
+    else:
+        X, lse, a, b, td, tt = (ora["X_rows"], ora["lse_q"], ora["coef_a"], ora["coef_b"], ora["tok_draft"],
+                                ora["tok_target"])
+    kl_idx = ora.get("kl_idx") if (name == "grad" and p.get("kl_weight", 0.0) > 0.0) else None
+    return grad_bar.summand_magnitude(X, lse, a, b, td, tt, p["temp_draft"], p["loss_scale"], kl_idx=kl_idx,
+                                      kl_weight=p.get("kl_weight", 0.0), n_paths=cfg.N)
+
+
+def check_grad_rows(cfg, grad, ref, rows, keep_rows, label, mag):
     """Assert a device gradient [R, ld] equals the oracle's on `rows` under the
-    gradient bar; returns the largest error."""
+    gradient bar (tests/grad_bar.py); returns the largest error and the
+    largest fraction of the element bound used."""
     g = grad.index_select(0, torch.as_tensor(rows, device=grad.device))[:, :cfg.v_draft]
     g = g.float().cpu().numpy()
-    err = np.abs(g - ref)
-    if grad.dtype == torch.bfloat16:
-        ok = (err <= 2e-3) | ((np.abs(ref) >= 1.0) & (err <= _bf16_ulp(ref)))
-    else:
-        ok = err <= 2e-3
-    ok |= ~keep_rows[:, None]
-    bad = np.argwhere(~ok)
-    assert bad.size == 0, f"{label}: {len(bad)} outside the bar, first {tuple(bad[0])}: gpu {g[tuple(bad[0])]} oracle {ref[tuple(bad[0])]}"
-    return float(err[keep_rows].max()) if keep_rows.any() else 0.0
+    bf16 = grad.dtype == torch.bfloat16
+    m, rel = mag
+    bad_elem, bad_row = grad_bar.violations(g, ref, m, rel, bf16)
+    bad_elem &= keep_rows[:, None]
+    bad_row &= keep_rows
+    bad = np.argwhere(bad_elem)
+    assert bad.size == 0, (f"{label}: {len(bad)} elements outside the bar, first {tuple(bad[0])}: "
+                           f"gpu {g[tuple(bad[0])]!r} oracle {ref[tuple(bad[0])]!r}")
+    assert not bad_row.any(), f"{label}: {int(bad_row.sum())} rows outside the relative L2 bar"
+    if not keep_rows.any():
+        return 0.0, 0.0
+    err = np.abs(g - ref)[keep_rows]
+    return float(err.max()), grad_bar.margin_used(g[keep_rows], ref[keep_rows], m[keep_rows], rel[keep_rows], bf16)
 

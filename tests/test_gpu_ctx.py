@@ -113,6 +113,8 @@ def check_rollout(cfg, params, label):
     ora = reference.run_positions(Xo.reshape(3, -1, cfg.v_draft), Yo.reshape(3, -1, cfg.v_target),
                                   None if inp["d2t"] is None else inp["d2t"].cpu().numpy(), depth, positions, cfg.N,
                                   cfg.L, _oracle_params(cfg, params), tokens=toks_o)
+    ora["X_ctx"] = Xo.reshape(3, -1, cfg.v_draft)  # the gradient bar's summand magnitudes
+    ora["_params"] = _oracle_params(cfg, params)
     rows = np.arange(prob.R)
     gpu = dict(tokens=toks, score=sc, grad=grads[0], grad_corr=grads[1], err_sample=err)
     summary = compare(cfg, gpu, rows, ora, positions, label=label)

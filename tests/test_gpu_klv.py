@@ -83,3 +83,58 @@ def test_vocabulary_of_exactly_k_tokens(fused):
     cfg = scaled("C2", B=1, T=2, N=3, L=2, v_draft=16, v_target=16)
     inp = make_inputs(cfg, DEV)
     check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.8, kl_topk=16), "V=K KL", fused)
+
+
+@FUSED
+def test_rows_with_fewer_than_k_finite_target_logits(fused):
+    """A vocabulary mask on every other position: each of its rows keeps 5
+    random draft tokens (and their mapped target entries) finite, the rest
+    -inf on both sides, so with K = 10 the top-K set holds the 5 finite
+    entries only (slots past them: index -1, coefficient 0)."""
+    cfg = scaled("C3", name="C3kinf", B=1, T=4, v_draft=3000, v_target=9000)
+    inp = make_inputs(cfg, DEV)
+    g = torch.Generator(device="cpu").manual_seed(77)
+    per = cfg.N * cfg.L
+    d2t = inp["d2t"].long().cpu()
+    rows = [r for pos in range(1, cfg.P, 2) for r in range(pos * per, (pos + 1) * per)]
+    mask = torch.ones(len(rows), cfg.v_draft, dtype=torch.bool)
+    for k in range(len(rows)):
+        mask[k, torch.randperm(cfg.v_draft, generator=g)[:5]] = False
+    idx = torch.as_tensor(rows, device=DEV)
+    X = inp["X"].index_select(0, idx)
+    Y = inp["Y"].index_select(0, idx)
+    X[:, :cfg.v_draft] = X[:, :cfg.v_draft].masked_fill(mask.to(DEV), -float("inf"))
+    ymask = torch.zeros(len(rows), Y.shape[1], dtype=torch.bool)
+    ymask[:, d2t] = mask
+    Y = Y.masked_fill(ymask.to(DEV), -float("inf"))
+    inp["X"].index_copy_(0, idx, X)
+    inp["Y"].index_copy_(0, idx, Y)
+    summary = check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.5, kl_topk=10), "C3s KL masked",
+                       fused)
+    sc_idx = run_step(cfg, inp, params_of(cfg, kl_weight=0.5, kl_topk=10), fused=fused)["score"].kl_idx
+    got = sc_idx.view(cfg.R, 10)[idx].cpu()
+    assert bool((got[:, 5:] == -1).all()) and bool((got[:, :5] >= 0).all())
+    assert summary is not None
+
+
+def test_duplicate_map_entry_is_reported():
+    """A map that sends two draft tokens to one target token: every call that
+    inverts the map reports VSD_DEVERR_MAP_DUPLICATE (4)."""
+    cfg = scaled("C3", name="dup", B=1, T=1, N=2, L=2, v_draft=600, v_target=2000)
+    inp = make_inputs(cfg, DEV)
+    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+    bad = inp["d2t"].clone()
+    bad[7] = bad[300]
+    params = params_of(cfg, kl_weight=0.5, kl_topk=4)
+    smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], None, 1.0, 1.0, 0, 0)
+    toks = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
+    sc = vsd.score_paths(prob, params, inp["X"], inp["Y"], *toks, bad, None)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 4
+    sc_ok = vsd.score_paths(prob, params, inp["X"], inp["Y"], *toks, inp["d2t"], None)
+    torch.cuda.synchronize()
+    assert int(sc_ok.device_error.item()) == 0
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    vsd.verify_paths(prob, params_of(cfg), inp["X"], inp["Y"], sc_ok, bad, None, 0, 0, device_error=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 4

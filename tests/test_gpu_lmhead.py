@@ -15,7 +15,7 @@ LM head (exact float64 logits handed to the per-position oracle).
 * Sizes: a small batch checked on every position (two row tiles, the last
   ragged; vocabularies that span several slices and end mid-tile), edge cases
   (identity map, ragged depth, temperature, one k-step, odd vocabulary), and
-  the full 49 152 x 4096 shape on sampled positions.
+  the full 49 152 x 4096 shape on 32 complete positions.
 """
 import numpy as np
 import pytest
@@ -65,6 +65,8 @@ def _oracle(cfg, inp, positions, params, tokens=None):
                                seed=cfg.philox_seed, offset=cfg.philox_offset, tokens=tokens)
     gaps = lmhead.key_gaps(ora["X"], ora["Y"], d2t, rows, params.temp_draft, params.temp_target,
                            cfg.philox_seed, cfg.philox_offset)
+    ora["X_rows"] = ora["X"]  # exact logits: the gradient bar's summand magnitudes
+    ora["_params"] = p
     return rows, ora, gaps
 
 
@@ -231,6 +233,11 @@ def test_device_errors_are_reported():
     smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, bad_map, None, 0, 0)
     torch.cuda.synchronize()
     assert int(sc.device_error.item()) == 2
+    dup_map = inp["d2t"].clone()
+    dup_map[5] = dup_map[400]
+    smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, dup_map, None, 0, 0)
+    torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 4
     depth = torch.full((cfg.B, cfg.T, cfg.N), 1, dtype=torch.int32, device=DEV)
     depth[0, 1, 1] = cfg.L + 1
     smp, sc = vsd.sample_score_paths(prob, params, Xs, Ys, inp["d2t"], depth, 0, 0)
@@ -238,8 +245,14 @@ def test_device_errors_are_reported():
     assert int(sc.device_error.item()) == 3
 
 
-def test_full_size_sampled_positions():
+def test_full_size_32_positions():
+    """The full 49 152 x 4096 shape; 32 complete positions spread over the
+    batch (the first and the last among them) through the float64 oracle."""
     cfg = CONFIGS["C5"]
     inp = make_inputs(cfg, DEV)
-    positions = [0, 517, cfg.P - 1]
-    check_lmhead(cfg, inp, positions, label="C5 full")
+    rng = np.random.default_rng(55)
+    positions = sorted(set([0, cfg.P - 1] + list(rng.choice(np.arange(1, cfg.P - 1), 30, replace=False))))
+    assert len(positions) == 32
+    summary = check_lmhead(cfg, inp, positions, label="C5 full")
+    log(f"[C5 full] near-tie positions {summary['near_tie_positions']}, gradient bound used "
+        f"{summary['grad_margin']}")

@@ -4,8 +4,8 @@
   vsd_weighted_loss_bwd with their given tokens;
 * C1 in full, and C2/C3/C4-recipe batches small enough for the oracle to check
   every position (several 512-element tiles per row and a ragged tail);
-* C2, C3 and C4 at full size, in the launch configuration bench.py times,
-  checked on sampled positions plus properties that hold at any size;
+* (C2, C3 and C4 at full size, every position: tests/test_gpu_full_batch.py,
+  which also uses the properties that hold at any size defined here);
 * edge cases: one path / depth one, vocabularies that are not a multiple of 8
   (padded rows), vocabularies smaller than a wavefront, equal draft and target
   (everything accepted), constant logits (every greedy choice a tie),
@@ -158,23 +158,6 @@ def _batch_properties(cfg, inp, gpu):
     idx = torch.arange(0, R, max(1, R // 512), device=DEV)
     gs = gpu["grad"].index_select(0, idx)[:, :cfg.v_draft].float().sum(dim=1)
     assert torch.all(gs.abs() < 0.05), float(gs.abs().max())
-
-
-@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
-def test_full_size_sampled_positions(name):
-    cfg = CONFIGS[name]
-    log(f"[parity] {name} full size R={cfg.R}")
-    inp = make_inputs(cfg, DEV)
-    gpu = run_step(cfg, inp)
-    assert int(gpu["err_sample"].item()) == 0 and int(gpu["score"].device_error.item()) == 0
-    _batch_properties(cfg, inp, gpu)
-    rng = np.random.default_rng(123)
-    positions = sorted(set([0, cfg.P - 1] + list(rng.choice(cfg.P, 6, replace=False))))
-    rows, ora = oracle_positions(cfg, inp, positions)
-    res = compare(cfg, gpu, rows, ora, positions, label=name)
-    log(f"[parity] {name} positions {positions} worst {res['worst']} near-ties {res['near_tie_positions']}")
-    del inp, gpu
-    torch.cuda.empty_cache()
 
 
 # ------------------------------------------------------------ edge cases
@@ -355,26 +338,3 @@ def test_fused_edge_cases(name):
     assert int(gpu["score"].device_error.item()) == 0
     rows, ora = oracle_positions(cfg, inp, list(range(cfg.P)))
     compare(cfg, gpu, rows, ora, list(range(cfg.P)), label=f"fused {name}")
-
-
-@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
-def test_fused_full_size_sampled_positions(name):
-    cfg = CONFIGS[name]
-    log(f"[fused] {name} full size R={cfg.R}")
-    inp = make_inputs(cfg, DEV)
-    gpu = run_step(cfg, inp, fused=True)
-    assert int(gpu["score"].device_error.item()) == 0
-    _batch_properties(cfg, inp, gpu)
-    prob = problem_of(cfg)
-    smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"], cfg.temp_draft,
-                           cfg.temp_target, cfg.philox_seed, cfg.philox_offset)
-    torch.cuda.synchronize()
-    for a, b in zip(gpu["tokens"], smp[:3]):
-        assert torch.equal(a, b), "fused and three-call tokens differ"
-    rng = np.random.default_rng(321)
-    positions = sorted(set([0, cfg.P - 1] + list(rng.choice(cfg.P, 6, replace=False))))
-    rows, ora = oracle_positions(cfg, inp, positions)
-    res = compare(cfg, gpu, rows, ora, positions, label=f"fused {name}")
-    log(f"[fused] {name} positions {positions} worst {res['worst']}")
-    del inp, gpu
-    torch.cuda.empty_cache()
