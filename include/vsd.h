@@ -55,7 +55,9 @@
  *   arguments (vsd_dims, vsd_params, vsd_src, vsd_score_out, vsd_grad) are
  *   HOST pointers read during the call only.  The library never allocates or
  *   frees memory, never synchronises, never reads device memory on the host
- *   and keeps no mutable global state other than a thread-local error string.
+ *   and keeps no mutable global state other than a thread-local error string
+ *   and, for vsd_sample_score_paths_static, its static scratch array and that
+ *   array's address per device.
  *   All work is enqueued on `hip_stream` (a hipStream_t; NULL = default
  *   stream) and is complete only when that stream is.
  *   Logit rows: row r starts at element r*ld of its array; the array holds R
@@ -357,6 +359,34 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
                                   int32_t* tok_greedy, const vsd_score_out* out,
                                   void* workspace, size_t workspace_bytes,
                                   void* hip_stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * vsd_sample_score_paths with the library's own scratch in place of the
+ * caller's workspace.  Same arguments, outputs and results otherwise (the
+ * same kernels run).
+ *   Scratch: a static device array of VSD_STATIC_SCRATCH_BYTES (64 MiB) that
+ *   every device the library runs on holds from the library's first use there
+ *   until the process ends; the call uses the one of the calling thread's
+ *   current device (hip_stream must belong to that device).  Its address is
+ *   looked up once per device (hipGetSymbolAddress); the call itself
+ *   allocates nothing.
+ *   Limit: dims whose vsd_score_workspace_bytes() exceeds
+ *   VSD_STATIC_SCRATCH_BYTES return VSD_ERR_WORKSPACE before anything is
+ *   launched (the five reference workloads need at most 62 MiB).
+ *   Sharing: every call on a device uses that device's one array, which keeps
+ *   the last call's contents; nothing in it needs to start at zero (each call
+ *   writes every region before reading it).  Calls that overlap on one device
+ *   (different streams, or threads without ordering between them) race on the
+ *   scratch and their outputs are undefined: order them on one stream. */
+#define VSD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+vsd_status vsd_sample_score_paths_static(const vsd_dims* dims, const vsd_params* params,
+                                         const vsd_src* draft, const vsd_src* target,
+                                         const int32_t* d2t, const int32_t* valid_depth,
+                                         uint64_t seed, uint32_t offset,
+                                         int32_t* tok_draft, int32_t* tok_target,
+                                         int32_t* tok_greedy, const vsd_score_out* out,
+                                         void* hip_stream);
 
 /* Gradient of loss_scale * sum_x L_x with respect to the draft logits (the
  * derivative of Eq. advance, with o', beta, zeta and the tokens held fixed):

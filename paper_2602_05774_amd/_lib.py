@@ -56,7 +56,8 @@ class VsdGrad(ctypes.Structure):
 
 _lib = None
 
-EXPORTS = ("vsd_sample_paths", "vsd_score_paths", "vsd_sample_score_paths", "vsd_weighted_loss_bwd",
+EXPORTS = ("vsd_sample_paths", "vsd_score_paths", "vsd_sample_score_paths", "vsd_sample_score_paths_static",
+           "vsd_weighted_loss_bwd",
            "vsd_sample_step", "vsd_score_paths_ctx", "vsd_weighted_loss_bwd_ctx", "vsd_verify_paths",
            "vsd_score_workspace_bytes", "vsd_status_string", "vsd_last_error", "vsd_abi_version")
 
@@ -81,6 +82,10 @@ def load():
                                            ctypes.c_uint64, ctypes.c_uint32, c_vp, c_vp, c_vp,
                                            P(VsdScoreOut), c_vp, ctypes.c_size_t, c_vp]
     lib.vsd_sample_score_paths.restype = c_i32
+    lib.vsd_sample_score_paths_static.argtypes = [P(VsdDims), P(VsdParams), P(VsdSrc), P(VsdSrc), c_vp, c_vp,
+                                                  ctypes.c_uint64, ctypes.c_uint32, c_vp, c_vp, c_vp,
+                                                  P(VsdScoreOut), c_vp]
+    lib.vsd_sample_score_paths_static.restype = c_i32
     lib.vsd_weighted_loss_bwd.argtypes = [P(VsdDims), P(VsdParams), P(VsdSrc), c_vp, c_vp, c_vp, c_vp,
                                           c_vp, c_vp, c_vp, P(VsdGrad), c_vp, c_vp]
     lib.vsd_weighted_loss_bwd.restype = c_i32

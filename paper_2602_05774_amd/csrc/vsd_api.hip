@@ -4,11 +4,19 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
 #include "vsd_topk.hpp"
+
+// Scratch of vsd_sample_score_paths_static: one copy of this array lives on
+// every device the library's code object is loaded on, until the process
+// ends.  Host code never passes the array's name to a kernel (on the host it
+// is a stand-in, not a device address): static_scratch() looks up this
+// device's address once and every launch takes that pointer.
+static __device__ __align__(256) unsigned char scratch[VSD_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -197,12 +205,18 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
 }
 
 // Validation of the score outputs and workspace shared by the scoring calls.
-vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const void* workspace,
-                           size_t workspace_bytes) {
+vsd_status check_score_out_fields(const vsd_score_out* out) {
   if (out == nullptr) return fail(VSD_ERR_NULL_POINTER, "out is NULL");
   if (out->lse_draft == nullptr || out->coef_a == nullptr || out->coef_b == nullptr)
     return fail(VSD_ERR_NULL_POINTER, "out->lse_draft, coef_a and coef_b are required");
   if (out->device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "out->device_error is NULL");
+  return VSD_OK;
+}
+
+vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const void* workspace,
+                           size_t workspace_bytes) {
+  vsd_status st = check_score_out_fields(out);
+  if (st != VSD_OK) return st;
   const WorkspaceLayout wl = workspace_layout(dims);
   if (workspace == nullptr || workspace_bytes < wl.total)
     return fail(VSD_ERR_WORKSPACE, "workspace of %zu bytes required, %zu given", wl.total,
@@ -388,6 +402,29 @@ vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_
   return VSD_OK;
 }
 
+// Device address of `scratch` on the calling thread's current device, looked
+// up with that device current on the first call there and kept per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+vsd_status static_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(VSD_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr) return fail(VSD_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return VSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -506,11 +543,12 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
   return ok();
 }
 
-vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
-                                  const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
-                                  uint64_t seed, uint32_t offset, int32_t* tok_draft, int32_t* tok_target,
-                                  int32_t* tok_greedy, const vsd_score_out* out, void* workspace,
-                                  size_t workspace_bytes, void* hip_stream) {
+// The body of vsd_sample_score_paths, shared with its static-scratch variant.
+static vsd_status sample_score_impl(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                                    const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                                    uint64_t seed, uint32_t offset, int32_t* tok_draft, int32_t* tok_target,
+                                    int32_t* tok_greedy, const vsd_score_out* out, void* workspace,
+                                    size_t workspace_bytes, void* hip_stream) {
   vsd_status st = check_dims(dims);
   if (st != VSD_OK) return st;
   if ((st = check_params(params)) != VSD_OK) return st;
@@ -576,6 +614,41 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
   st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s);
   if (st != VSD_OK) return st;
   return ok();
+}
+
+vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                                  const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                                  uint64_t seed, uint32_t offset, int32_t* tok_draft, int32_t* tok_target,
+                                  int32_t* tok_greedy, const vsd_score_out* out, void* workspace,
+                                  size_t workspace_bytes, void* hip_stream) {
+  return sample_score_impl(dims, params, draft, target, d2t, valid_depth, seed, offset, tok_draft, tok_target,
+                           tok_greedy, out, workspace, workspace_bytes, hip_stream);
+}
+
+vsd_status vsd_sample_score_paths_static(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,
+                                         const vsd_src* target, const int32_t* d2t, const int32_t* valid_depth,
+                                         uint64_t seed, uint32_t offset, int32_t* tok_draft, int32_t* tok_target,
+                                         int32_t* tok_greedy, const vsd_score_out* out, void* hip_stream) {
+  // everything the shared body checks except the workspace, before the
+  // device is asked for the scratch's address
+  vsd_status st = check_dims(dims);
+  if (st != VSD_OK) return st;
+  if ((st = check_params(params)) != VSD_OK) return st;
+  if ((st = check_sources(dims, draft, target)) != VSD_OK) return st;
+  if ((st = check_map(dims, d2t)) != VSD_OK) return st;
+  if (tok_draft == nullptr || tok_target == nullptr || tok_greedy == nullptr)
+    return fail(VSD_ERR_NULL_POINTER, "token outputs must not be NULL");
+  if ((st = check_score_out_fields(out)) != VSD_OK) return st;
+  if ((st = check_kl_out(dims, params, out)) != VSD_OK) return st;
+  const size_t need = workspace_layout(dims).total;
+  if (need > VSD_STATIC_SCRATCH_BYTES)
+    return fail(VSD_ERR_WORKSPACE,
+                "these dims need %zu bytes of workspace; the static scratch holds %zu (use vsd_sample_score_paths)",
+                need, (size_t)VSD_STATIC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = static_scratch(&ws)) != VSD_OK) return st;
+  return sample_score_impl(dims, params, draft, target, d2t, valid_depth, seed, offset, tok_draft, tok_target,
+                           tok_greedy, out, ws, VSD_STATIC_SCRATCH_BYTES, hip_stream);
 }
 
 vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft,

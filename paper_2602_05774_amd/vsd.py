@@ -319,6 +319,35 @@ def sample_score_paths(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, o
     return SampleResult(tokens[0], tokens[1], tokens[2], out.device_error), out
 
 
+def sample_score_paths_static(prob, params, X, Y, d2t=None, valid_depth=None, seed=0, offset=0,
+                              out: Optional[ScoreResult] = None, tokens=None):
+    """sample_score_paths on the library's static device scratch instead of
+    a caller workspace (vsd_sample_score_paths_static: for callers that
+    cannot allocate; calls that overlap on one device race on the scratch).
+    With `out` and `tokens` given, the call allocates nothing."""
+    lib = _lib.load()
+    _check_src("X", X, prob, prob.v_draft)
+    _check_src("Y", Y, prob, prob.v_target)
+    _check_i32("d2t", d2t, prob.v_draft)
+    _check_i32("valid_depth", valid_depth, prob.B * prob.T * prob.N)
+    dev = X.device
+    if out is None:
+        out = alloc_score_outputs(prob, dev, kl_topk=params.kl_topk if params.kl_weight > 0 else 0)
+    if tokens is None:
+        tokens = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+    for name, t in zip(("tok_draft", "tok_target", "tok_greedy"), tokens):
+        _check_i32(name, t, prob.R)
+    dims = _dims(prob, X, Y)
+    names = [f[0] for f in _lib.VsdScoreOut._fields_]
+    so = _lib.VsdScoreOut(*[None if getattr(out, k) is None else getattr(out, k).data_ptr() for k in names])
+    pr = params.c()
+    _lib.check(lib.vsd_sample_score_paths_static(ctypes.byref(dims), ctypes.byref(pr), ctypes.byref(_src(X)),
+                                                 ctypes.byref(_src(Y)), _ptr(d2t), _ptr(valid_depth), int(seed),
+                                                 int(offset), _ptr(tokens[0]), _ptr(tokens[1]), _ptr(tokens[2]),
+                                                 ctypes.byref(so), _stream(dev)))
+    return SampleResult(tokens[0], tokens[1], tokens[2], out.device_error), out
+
+
 def weighted_loss_bwd(prob, params, X, lse_draft, tok_draft, tok_target, coef_a, coef_b,
                       grad=None, device_error=None, kl_idx=None, kl_grad=None, weight_grad=False):
     """Gradient of loss_scale * sum_x L_x with respect to the draft logits

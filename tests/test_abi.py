@@ -313,3 +313,35 @@ def test_verify_validation(lib):
     assert verify(dims=mapped, d2t=FAKE) == 7                        # workspace required with a map
     assert verify(dims=mapped, d2t=FAKE, ws=FAKE + 8, nbytes=1 << 30) == 4
     assert verify(dims=_dims(ld_draft=999)) == 2
+
+
+def test_static_scratch_variant_validates_before_touching_the_device(lib):
+    """vsd_sample_score_paths_static checks every argument, then the size
+    its dims need against VSD_STATIC_SCRATCH_BYTES, before it asks the device
+    for the scratch's address."""
+    src = _lib.VsdSrc(FAKE, None, None)
+    out = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+
+    def call(dims=None, params=None, toks=(FAKE, FAKE, FAKE), out=out, d2t=None):
+        dims = dims or _dims()
+        params = params or _params()
+        return lib.vsd_sample_score_paths_static(ctypes.byref(dims), ctypes.byref(params), ctypes.byref(src),
+                                                 ctypes.byref(src), d2t, None, 0, 0, *toks, ctypes.byref(out), None)
+    assert call(dims=_dims(N=0)) == 2
+    assert call(params=_params(car_tau=0.0)) == 3
+    assert call(toks=(FAKE, None, FAKE)) == 1
+    assert call(out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=None, device_error=FAKE)) == 1
+    assert call(dims=_dims(v_target=2000, ld_target=2000)) == 5
+    # dims whose workspace exceeds the static scratch
+    limit = 64 << 20
+    B = 1
+    while True:
+        d = _dims(B=B, T=512, N=8, L=6, v_draft=32000, v_target=128256, dtype=_lib.VSD_BF16, ld_draft=32000,
+                  ld_target=128256)
+        n = ctypes.c_size_t(0)
+        assert lib.vsd_score_workspace_bytes(ctypes.byref(d), ctypes.byref(n)) == 0
+        if n.value > limit:
+            break
+        B *= 2
+    assert call(dims=d, d2t=FAKE) == 7
+    assert "static scratch" in lib.vsd_last_error().decode()
