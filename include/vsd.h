@@ -224,9 +224,8 @@ enum {
   VSD_DEVERR_MAP_RANGE = 2,   /* d2t entry outside [0, v_target) */
   VSD_DEVERR_DEPTH_RANGE = 3, /* valid_depth entry outside [1, L] */
   VSD_DEVERR_MAP_DUPLICATE = 4 /* two d2t entries name the same target token
-                                  (detected where the map is inverted: the KL
-                                  term, the fused LM head's draws,
-                                  verification) */
+                                  (detected where the map is inverted: the
+                                  fused LM head's draws, verification) */
 };
 
 typedef enum vsd_dtype { VSD_F32 = 0, VSD_BF16 = 1 } vsd_dtype;

@@ -321,9 +321,9 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       if (FUSED && !MAPPED) lp.add8_lazy(y, ymax, f.c2);
       greedy(base, y, 8, ymax);
       if (DRAW) f.draw8(base, y, ymax, it == 0);
-      if (KL) {
+      if (KL) {  // a slice whose largest mapped value is below the top-K threshold offers nothing
         if (it == 0) tk.seed_lane_max(ymax, lane);
-        tk.offer8(y, base, 0xFFu, same, lane);
+        if (it == 0 || __ballot(ymax >= tk.thv) != 0ull) tk.offer8(y, base, 0xFFu, same, lane);
       }
       if (next) {
         if (MAPPED)

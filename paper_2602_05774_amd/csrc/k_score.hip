@@ -16,8 +16,8 @@
 // With the top-K renormalised KL term on (VSD (KL) variant, Eq. klv),
 // k_score_rows also selects, while it streams the target row, the K mapped
 // target tokens with the largest logits (exact wavefront top-K, vsd_topk.hpp;
-// a mapped column is found by a bit mask and its draft index by the inverse
-// map), then forms p_hat and q_hat renormalised over them, the row's term
+// the mapped values are gathered through the map next to the block being
+// streamed), then forms p_hat and q_hat renormalised over them, the row's term
 // -sum p_hat log q_hat and its gradient coefficients; k_combine adds the
 // per-position average over paths to the loss.
 #include "vsd_device.hpp"
@@ -99,25 +99,37 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
   return RowLse{mraw, (log2f(s) - delta) * kLn2};
 }
 
-// row_lse of the target row, also offering every mapped column to a
-// wavefront top-K (value = raw target logit, index = its draft index).  Four
-// chunks are in flight per lane as in row_lse; a chunk's 8 elements are
-// offered only when some lane's largest mapped value reaches the threshold
-// (one ballot per chunk once the threshold has risen).
+// row_lse of the target row, also selecting the K mapped target logits of
+// largest value (wavefront top-K; value = raw target logit, index = its
+// draft index).  Four chunks are in flight per lane as in row_lse, so one
+// iteration streams a 2048-column block.  With a map, the same iteration
+// offers draft chunk it = 512 indices: each lane gathers Y[d2t[v]] for
+// v = 512 it + 64 k + lane, k < 8.  For an ascending map (about four target
+// columns per draft index) those columns lie in the block just streamed, so
+// the gathers find their lines in L2.  Draft chunks left when the stream ends
+// (a map onto fewer columns than 4 per index) are offered after it.  Without
+// a map the streamed values themselves are offered.  Only values at or above
+// the top-K threshold are ever appended, so a slice whose largest value is
+// below it in every lane offers nothing: one ballot decides.  Map entries
+// outside [0, Vt) are reported and offer nothing.
 template <typename T, bool MAPPED>
-__device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const uint32_t* mask,
-                               const int32_t* inv) {
+__device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const int32_t* d2t, int Vd,
+                               int32_t* err) {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
   constexpr int U = 4;
   constexpr int step = 8 * kWave;
-  auto idx_of = [&](int col) { return MAPPED ? inv[col] : col; };
-  auto bits_of = [&](int base, int nvalid) -> uint32_t {
-    if (nvalid <= 0) return 0u;
-    const uint32_t keep = nvalid >= 8 ? 0xFFu : ((1u << nvalid) - 1u);
-    return MAPPED ? ((mask[base >> 5] >> (base & 31)) & keep) : keep;
+  bool seeded = false;
+  auto offer = [&](const float (&x)[8], int base, uint32_t bits, float vmax, auto idx_of) {
+    if (!seeded) {  // the threshold from the lanes' largest offered values of the first slice
+      seeded = true;
+      tk.seed_lane_max(vmax, lane);
+      tk.offer8(x, base, bits, idx_of, lane);
+      return;
+    }
+    if (__ballot(vmax >= tk.thv) == 0ull) return;
+    tk.offer8(x, base, bits, idx_of, lane);
   };
-  auto fold = [&](int base, const float (&x)[8], uint32_t bits, bool first = false) {
-    const float cm = max8(x);
+  auto lse8 = [&](const float (&x)[8], float cm) {
     if (cm > mraw) {
       const float nmc = cm * c;
       s *= __builtin_amdgcn_exp2f(mc - nmc);
@@ -126,26 +138,62 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) s += __builtin_amdgcn_exp2f(fmaf(x[k], c, -mc));
-    if (first) {  // the threshold from the lanes' largest offered values of the first slice
-      float best = -INFINITY;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) best = ((bits >> k) & 1u) ? fmaxf(best, x[k]) : best;
-      tk.seed_lane_max(best, lane);
-    }
-    tk.offer8(x, base, bits, idx_of, lane);
   };
+  // Draft chunk dc (512 indices; lane-strided: k-th value of a lane is draft
+  // index 512 dc + 64 k + lane) is offered from gathered raw values.  Its map
+  // entries are loaded one iteration ahead and its gathers are issued right
+  // after the stream loads of the iteration that offers it, so the
+  // log-sum-exp work of the block covers their latency.
+  const int ndc = MAPPED ? (Vd + step - 1) / step : 0;
+  int dc = 0;
+  uint32_t tmap[8];
+  T graw[8];
+  bool map_bad = false;
+  auto load_map = [&](int d) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int v = d * step + k * kWave + lane;
+      tmap[k] = v < Vd ? (uint32_t)d2t[v] : 0xFFFFFFFFu;
+    }
+  };
+  auto gather = [&]() {  // map entries outside [0, Vt) offer nothing (reported)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const bool ok = tmap[k] < (uint32_t)V;
+      map_bad |= !ok && tmap[k] != 0xFFFFFFFFu;
+      graw[k] = row[ok ? tmap[k] : 0u];
+    }
+  };
+  auto offer_gathered = [&](int d) {
+    float y[8];
+    uint32_t bits = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const bool ok = tmap[k] < (uint32_t)V;
+      y[k] = ok ? load1(&graw[k]) : -INFINITY;
+      bits |= ok ? (1u << k) : 0u;
+    }
+    const int base = d * step + lane;
+    offer(y, 0, bits, max8(y), [&](int k) { return base + k * kWave; });
+  };
+  if (MAPPED && ndc > 0) load_map(0);
   int chunk = 0;
   for (; chunk + U * step <= V; chunk += U * step) {
     float x[U][8];
-    uint32_t bits[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) load8(row + chunk + u * step + lane * 8, x[u]);
+    const bool g = MAPPED && dc < ndc;
+    if (g) gather();
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int base = chunk + u * step + lane * 8;
-      load8(row + base, x[u]);
-      bits[u] = bits_of(base, 8);
+      const float cm = max8(x[u]);
+      lse8(x[u], cm);
+      if (!MAPPED) offer(x[u], chunk + u * step + lane * 8, 0xFFu, cm, [](int col) { return col; });
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) fold(chunk + u * step + lane * 8, x[u], bits[u], chunk == 0 && u == 0);
+    if (g) {
+      offer_gathered(dc);
+      if (++dc < ndc) load_map(dc);
+    }
   }
   for (; chunk < V; chunk += step) {
     const int base = chunk + lane * 8;
@@ -157,8 +205,19 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
 #pragma unroll
       for (int k = 0; k < 8; ++k) x[k] = k < nvalid ? load1(row + base + k) : -INFINITY;
     }
-    fold(base, x, bits_of(base, nvalid));
+    const float cm = max8(x);
+    lse8(x, cm);
+    if (!MAPPED) {
+      const uint32_t bits = nvalid <= 0 ? 0u : nvalid >= 8 ? 0xFFu : (1u << nvalid) - 1u;
+      offer(x, base, bits, cm, [](int col) { return col; });
+    }
   }
+  for (; MAPPED && dc < ndc;) {  // draft chunks past the streamed blocks
+    gather();
+    offer_gathered(dc);
+    if (++dc < ndc) load_map(dc);
+  }
+  if (map_bad) report_error(err, VSD_DEVERR_MAP_RANGE);
   wave_lse2(mc, s);
   mraw = wave_max(mraw);
   const float delta = fmaf(mraw, c, -mc);
@@ -208,7 +267,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   if (KL) {
     const int slot = wave_id();
     tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
-    p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.map_mask, a.inv);
+    p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.d2t, a.Vd, a.err);
   } else {
     p = row_lse(Y, a.Vt, a.inv_tp * kLog2e, lane);
   }
@@ -396,26 +455,10 @@ hipError_t launch_rows_t(const ScoreRowArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Bit mask of the mapped target columns (bit t of word t/32), from the
-// inverse map.
-__global__ void k_map_mask(const int32_t* inv, int Vt, uint32_t* mask) {
-  const int w = blockIdx.x * blockDim.x + threadIdx.x;
-  if (w * 32 >= Vt) return;
-  uint32_t m = 0;
-  for (int b = 0; b < 32 && w * 32 + b < Vt; ++b) m |= (inv[w * 32 + b] >= 0 ? 1u : 0u) << b;
-  mask[w] = m;
-}
-
 }  // namespace
 
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s) {
   return bf16 ? launch_rows_t<bf16_t>(a, s) : launch_rows_t<float>(a, s);
-}
-
-hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s) {
-  const int words = (Vt + 31) / 32;
-  hipLaunchKernelGGL(k_map_mask, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, s, inv, Vt, mask);
-  return hipGetLastError();
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {

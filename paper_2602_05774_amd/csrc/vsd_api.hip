@@ -179,12 +179,12 @@ vsd_status hip_fail(hipError_t e, const char* what) {
 }
 
 struct WorkspaceLayout {
-  size_t la, lq, loss, klrow, inv, mask, part, total;
+  size_t la, lq, loss, klrow, inv, part, total;
 };
 
 // la [R,3], lq [R,3], loss [P], KL row terms [R] fp32; the inverse map
-// [v_target] int32 and the mapped-column bit mask [ceil(v_target/32)]; fused
-// LM head also the slice partials [R, nslice_t + nslice_d].
+// [v_target] int32 (fused LM head draws, verification); fused LM head also
+// the slice partials [R, nslice_t + nslice_d].
 WorkspaceLayout workspace_layout(const vsd_dims* d) {
   const int64_t R = rows_of(d);
   const int64_t P = (int64_t)d->B * d->T;
@@ -194,8 +194,7 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   w.loss = w.lq + align_up((size_t)R * 3 * sizeof(float));
   w.klrow = w.loss + align_up((size_t)P * sizeof(float));
   w.inv = w.klrow + align_up((size_t)R * sizeof(float));
-  w.mask = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
-  w.part = w.mask + align_up((size_t)((d->v_target + 31) / 32) * sizeof(uint32_t));
+  w.part = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
   w.total = w.part;
   if (d->hidden_dim > 0) {
     const size_t nsl = (size_t)(vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
@@ -247,16 +246,8 @@ vsd_status score_rows(const vsd_dims* dims, const vsd_params* params, const void
                       const WorkspaceLayout& wl, float* la, float* lq, float** kl_row_out, hipStream_t s) {
   float* kl_row = nullptr;
   hipError_t e;
-  if (kl_on(params)) {
+  if (kl_on(params))
     kl_row = out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
-    if (d2t != nullptr) {
-      int32_t* inv = reinterpret_cast<int32_t*>(ws + wl.inv);
-      e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
-      if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
-      e = vsd::launch_map_mask(inv, dims->v_target, reinterpret_cast<uint32_t*>(ws + wl.mask), s);
-      if (e != hipSuccess) return hip_fail(e, "k_map_mask launch");
-    }
-  }
   *kl_row_out = kl_row;
   for (int f = 0; f < (ctx ? 3 : 1); ++f) {
     vsd::ScoreRowArgs ra{};
@@ -282,8 +273,6 @@ vsd_status score_rows(const vsd_dims* dims, const vsd_params* params, const void
     ra.inv_tp = 1.0f / params->temp_target;
     if (kl_on(params) && f == 0) {
       ra.kl_k = params->kl_topk;
-      ra.map_mask = reinterpret_cast<const uint32_t*>(ws + wl.mask);
-      ra.inv = reinterpret_cast<const int32_t*>(ws + wl.inv);
       ra.kl_idx = out->kl_idx;
       ra.kl_grad = out->kl_grad;
       ra.kl_row = kl_row;

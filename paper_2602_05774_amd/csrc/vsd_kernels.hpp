@@ -88,8 +88,6 @@ struct ScoreRowArgs {
   int32_t fam_lo, fam_hi;    // families [fam_lo, fam_hi) gathered on these rows (columns of la / lq)
   // top-K renormalised KL term (kl_k > 0 turns it on)
   int32_t kl_k;
-  const uint32_t* map_mask;  // [ceil(Vt/32)] bit t: target column t is mapped (with d2t)
-  const int32_t* inv;        // [Vt] draft index of target column t, -1 unmapped (with d2t)
   int32_t* kl_idx;           // [R, kl_k]
   float* kl_grad;            // [R, kl_k]
   float* kl_row;             // [R]
@@ -238,7 +236,6 @@ hipError_t launch_sample_step(const SampleStepArgs& a, bool bf16, hipStream_t s)
 hipError_t launch_verify(const VerifyArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_score_rows(const ScoreRowArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
-hipError_t launch_map_mask(const int32_t* inv, int Vt, uint32_t* mask, hipStream_t s);
 hipError_t launch_loss_total(const float* loss_pos, int32_t P, float scale, float* out, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, bool bf16, hipStream_t s);
 

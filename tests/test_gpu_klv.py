@@ -117,24 +117,26 @@ def test_rows_with_fewer_than_k_finite_target_logits(fused):
     assert summary is not None
 
 
-def test_duplicate_map_entry_is_reported():
-    """A map that sends two draft tokens to one target token: every call that
-    inverts the map reports VSD_DEVERR_MAP_DUPLICATE (4)."""
-    cfg = scaled("C3", name="dup", B=1, T=1, N=2, L=2, v_draft=600, v_target=2000)
+@FUSED
+def test_duplicate_map_entry(fused):
+    """A map that sends two draft tokens to one target token.  The KL term
+    gathers through the map, so both draft tokens carry that target logit
+    and the top-K orders them by draft index, exactly as the oracle does;
+    verification inverts the map and reports VSD_DEVERR_MAP_DUPLICATE (4)."""
+    cfg = scaled("C3", name="dup", B=1, T=2, v_draft=600, v_target=2000)
     inp = make_inputs(cfg, DEV)
-    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
     bad = inp["d2t"].clone()
-    bad[7] = bad[300]
-    params = params_of(cfg, kl_weight=0.5, kl_topk=4)
-    smp = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], None, 1.0, 1.0, 0, 0)
-    toks = (smp.tok_draft, smp.tok_target, smp.tok_greedy)
-    sc = vsd.score_paths(prob, params, inp["X"], inp["Y"], *toks, bad, None)
-    torch.cuda.synchronize()
-    assert int(sc.device_error.item()) == 4
-    sc_ok = vsd.score_paths(prob, params, inp["X"], inp["Y"], *toks, inp["d2t"], None)
-    torch.cuda.synchronize()
-    assert int(sc_ok.device_error.item()) == 0
+    ymax_col = int(inp["Y"][:, :cfg.v_target].float().sum(0).argmax().item())
+    bad[7] = ymax_col    # likely inside every row's top K: the duplicate pair is selected
+    bad[300] = ymax_col
+    inp["d2t"] = bad
+    check_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.5, kl_topk=4), "dup-map KL", fused)
+    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+    smp = vsd.sample_paths(prob, inp["X"], inp["Y"], bad, None, 1.0, 1.0, 0, 0)
+    sc = vsd.score_paths(prob, params_of(cfg), inp["X"], inp["Y"], smp.tok_draft, smp.tok_target, smp.tok_greedy,
+                         bad, None)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
-    vsd.verify_paths(prob, params_of(cfg), inp["X"], inp["Y"], sc_ok, bad, None, 0, 0, device_error=err)
+    vsd.verify_paths(prob, params_of(cfg), inp["X"], inp["Y"], sc, bad, None, 0, 0, device_error=err)
     torch.cuda.synchronize()
+    assert int(sc.device_error.item()) == 0
     assert int(err.item()) == 4
