@@ -84,7 +84,7 @@ def cpu_baseline(cfg, workers, per_worker=8):
     rows = npos * cfg.N * cfg.L
     return {"value": rows / wall, "unit": "path-tokens/s", "cores": workers, "kind": "oracle",
             "sample": f"{npos} positions ({rows} path-tokens) of the {cfg.name} recipe, sample+score+grad, "
-                      f"{workers} worker processes, {wall:.1f} s wall"}
+                      f"{workers} worker processes, {wall:.1f} s wall", **host_cpu_info()}
 
 
 def _oracle_lm_position(k):
@@ -119,7 +119,33 @@ def cpu_baseline_lm(cfg, workers, per_worker=1):
     rows = npos * cfg.N * cfg.L
     return {"value": rows / wall, "unit": "path-tokens/s", "cores": workers, "kind": "oracle",
             "sample": f"{npos} positions ({rows} path-tokens) of the {cfg.name} recipe, float64 LM-head logits + "
-                      f"sample+score+grad, {workers} worker processes, {wall:.1f} s wall"}
+                      f"sample+score+grad, {workers} worker processes, {wall:.1f} s wall", **host_cpu_info()}
+
+
+def host_cpu_info():
+    """The host's logical CPU count, the CPUs this process may run on and the
+    CPU model (from /proc/cpuinfo)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"host_cpus": os.cpu_count(), "usable_cpus": usable, "cpu_model": model}
+
+
+def default_workers():
+    """Worker processes of the oracle timing: the CPUs this process may use,
+    at most 16 (one GPU's share of the host)."""
+    info = host_cpu_info()
+    return max(1, min(16, info["usable_cpus"] or info["host_cpus"] or 1))
 
 
 def copy_calibration(mib, dev):
@@ -213,16 +239,19 @@ def bench_lm_head(cfg, steps, warmup, dev):
         "step_TFLOP/s": tf(fwd_flop + bwd_flop, t_fwd + t_bwd),
         "roofline": {"bound": "mfma", "kernel": "k_lm_fwd (forward call: GEMM tiles + sampling epilogue)",
                      "achieved": tf(fwd_flop, t_fwd), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": tf(fwd_flop, t_fwd) / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
+                     "frac": tf(fwd_flop, t_fwd) / MFMA_BF16_PEAK_TFLOPS,
+                     "traffic": measured_traffic(cfg.name, "lm_fwd")},
     }
     del inp, out, ws, grad
     torch.cuda.empty_cache()
     return res
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
-KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_draw.hpp", "vsd_topk.hpp", "vsd_device.hpp"],
-                  "bwd": ["k_bwd.hip", "vsd_topk.hpp", "vsd_device.hpp"]}
+PROFILE_FILES = [os.path.join(ROOT, "profiles", f) for f in ("hbm_traffic.md", "lm_head_c5.md",
+                                                               "sample_score_valu.md")]
+KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_draw.hpp", "vsd_topk.hpp", "vsd_device.hpp", "vsd_kernels.hpp"],
+                  "bwd": ["k_bwd.hip", "vsd_topk.hpp", "vsd_device.hpp", "vsd_kernels.hpp"],
+                  "lm_fwd": ["k_lmhead.hip", "vsd_device.hpp", "vsd_kernels.hpp"]}
 
 
 def source_hash(kernel):
@@ -235,19 +264,26 @@ def source_hash(kernel):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, kernel):
-    """HBM bytes per launch from the PMC summary in profiles/, or None when no
-    figure exists for this workload and kernel or the kernel changed since."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None
-    for line in open(TRAFFIC_FILE):
-        if line.startswith("traffic:"):
-            rec = json.loads(line[len("traffic:"):])
-            if rec.get("workload") == workload and rec.get("kernel") == kernel:
-                if rec.get("source_hash") != source_hash(kernel):
-                    return None
-                return rec.get("bytes_per_launch")
+def profile_record(tag, workload, kernel):
+    """The machine-readable `tag:` record of a PMC summary in profiles/ for
+    this workload and kernel, or None when there is none or the kernel's
+    sources changed since the counters were taken."""
+    for path in PROFILE_FILES:
+        if not os.path.exists(path):
+            continue
+        for line in open(path):
+            if line.startswith(tag + ":"):
+                rec = json.loads(line[len(tag) + 1:])
+                if rec.get("workload") == workload and rec.get("kernel") == kernel:
+                    return rec if rec.get("source_hash") == source_hash(kernel) else None
     return None
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated) from the PMC
+    summaries in profiles/, or None."""
+    rec = profile_record("traffic", workload, kernel)
+    return None if rec is None else rec.get("bytes_per_launch")
 
 
 def main():
@@ -261,6 +297,7 @@ def main():
     ap.add_argument("--no-lm-head", action="store_true", help="skip the fused LM-head measurement")
     ap.add_argument("--lm-steps", type=int, default=3, help="timed steps of the fused LM-head measurement")
     ap.add_argument("--no-ctx", action="store_true", help="skip the exact-context measurement")
+    ap.add_argument("--no-configs", action="store_true", help="skip the C2 and C4 measurements")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this size first (calibrates PMC byte counters)")
     args = ap.parse_args()
@@ -277,7 +314,7 @@ def main():
 
     base = None
     if not args.no_cpu_baseline:
-        workers = args.cpu_workers or max(1, min(16, os.cpu_count() or 1))
+        workers = args.cpu_workers or default_workers()
         base = cpu_baseline(cfg, workers)
         print(f"[bench] cpu baseline: {base['value']:.1f} {base['unit']} on {base['cores']} cores", flush=True)
 
@@ -408,18 +445,15 @@ def main():
     three_calls = {"ms_per_step": t_step3, "sample_ms": t_sample3, "score_ms": t_score3, "bwd_ms": t_bwd3,
                    "score_GB/s": gbs(ss_bytes, t_score3),
                    "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score3 + t_bwd3) / HBM_PEAK_GBS}
-    # The one-pass sampler is bound by VALU issue (its counters show the SIMDs
-    # issuing at their peak rate): its roofline counts the method's essential
-    # lane operations per live row -- 4 per logit for the two log-sum-exps
-    # (unpack, fma, exp2, add), 40 per Philox4x32-10 call (10 rounds of two
-    # 32x32->64 products and two 3-way XORs; ceil(V_d/4) calls per family, two
-    # families) and 14 per 8-key slice for the candidate bound (largest of 8
-    # values and of 8 Philox words, 4 three-way maxima each; not, shift,
-    # convert, log2, fma, compare).  The backward is bound by HBM.
+    # The essential VALU lane operations of the one-pass sampler per live row
+    # (a model, reported beside the byte roofline): 4 per logit for the two
+    # log-sum-exps (unpack, fma, exp2, add), 40 per Philox4x32-10 call (10
+    # rounds of two 32x32->64 products and two 3-way XORs; ceil(V_d/4) calls
+    # per family, two families) and 14 per 8-key slice for the candidate bound.
     ss_ops = live * (4.0 * (cfg.v_draft + cfg.v_target) + 40.0 * 2 * ((cfg.v_draft + 3) // 4)
                      + 14.0 * 2 * ((cfg.v_draft + 7) // 8))
-    kernels["sample_score"]["valu_lane_ops"] = ss_ops
-    kernels["sample_score"]["TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
+    kernels["sample_score"]["valu_model_lane_ops"] = ss_ops
+    kernels["sample_score"]["valu_model_TOP/s"] = ss_ops / (t_ss * 1e-3) / 1e12
     kl_variant = {"kl_topk": params_kl.kl_topk, "kl_weight": params_kl.kl_weight,
                   "one_pass": {"ms_per_step": t_step_kl1, "path_tokens_per_s": live / (t_step_kl1 * 1e-3),
                                "sample_score_ms": t_ss_kl, "bwd_ms": t_bwd_kl1},
@@ -428,16 +462,28 @@ def main():
                                   "bwd_GB/s": gbs(bwd_bytes, t_bwd_kl),
                                   "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score_kl + t_bwd_kl)
                                   / HBM_PEAK_GBS}}
+    # Roofline of the step's dominant kernel against HBM: its algorithmic
+    # bytes (every live row's draft and target logits read once for the
+    # one-pass sampler; the backward's reads and writes) over its measured
+    # time.  The one-pass sampler also runs close to the VALU issue limit: the
+    # counter-based issue fraction (SQ_INSTS_VALU x 64 lanes over the time,
+    # against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz) comes from its profile
+    # summary when that was taken on the current sources.
     dominant = "sample_score" if t_ss >= t_bwd else "bwd"
     k = kernels[dominant]
+    roof = {"bound": "hbm", "kernel": "k_sample (one-pass sample + score, mapped, bf16)" if dominant == "sample_score"
+            else "k_bwd", "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": k["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name, dominant),
+            "bytes_per_launch": k["bytes"], "ms_per_launch": k["ms"]}
     if dominant == "sample_score":
-        roof = {"bound": "alu", "kernel": "k_sample (one-pass sample + score, mapped, bf16)",
-                "achieved": k["TOP/s"], "peak": VALU_PEAK_TOPS, "unit": "TOP/s (VALU lane-ops)",
-                "frac": k["TOP/s"] / VALU_PEAK_TOPS, "hbm_GB/s": k["GB/s"], "hbm_frac": k["GB/s"] / HBM_PEAK_GBS,
-                "traffic": measured_traffic(cfg.name, dominant)}
-    else:
-        roof = {"bound": "hbm", "kernel": "k_bwd", "achieved": k["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": k["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name, dominant)}
+        roof["valu_model"] = {"lane_ops_per_launch": ss_ops, "achieved_TOP/s": k["valu_model_TOP/s"],
+                              "issue_peak_TOP/s": VALU_PEAK_TOPS, "frac": k["valu_model_TOP/s"] / VALU_PEAK_TOPS}
+        rec = profile_record("valu", cfg.name, dominant)
+        if rec is not None:
+            lane_ops = rec["sq_insts_valu"] * 64.0
+            roof["valu_counters"] = {"sq_insts_valu": rec["sq_insts_valu"],
+                                     "lane_ops_per_s": lane_ops / (k["ms"] * 1e-3),
+                                     "frac_of_issue_peak": lane_ops / (k["ms"] * 1e-3) / (VALU_PEAK_TOPS * 1e12)}
     line = {
         "metric": METRIC, "value": live / (t_step * 1e-3), "unit": "path-tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step, "wall_ms_per_step": wall * 1e3 / args.steps,
@@ -459,11 +505,107 @@ def main():
     line["verification"] = bench_verify(cfg, prob, params, inp, out, ws, timed, dev)
     if not args.no_ctx:
         line["exact_context"] = bench_ctx(cfg, prob, params, inp, ws, timed, live, dev)
+    del inp, X, Y, out, out_kl, ws, grad
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        line["configs"] = {name: bench_config(CONFIGS[name], args.steps, args.warmup, dev)
+                           for name in ("C2", "C4") if name != cfg.name}
     if not args.no_lm_head:
-        del inp, X, Y, out, out_kl, ws, grad
-        torch.cuda.empty_cache()
         line["fused_lm_head"] = bench_lm_head(CONFIGS["C5"], args.lm_steps, 1, dev)
     print(json.dumps(line), flush=True)
+
+
+def time_calls(fn, nev, steps, warmup):
+    """warmup untimed calls, then `steps` timed ones; fn(ev) records nev
+    events on the current stream.  Returns (mean ms between consecutive
+    events, mean ms first to last)."""
+    import torch
+    for _ in range(warmup):
+        fn(None)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
+    for k in range(steps):
+        fn(evs[k])
+    torch.cuda.synchronize()
+    seg = [sum(e[j].elapsed_time(e[j + 1]) for e in evs) / steps for j in range(nev - 1)]
+    return seg, sum(e[0].elapsed_time(e[nev - 1]) for e in evs) / steps
+
+
+def bench_config(cfg, steps, warmup, dev):
+    """The EM step on another workload: the one-pass step (sample + score in
+    one call, then the backward) and the graded score + backward of the three
+    calls, with their HBM fractions (algorithmic bytes: every live row's draft
+    and target logits once for sample + score or score; the backward reads the
+    rows with a or b != 0 and writes every row)."""
+    import torch
+
+    import paper_2602_05774_amd as vsd
+    from synth import make_inputs
+    t0 = time.perf_counter()
+    inp = make_inputs(cfg, dev)
+    torch.cuda.synchronize()
+    print(f"[bench] inputs {cfg.name} generated in {time.perf_counter() - t0:.1f} s", flush=True)
+    prob = vsd.Problem(cfg.B, cfg.T, cfg.N, cfg.L, cfg.v_draft, cfg.v_target)
+    params = vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target)
+    X, Y, d2t, depth = inp["X"], inp["Y"], inp["d2t"], inp["valid_depth"]
+    out = vsd.alloc_score_outputs(prob, dev)
+    ws = torch.empty(vsd.score_workspace_bytes(prob, X.dtype), dtype=torch.uint8, device=dev)
+    grad = torch.empty_like(X)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    tok = [torch.empty(prob.R, dtype=torch.int32, device=dev) for _ in range(3)]
+
+    def one_pass(ev):
+        if ev:
+            ev[0].record()
+        vsd.sample_score_paths(prob, params, X, Y, d2t, depth, cfg.philox_seed, cfg.philox_offset, out=out,
+                               workspace=ws, tokens=tok)
+        if ev:
+            ev[1].record()
+        vsd.weighted_loss_bwd(prob, params, X, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=grad,
+                              device_error=err)
+        if ev:
+            ev[2].record()
+
+    def three_calls(ev):
+        if ev:
+            ev[0].record()
+        vsd.sample_paths(prob, X, Y, d2t, depth, cfg.temp_draft, cfg.temp_target, cfg.philox_seed,
+                         cfg.philox_offset, tokens=tok, device_error=err)
+        if ev:
+            ev[1].record()
+        vsd.score_paths(prob, params, X, Y, tok[0], tok[1], tok[2], d2t, depth, out=out, workspace=ws)
+        if ev:
+            ev[2].record()
+        vsd.weighted_loss_bwd(prob, params, X, out.lse_draft, tok[0], tok[1], out.coef_a, out.coef_b, grad=grad,
+                              device_error=err)
+        if ev:
+            ev[3].record()
+
+    (t_sample3, t_score3, t_bwd3), t_step3 = time_calls(three_calls, 4, steps, warmup)
+    (t_ss, t_bwd), t_step = time_calls(one_pass, 3, steps, warmup)
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+        raise RuntimeError(f"device error reported during the {cfg.name} benchmark")
+    live = prob.R if depth is None else int((tok[0] >= 0).sum().item())
+    nonzero = int(((out.coef_a != 0) | (out.coef_b != 0)).sum().item())
+    es = X.element_size()
+    ss_bytes = live * es * (cfg.v_draft + cfg.v_target)
+    bwd_bytes = nonzero * es * cfg.v_draft + prob.R * es * cfg.v_draft
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    res = {"workload": f"{cfg.name}: B={cfg.B} T={cfg.T} N={cfg.N} L={cfg.L} V_target={cfg.v_target} "
+                       f"V_draft={cfg.v_draft} logits={cfg.dtype} T_q={cfg.temp_draft}"
+                       + (" ragged depths" if cfg.ragged else ""),
+           "path_tokens_per_step": live, "ms_per_step": t_step, "value": live / (t_step * 1e-3),
+           "unit": "path-tokens/s",
+           "one_pass": {"sample_score_ms": t_ss, "bwd_ms": t_bwd, "sample_score_GB/s": gbs(ss_bytes, t_ss),
+                        "bwd_GB/s": gbs(bwd_bytes, t_bwd)},
+           "three_calls": {"ms_per_step": t_step3, "sample_ms": t_sample3, "score_ms": t_score3, "bwd_ms": t_bwd3,
+                           "score_bytes": ss_bytes, "bwd_bytes": bwd_bytes,
+                           "score_GB/s": gbs(ss_bytes, t_score3), "bwd_GB/s": gbs(bwd_bytes, t_bwd3),
+                           "score_bwd_frac_of_hbm_peak": gbs(ss_bytes + bwd_bytes, t_score3 + t_bwd3)
+                           / HBM_PEAK_GBS}}
+    del inp, X, Y, out, ws, grad
+    torch.cuda.empty_cache()
+    return res
 
 
 def hbm_reference(dev, gib=4):
@@ -596,7 +738,7 @@ def main_lm_head(args, cfg):
     """--config C5: the fused LM-head step as the line's own workload."""
     base = None
     if not args.no_cpu_baseline:
-        workers = args.cpu_workers or max(1, min(16, os.cpu_count() or 1))
+        workers = args.cpu_workers or default_workers()
         base = cpu_baseline_lm(cfg, workers)
         print(f"[bench] cpu baseline: {base['value']:.2f} {base['unit']} on {base['cores']} cores", flush=True)
     import torch
