@@ -5,13 +5,16 @@
   * Chain rule: central finite differences of the whole loss (Eq. advance with
     the E-step quantities frozen) as a function of the hidden states equal
     grad_hidden(g, W) with g the oracle's logit gradient.
+  * The same with the top-K renormalised KL term on (Eq. klv): the loss
+    L_x + kl_weight KL_x through the head, with respect to the draft hidden
+    states and the draft weight (the top-K set depends on the target only).
   * The LM-head driver equals the materialised driver on the same logits, and
     its draws are the Gumbel-max draws of those logits.
 """
 import numpy as np
 import pytest
 
-from oracle import lmhead, paths, reference, sampler
+from oracle import klv, lmhead, paths, reference, sampler
 
 
 def test_unit_vector_weights_select_hidden_entries():
@@ -126,3 +129,47 @@ def test_key_gaps_are_top_two_differences():
     kd = np.sort(sampler.gumbel_keys(X, [0], 0, 1.0, 0, 0)[0].astype(np.float64))
     assert gd[0] == pytest.approx(kd[-1] - kd[-2])
     assert gt[0] > 0
+
+
+@pytest.mark.parametrize("wrt", ["hidden", "weight"])
+def test_kl_term_gradients_through_the_head_match_finite_differences(wrt):
+    rng = np.random.default_rng(9)
+    N, L, H, Vd, Vt, K = 3, 2, 4, 8, 13, 3
+    hd = rng.normal(size=(N * L, H))
+    ht = rng.normal(size=(N * L, H))
+    Wd = rng.normal(size=(Vd, H))
+    Wt = rng.normal(size=(Vt, H))
+    d2t = np.sort(rng.permutation(Vt)[:Vd])
+    depth = np.array([L, 1, L])
+    toks = [rng.integers(0, Vd, N * L) for _ in range(3)]
+    lam = 0.6
+    params = dict(temp_draft=0.7, temp_target=1.3, loss_scale=1.5, kl_weight=lam, kl_topk=K)
+    res = lmhead.run_positions(hd, ht, Wd, Wt, d2t, depth[None, :], [0], N, L, params, tokens=toks)
+    Y = res["Y"].reshape(N, L, Vt)
+    t3 = [t.reshape(N, L) for t in toks]
+    frozen = paths.score_position(res["X"].reshape(N, L, Vd), Y, d2t, depth, *t3, params)
+
+    def loss_of(h, W):
+        X = lmhead.logits(h, W).reshape(N, L, Vd)
+        base = paths.loss_from_logits(X, Y, d2t, depth, *t3, frozen, params)
+        kl = klv.position_terms(X, Y, d2t, depth, K, params["temp_draft"], params["temp_target"])[3]
+        return params["loss_scale"] * (base + lam * kl)
+
+    assert loss_of(hd, Wd) == pytest.approx(params["loss_scale"] * res["loss_pos"][0], rel=1e-12)
+    target = hd if wrt == "hidden" else Wd
+    eps = 1e-6
+    fd = np.zeros_like(target)
+    for idx in np.ndindex(target.shape):
+        p_, m_ = target.copy(), target.copy()
+        p_[idx] += eps
+        m_[idx] -= eps
+        lp = loss_of(p_, Wd) if wrt == "hidden" else loss_of(hd, p_)
+        lm = loss_of(m_, Wd) if wrt == "hidden" else loss_of(hd, m_)
+        fd[idx] = (lp - lm) / (2 * eps)
+    got = res["grad_hidden"] if wrt == "hidden" else res["grad_weight"]
+    np.testing.assert_allclose(got, fd, atol=1e-8, rtol=1e-6)
+    # the KL part is not negligible in this case
+    res0 = lmhead.run_positions(hd, ht, Wd, Wt, d2t, depth[None, :], [0], N, L, dict(params, kl_weight=0.0),
+                                tokens=toks)
+    got0 = res0["grad_hidden"] if wrt == "hidden" else res0["grad_weight"]
+    assert np.abs(got - got0).max() > 1e-2
