@@ -169,10 +169,11 @@
  *   loss_pos[x] = L_x + kl_weight KL_x.  The gradient gains
  *   kl_grad[r][k] = loss_scale kl_weight / N (q_hat - p_hat)(Omega_r[k]) / T_q
  *   at draft index kl_idx[r][k] = Omega_r[k]; vsd_weighted_loss_bwd adds
- *   these when given kl_idx and kl_grad.  K <= v_draft.  Computed on
- *   materialised logits by vsd_score_paths and vsd_sample_score_paths (same
- *   outputs, same results); with the fused LM head (hidden_dim > 0) both
- *   return VSD_ERR_UNSUPPORTED when kl_weight > 0.
+ *   these when given kl_idx and kl_grad.  K <= v_draft.  Computed by
+ *   vsd_score_paths and vsd_sample_score_paths (same outputs, same results),
+ *   on materialised logits and with the fused LM head alike; fused, the
+ *   backward adds the sparse gradient to g before g is contracted with the
+ *   weight (so grad_hidden and grad_weight include the term).
  *
  * Exact context (vsd_sample_step, vsd_score_paths_ctx, vsd_weighted_loss_bwd_ctx)
  * ------------------------------------------------------------------------------
@@ -364,7 +365,7 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
  * vsd_sample_score_paths with the library's own scratch in place of the
  * caller's workspace.  Same arguments, outputs and results otherwise (the
  * same kernels run).
- *   Scratch: a static device array of VSD_STATIC_SCRATCH_BYTES (64 MiB) that
+ *   Scratch: a static device array of VSD_STATIC_SCRATCH_BYTES (256 MiB) that
  *   every device the library runs on holds from the library's first use there
  *   until the process ends; the call uses the one of the calling thread's
  *   current device (hip_stream must belong to that device).  Its address is
@@ -372,13 +373,14 @@ vsd_status vsd_sample_score_paths(const vsd_dims* dims, const vsd_params* params
  *   allocates nothing.
  *   Limit: dims whose vsd_score_workspace_bytes() exceeds
  *   VSD_STATIC_SCRATCH_BYTES return VSD_ERR_WORKSPACE before anything is
- *   launched (the five reference workloads need at most 62 MiB).
+ *   launched (the five reference workloads need at most 164 MiB, the
+ *   fused 128k-vocabulary head with its KL lists).
  *   Sharing: every call on a device uses that device's one array, which keeps
  *   the last call's contents; nothing in it needs to start at zero (each call
  *   writes every region before reading it).  Calls that overlap on one device
  *   (different streams, or threads without ordering between them) race on the
  *   scratch and their outputs are undefined: order them on one stream. */
-#define VSD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+#define VSD_STATIC_SCRATCH_BYTES ((size_t)256 << 20)
 vsd_status vsd_sample_score_paths_static(const vsd_dims* dims, const vsd_params* params,
                                          const vsd_src* draft, const vsd_src* target,
                                          const int32_t* d2t, const int32_t* valid_depth,

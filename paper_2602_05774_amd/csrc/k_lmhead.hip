@@ -28,6 +28,7 @@
 // dH_d = g W_d and, when asked for, dW_d = g^T H_d (fp32).
 #include "vsd_device.hpp"
 #include "vsd_kernels.hpp"
+#include "vsd_topk.hpp"
 
 namespace vsd {
 
@@ -52,6 +53,7 @@ static_assert(TM * LDK == TK * LDN, "both operand layouts fill the same stage sl
 static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit the operand buffers");
 static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
 static_assert(2 * kStageNT * 2 <= kLdsBytes, "two direct-loaded NT stages fit");
+static_assert(TM * 4 * (32 + kLmKlM * 8 + 4) <= kLdsBytes, "the slice merge's row states and KL lists fit");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -367,6 +369,49 @@ __device__ __forceinline__ void state_merge(RowState& a, const RowState& b) {
   best_merge(a.gval, a.gidx, b.gval, b.gidx);
 }
 
+// KL term (Eq. klv): the M best (value, draft index) pairs offered to one row
+// segment, ordered as the top-K orders them (larger value first, equal
+// values by the smaller index); n counts the finite values offered, so
+// n > M means some were dropped, every one of them at most v[M - 1].  Only
+// finite values take part (a token of zero target probability is not a
+// member).
+struct KlList {
+  float v[kLmKlM];
+  int i[kLmKlM];
+  int n;
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int j = 0; j < kLmKlM; ++j) {
+      v[j] = -INFINITY;
+      i[j] = 0x7FFFFFFF;
+    }
+    n = 0;
+  }
+  __device__ __forceinline__ static bool beats(float a, int ia, float b, int ib) {
+    return a > b || (a == b && ia < ib);
+  }
+  __device__ __forceinline__ void offer(float x, int idx) {
+    if (!(x > -INFINITY)) return;
+    ++n;
+    if (!beats(x, idx, v[kLmKlM - 1], i[kLmKlM - 1])) return;
+    v[kLmKlM - 1] = x;
+    i[kLmKlM - 1] = idx;
+#pragma unroll
+    for (int j = kLmKlM - 1; j > 0; --j) {  // one bubble pass keeps the list ordered
+      const bool up = beats(v[j], i[j], v[j - 1], i[j - 1]);
+      const float tv = v[j];
+      const int ti = i[j];
+      v[j] = up ? v[j - 1] : tv;
+      i[j] = up ? i[j - 1] : ti;
+      v[j - 1] = up ? tv : v[j - 1];
+      i[j - 1] = up ? ti : i[j - 1];
+    }
+  }
+  // an upper bound of every dropped value (-inf: nothing dropped)
+  __device__ __forceinline__ float bound() const { return n > kLmKlM ? v[kLmKlM - 1] : -INFINITY; }
+};
+
 // Fold eight consecutive columns c .. c+7 of row r (values x; columns past
 // the vocabulary hold -inf) into the running state st of one row segment.
 // Every lane of a wavefront works on the same columns of a different row, so
@@ -376,9 +421,9 @@ __device__ __forceinline__ void state_merge(RowState& a, const RowState& b) {
 // its draft index; the last Philox call (group cg, words cw) is reused, and
 // for an ascending map the draft indices increase along the row, so a new
 // call is made once per four mapped columns.
-template <bool TARGET>
+template <bool TARGET, bool KL>
 __device__ __forceinline__ void fold8(const LmFwdArgs& a, const float (&x)[8], uint32_t r, int c, int nvalid,
-                                      float inv_t, float c2, RowState& st, int& cg, uint4& cw) {
+                                      float inv_t, float c2, RowState& st, int& cg, uint4& cw, KlList& kl) {
   float cm = x[0];
 #pragma unroll
   for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
@@ -390,6 +435,13 @@ __device__ __forceinline__ void fold8(const LmFwdArgs& a, const float (&x)[8], u
   }
 #pragma unroll
   for (int k = 0; k < 8; ++k) st.s += __builtin_amdgcn_exp2f(fmaf(x[k], c2, -st.mc));
+  if (TARGET && KL) {  // the mapped columns' logits, for the row's top-K set
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int vk = k < nvalid ? (a.inv == nullptr ? c + k : a.inv[c + k]) : -1;
+      if (vk >= 0) kl.offer(x[k], vk);
+    }
+  }
   if (!a.sample) return;
   const float off = bound_offset(st.key);
   if (!TARGET) {
@@ -446,7 +498,7 @@ __device__ __forceinline__ void fold8(const LmFwdArgs& a, const float (&x)[8], u
 // hb*128 + rd*64 + l (rounds rd = 0, 1) and columns seg*64 .. +63: each
 // thread carries the state of two row segments across the slice's tiles, and
 // the four segments of a row are merged once, at the end, through LDS.
-template <bool TARGET>
+template <bool TARGET, bool KL>
 __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds, float* T) {
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -459,6 +511,11 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
   const float inv_t = TARGET ? a.inv_tp : a.inv_tq;
   const float c2 = inv_t * kLog2e;
   RowState st[2] = {empty_state(), empty_state()};
+  KlList kl[2];
+  if (TARGET && KL) {
+    kl[0].init();
+    kl[1].init();
+  }
   Core<false> g{static_cast<const bf16_t*>(TARGET ? a.Ht : a.Hd), static_cast<const bf16_t*>(TARGET ? a.Wt : a.Wd),
                 a.H, a.H, row0, a.R, 0, V, a.H};
   for (int tile = t_begin; tile < t_end; ++tile) {
@@ -489,16 +546,47 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
             for (int k = 0; k < 8; ++k)
               if (k >= nvalid) x[k] = -INFINITY;
           }
-          fold8<TARGET>(a, x, (uint32_t)r, c, nvalid, inv_t, c2, st[rd], cg, cw);
+          fold8<TARGET, KL>(a, x, (uint32_t)r, c, nvalid, inv_t, c2, st[rd], cg, cw, kl[rd]);
         }
       }
       __syncthreads();  // the buffers are the next round's (or the next GEMM's)
     }
   }
   RowState* red = reinterpret_cast<RowState*>(T);  // [TM rows][4 segments]
+  LmKlEntry* klred = reinterpret_cast<LmKlEntry*>(red + TM * 4);  // [TM rows][4 segments][kLmKlM]
+  float* klbnd = reinterpret_cast<float*>(klred + TM * 4 * kLmKlM);  // [TM rows][4 segments]
 #pragma unroll
-  for (int rd = 0; rd < 2; ++rd) red[(hb * 128 + rd * 64 + lane) * 4 + seg] = st[rd];
+  for (int rd = 0; rd < 2; ++rd) {
+    const int q = (hb * 128 + rd * 64 + lane) * 4 + seg;
+    red[q] = st[rd];
+    if (TARGET && KL) {
+#pragma unroll
+      for (int j = 0; j < kLmKlM; ++j) klred[q * kLmKlM + j] = LmKlEntry{kl[rd].v[j], kl[rd].i[j]};
+      klbnd[q] = kl[rd].bound();
+    }
+  }
   __syncthreads();
+  if (TARGET && KL && threadIdx.x < TM && row0 + threadIdx.x < a.R) {
+    // the slice's list: the best kLmKlM of its four segments' lists; its
+    // bound covers what the segments dropped and what this merge drops
+    KlList m;
+    m.init();
+    float bnd = -INFINITY;
+#pragma unroll 1
+    for (int sg = 0; sg < 4; ++sg) {
+      const int q = threadIdx.x * 4 + sg;
+      bnd = fmaxf(bnd, klbnd[q]);
+#pragma unroll
+      for (int j = 0; j < kLmKlM; ++j) {
+        const LmKlEntry e = klred[q * kLmKlM + j];
+        m.offer(e.val, e.idx);
+      }
+    }
+    const int64_t rec = (row0 + threadIdx.x) * a.nslice_t + slice;
+#pragma unroll
+    for (int j = 0; j < kLmKlM; ++j) a.kl_part[rec * kLmKlM + j] = LmKlEntry{m.v[j], m.i[j]};
+    a.kl_bound[rec] = fmaxf(bnd, m.bound());
+  }
   if (threadIdx.x < TM && row0 + threadIdx.x < a.R) {
     RowState m = red[threadIdx.x * 4];
 #pragma unroll
@@ -509,6 +597,7 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
   }
 }
 
+template <bool KL>
 __global__ __launch_bounds__(kThreads, 1) void k_lm_fwd(LmFwdArgs a) {
   __shared__ __align__(16) unsigned char smem[kLdsBytes];
   bf16_t* lds = reinterpret_cast<bf16_t*>(smem);
@@ -517,9 +606,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_lm_fwd(LmFwdArgs a) {
   int rt, col;
   tile_of(blockIdx.x, nrt, a.nslice_t + a.nslice_d, rt, col);
   if (col < a.nslice_t)
-    lm_pass<true>(a, (int64_t)rt * TM, col, lds, T);
+    lm_pass<true, KL>(a, (int64_t)rt * TM, col, lds, T);
   else
-    lm_pass<false>(a, (int64_t)rt * TM, col - a.nslice_t, lds, T);
+    lm_pass<false, false>(a, (int64_t)rt * TM, col - a.nslice_t, lds, T);
 }
 
 // Inverse of the draft->target map: inv[t] = v where d2t[v] = t, else -1.
@@ -556,11 +645,51 @@ __device__ __forceinline__ float wave_dot(const bf16_t* x, const bf16_t* y, int 
   return wave_sum(acc);
 }
 
+// Dot product of two bf16 rows of length H by one lane (H % 8 == 0).
+__device__ __forceinline__ float lane_dot(const bf16_t* x, const bf16_t* y, int H) {
+  float acc = 0.0f;
+  for (int k = 0; k < H; k += 8) {
+    float xv[8], yv[8];
+    load8(x + k, xv);
+    load8(y + k, yv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = fmaf(xv[j], yv[j], acc);
+  }
+  return acc;
+}
+
+// The KL term of row r from its members in tk (after finish()): the draft
+// logits at the members by dot products, then the row term (Eq. klv).
+__device__ void lm_kl_row(const LmCombineArgs& a, const WaveTopK& tk, int64_t r, int lane) {
+  const bf16_t* hd = static_cast<const bf16_t*>(a.Hd) + r * a.H;
+  const bf16_t* Wd = static_cast<const bf16_t*>(a.Wd);
+  const int n = min(tk.n, a.kl_k);
+  float x = -INFINITY;
+  for (int k = 0; k < n; ++k) {
+    const int v = tk.bi[k];
+    const float xk = (uint32_t)v < (uint32_t)a.Vd ? wave_dot(hd, Wd + (int64_t)v * a.H, a.H, lane) : -INFINITY;
+    x = lane == k ? xk : x;
+  }
+  const bool mine = lane < n;
+  int v = mine ? tk.bi[lane] : -1;
+  v = (uint32_t)v < (uint32_t)a.Vd ? v : -1;
+  const float y = mine ? tk.bv[lane] : -INFINITY;
+  kl_row_term_xy(mine, v, y, x, a.kl_k, a.inv_tq, a.inv_tp, a.kl_gscale, a.kl_idx + r * a.kl_k,
+                 a.kl_grad + r * a.kl_k, a.kl_row + r, lane);
+}
+
 // Merge the slices of both models, write tokens (sampling) and the row
-// statistics.  One wavefront per row.
+// statistics.  One wavefront per row.  With the KL term, the slices' lists
+// are merged into the row's top-K set: exact unless some slice dropped a
+// value reaching the set's K-th value (then kl_flag[r] = 1 and
+// k_lm_kl_fallback recomputes the row).
+template <bool KL>
 __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
+  __shared__ float kl_bv[KL ? 4 * kTopKCap : 1];
+  __shared__ int kl_bi[KL ? 4 * kTopKCap : 1];
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wave = wave_id();
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
   if (r >= a.R) return;
   const int i = (int)(r % a.L);
   int d = a.L;
@@ -581,6 +710,16 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     if (lane == 0) {
       a.lse_q[r] = 0.0f;
       if (a.lse_p != nullptr) a.lse_p[r] = 0.0f;
+    }
+    if (KL) {
+      if (lane < a.kl_k) {
+        a.kl_idx[r * a.kl_k + lane] = -1;
+        a.kl_grad[r * a.kl_k + lane] = 0.0f;
+      }
+      if (lane == 0) {
+        a.kl_row[r] = 0.0f;
+        a.kl_flag[r] = 0;
+      }
     }
     return;
   }
@@ -648,6 +787,67 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     a.lse_q[r] = qmraw * a.inv_tq + qt;
     if (a.lse_p != nullptr) a.lse_p[r] = pmraw * a.inv_tp + pt;
   }
+  if (KL) {
+    WaveTopK tk;
+    tk.init(kl_bv + wave * kTopKCap, kl_bi + wave * kTopKCap, a.kl_k);
+    const int ne = a.nslice_t * kLmKlM;
+    const LmKlEntry* ent = a.kl_part + r * ne;
+    for (int e0 = 0; e0 < ne; e0 += 8 * kWave) {
+      float x[8];
+      int ix[8];
+      uint32_t bits = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = e0 + lane * 8 + k;
+        const LmKlEntry en = e < ne ? ent[e] : LmKlEntry{-INFINITY, 0x7FFFFFFF};
+        x[k] = en.val;
+        ix[k] = en.idx;
+        bits |= en.val > -INFINITY ? (1u << k) : 0u;
+      }
+      tk.offer8(x, 0, bits, [&](int k) { return ix[k]; }, lane);
+    }
+    tk.finish(lane);
+    const float tau = tk.n >= a.kl_k ? tk.bv[a.kl_k - 1] : -INFINITY;
+    float bmax = -INFINITY;
+    for (int sl = lane; sl < a.nslice_t; sl += kWave) bmax = fmaxf(bmax, a.kl_bound[r * a.nslice_t + sl]);
+    bmax = wave_max(bmax);
+    // a dropped value at or above the K-th member (or any, with fewer than K
+    // members) might belong to the set
+    const bool redo = tk.n >= a.kl_k ? bmax >= tau : bmax > -INFINITY;
+    if (lane == 0) a.kl_flag[r] = redo ? 1 : 0;
+    if (!redo) lm_kl_row(a, tk, r, lane);
+  }
+}
+
+// The KL term of the rows flagged by k_lm_combine, from every mapped target
+// logit of the row (each lane a dot product per draft index), exactly.  One
+// wavefront per row; unflagged rows return at once.
+__global__ __launch_bounds__(256) void k_lm_kl_fallback(LmCombineArgs a) {
+  __shared__ float kl_bv[4 * kTopKCap];
+  __shared__ int kl_bi[4 * kTopKCap];
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_id();
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  if (r >= a.R || a.kl_flag[r] == 0) return;
+  const bf16_t* ht = static_cast<const bf16_t*>(a.Ht) + r * a.H;
+  const bf16_t* Wt = static_cast<const bf16_t*>(a.Wt);
+  WaveTopK tk;
+  tk.init(kl_bv + wave * kTopKCap, kl_bi + wave * kTopKCap, a.kl_k);
+  for (int v0 = 0; v0 < a.Vd; v0 += 8 * kWave) {
+    float y[8];
+    uint32_t bits = 0;
+#pragma unroll 1
+    for (int k = 0; k < 8; ++k) {
+      const int v = v0 + lane * 8 + k;
+      const int t = v < a.Vd ? (a.d2t != nullptr ? a.d2t[v] : v) : -1;
+      const bool ok = (uint32_t)t < (uint32_t)a.Vt;
+      y[k] = ok ? lane_dot(ht, Wt + (int64_t)t * a.H, a.H) : -INFINITY;
+      bits |= ok && y[k] > -INFINITY ? (1u << k) : 0u;
+    }
+    tk.offer8(y, v0 + lane * 8, bits, [](int col) { return col; }, lane);
+  }
+  tk.finish(lane);
+  lm_kl_row(a, tk, r, lane);
 }
 
 // ----------------------------------------------------------- backward pass ---
@@ -712,6 +912,37 @@ __global__ __launch_bounds__(kThreads, 1) void k_lm_bwd_g(LmBwdArgs a) {
       }
     }
     __syncthreads();
+  }
+}
+
+// With the KL term: g at the row's top-K members, recomputed in fp32 with the
+// term's sparse gradient added, then rounded once (the entries k_lm_bwd_g
+// wrote there are replaced).  One wavefront per row.
+__global__ __launch_bounds__(256) void k_lm_kl_fix(LmBwdArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave_id();
+  if (r >= a.R) return;
+  const bf16_t* hd = static_cast<const bf16_t*>(a.Hd) + r * a.H;
+  const bf16_t* Wd = static_cast<const bf16_t*>(a.Wd);
+  const float ca = a.coef_a[r], cb = a.coef_b[r];
+  const float c2 = a.inv_tq * kLog2e;
+  const float k = a.scale * a.inv_tq;
+  const float kab = k * (ca + cb), ka = k * ca, kb = k * cb;
+  const float lse2 = a.lse_q[r] * kLog2e;
+  const int zd = a.tok_d[r], zt = a.tok_t[r];
+  bf16_t* G = static_cast<bf16_t*>(a.G) + r * a.ldg;
+  for (int j = 0; j < a.kl_k; ++j) {
+    const int v = a.kl_idx[r * a.kl_k + j];
+    if ((uint32_t)v >= (uint32_t)a.Vd) continue;
+    float t = 0.0f;
+    if (ca != 0.0f || cb != 0.0f) {
+      const float x = wave_dot(hd, Wd + (int64_t)v * a.H, a.H, lane);
+      t = kab * __builtin_amdgcn_exp2f(fmaf(x, c2, -lse2));
+      t -= (v == zd) ? ka : 0.0f;
+      t -= (v == zt) ? kb : 0.0f;
+    }
+    t += a.kl_grad[r * a.kl_k + j];
+    if (lane == 0) store1(G + v, t);
   }
 }
 
@@ -781,12 +1012,25 @@ hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32
 
 hipError_t launch_lm_fwd(const LmFwdArgs& a, hipStream_t s) {
   const int64_t nrt = (a.R + TM - 1) / TM;
-  hipLaunchKernelGGL(k_lm_fwd, dim3((unsigned)(nrt * (a.nslice_t + a.nslice_d))), dim3(kThreads), 0, s, a);
+  const dim3 grid((unsigned)(nrt * (a.nslice_t + a.nslice_d)));
+  if (a.kl_part != nullptr)
+    hipLaunchKernelGGL(k_lm_fwd<true>, grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_lm_fwd<false>, grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)((a.R + 3) / 4));
+  if (a.kl_k > 0)
+    hipLaunchKernelGGL(k_lm_combine<true>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_lm_combine<false>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_kl_fallback(const LmCombineArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_lm_kl_fallback, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -795,6 +1039,11 @@ hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_bwd_g, dim3((unsigned)(nrt * ((a.Vd + TN - 1) / TN))), dim3(kThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.kl_idx != nullptr) {
+    hipLaunchKernelGGL(k_lm_kl_fix, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   LmGemmNNArgs gm{a.G, a.Wd, a.dH, a.R, a.ldg, a.H, a.H, a.H, a.Vd};
   hipLaunchKernelGGL(k_lm_gemm_nn, dim3((unsigned)(nrt * ((a.H + TN - 1) / TN))), dim3(kThreads), 0, s, gm);
   e = hipGetLastError();

@@ -179,12 +179,14 @@ vsd_status hip_fail(hipError_t e, const char* what) {
 }
 
 struct WorkspaceLayout {
-  size_t la, lq, loss, klrow, inv, part, total;
+  size_t la, lq, loss, klrow, inv, part, klpart, klbound, klflag, total;
 };
 
 // la [R,3], lq [R,3], loss [P], KL row terms [R] fp32; the inverse map
 // [v_target] int32 (fused LM head draws, verification); fused LM head also
-// the slice partials [R, nslice_t + nslice_d].
+// the slice partials [R, nslice_t + nslice_d] and, for the KL term, the
+// target slices' lists [R, nslice_t, kLmKlM], their bounds [R, nslice_t] and
+// the per-row recompute flags [R].
 WorkspaceLayout workspace_layout(const vsd_dims* d) {
   const int64_t R = rows_of(d);
   const int64_t P = (int64_t)d->B * d->T;
@@ -195,10 +197,14 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   w.klrow = w.loss + align_up((size_t)P * sizeof(float));
   w.inv = w.klrow + align_up((size_t)R * sizeof(float));
   w.part = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
-  w.total = w.part;
+  w.total = w.klpart = w.klbound = w.klflag = w.part;
   if (d->hidden_dim > 0) {
-    const size_t nsl = (size_t)(vsd::lm_nslice(d->v_target) + vsd::lm_nslice(d->v_draft));
-    w.total = w.part + align_up((size_t)R * nsl * sizeof(vsd::LmPartial));
+    const size_t nst = (size_t)vsd::lm_nslice(d->v_target);
+    const size_t nsl = nst + (size_t)vsd::lm_nslice(d->v_draft);
+    w.klpart = w.part + align_up((size_t)R * nsl * sizeof(vsd::LmPartial));
+    w.klbound = w.klpart + align_up((size_t)R * nst * vsd::kLmKlM * sizeof(vsd::LmKlEntry));
+    w.klflag = w.klbound + align_up((size_t)R * nst * sizeof(float));
+    w.total = w.klflag + align_up((size_t)R * sizeof(int32_t));
   }
   return w;
 }
@@ -227,7 +233,6 @@ vsd_status check_score_out(const vsd_dims* dims, const vsd_score_out* out, const
 // Validation of the KL outputs (kl_weight > 0) shared by the scoring calls.
 vsd_status check_kl_out(const vsd_dims* dims, const vsd_params* params, const vsd_score_out* out) {
   if (!kl_on(params)) return VSD_OK;
-  if (is_fused(dims)) return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
   if (params->kl_topk > dims->v_draft)
     return fail(VSD_ERR_INVALID_VALUE, "kl_topk=%d > v_draft=%d", params->kl_topk, dims->v_draft);
   if (out->kl_idx == nullptr || out->kl_grad == nullptr)
@@ -323,17 +328,24 @@ vsd_status launch_combine_and_total(const vsd_dims* dims, const vsd_params* para
   return VSD_OK;
 }
 
+// The KL row terms' buffer of a fused call: the caller's kl_row or the
+// workspace's (null with the term off).
+float* fused_kl_row(const vsd_params* params, const vsd_score_out* out, char* ws, const WorkspaceLayout& wl) {
+  if (!kl_on(params)) return nullptr;
+  return out->kl_row != nullptr ? out->kl_row : reinterpret_cast<float*>(ws + wl.klrow);
+}
+
 // Fused LM head: the forward GEMM pass over both vocabularies (sampling
 // or log-sum-exp only), then the slice combine into tokens and row
 // statistics.  tok_in != null scores the given tokens; otherwise draws.
 vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_src* draft, const vsd_src* target,
                       const int32_t* d2t, const int32_t* valid_depth, uint64_t seed, uint32_t offset,
                       const int32_t* const tok_in[3], int32_t* const tok_out[3], const vsd_score_out* out,
-                      char* ws, const WorkspaceLayout& wl, float* la, float* lq, hipStream_t s) {
+                      char* ws, const WorkspaceLayout& wl, float* la, float* lq, float* kl_row, hipStream_t s) {
   const bool sampling = tok_in == nullptr;
   int32_t* inv = nullptr;
   hipError_t e;
-  if (sampling && d2t != nullptr) {
+  if ((sampling || kl_on(params)) && d2t != nullptr) {  // the target draws and the KL lists go through it
     inv = reinterpret_cast<int32_t*>(ws + wl.inv);
     e = vsd::launch_lm_inv(d2t, dims->v_draft, dims->v_target, inv, out->device_error, s);
     if (e != hipSuccess) return hip_fail(e, "k_lm_inv launch");
@@ -358,6 +370,10 @@ vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_
   f.k0 = (uint32_t)(seed & 0xFFFFFFFFu);
   f.k1 = (uint32_t)(seed >> 32);
   f.offset = offset;
+  if (kl_on(params)) {
+    f.kl_part = reinterpret_cast<vsd::LmKlEntry*>(ws + wl.klpart);
+    f.kl_bound = reinterpret_cast<float*>(ws + wl.klbound);
+  }
   e = vsd::launch_lm_fwd(f, s);
   if (e != hipSuccess) return hip_fail(e, "k_lm_fwd launch");
   vsd::LmCombineArgs c{};
@@ -386,8 +402,22 @@ vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_
   c.nslice_d = f.nslice_d;
   c.inv_tq = f.inv_tq;
   c.inv_tp = f.inv_tp;
+  if (kl_on(params)) {
+    c.kl_k = params->kl_topk;
+    c.kl_part = f.kl_part;
+    c.kl_bound = f.kl_bound;
+    c.kl_flag = reinterpret_cast<int32_t*>(ws + wl.klflag);
+    c.kl_idx = out->kl_idx;
+    c.kl_grad = out->kl_grad;
+    c.kl_row = kl_row;
+    c.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
+  }
   e = vsd::launch_lm_combine(c, s);
   if (e != hipSuccess) return hip_fail(e, "k_lm_combine launch");
+  if (kl_on(params)) {
+    e = vsd::launch_lm_kl_fallback(c, s);
+    if (e != hipSuccess) return hip_fail(e, "k_lm_kl_fallback launch");
+  }
   return VSD_OK;
 }
 
@@ -512,9 +542,11 @@ vsd_status vsd_score_paths(const vsd_dims* dims, const vsd_params* params, const
 
   if (is_fused(dims)) {
     const int32_t* const tin[3] = {tok_draft, tok_target, tok_greedy};
-    st = lm_forward(dims, params, draft, target, d2t, valid_depth, 0, 0, tin, nullptr, out, ws, wl, la, lq, s);
+    float* kl_row = fused_kl_row(params, out, ws, wl);
+    st = lm_forward(dims, params, draft, target, d2t, valid_depth, 0, 0, tin, nullptr, out, ws, wl, la, lq, kl_row,
+                    s);
     if (st != VSD_OK) return st;
-    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s)) != VSD_OK)
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s)) != VSD_OK)
       return st;
     return ok();
   }
@@ -557,10 +589,11 @@ static vsd_status sample_score_impl(const vsd_dims* dims, const vsd_params* para
 
   if (is_fused(dims)) {
     int32_t* const tout[3] = {tok_draft, tok_target, tok_greedy};
+    float* kl_row = fused_kl_row(params, out, ws, wl);
     st = lm_forward(dims, params, draft, target, d2t, valid_depth, seed, offset, nullptr, tout, out, ws, wl, la,
-                    lq, s);
+                    lq, kl_row, s);
     if (st != VSD_OK) return st;
-    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, nullptr, s)) != VSD_OK)
+    if ((st = launch_combine_and_total(dims, params, valid_depth, out, la, lq, loss_pos, kl_row, s)) != VSD_OK)
       return st;
     return ok();
   }
@@ -659,12 +692,8 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
   if (grad == nullptr || grad->grad_logits == nullptr) return fail(VSD_ERR_NULL_POINTER, "grad->grad_logits is NULL");
   if (!aligned16(grad->grad_logits)) return fail(VSD_ERR_MISALIGNED, "grad_logits not 16-byte aligned");
   if (device_error == nullptr) return fail(VSD_ERR_NULL_POINTER, "device_error is NULL");
-  if (kl_on(params)) {
-    if (is_fused(dims))
-      return fail(VSD_ERR_UNSUPPORTED, "the top-K KL term is computed on materialised logits only");
-    if (kl_idx == nullptr || kl_grad == nullptr)
-      return fail(VSD_ERR_NULL_POINTER, "kl_idx and kl_grad are required with kl_weight > 0");
-  }
+  if (kl_on(params) && (kl_idx == nullptr || kl_grad == nullptr))
+    return fail(VSD_ERR_NULL_POINTER, "kl_idx and kl_grad are required with kl_weight > 0");
 
   if (is_fused(dims)) {
     // grad_logits receives g (bf16, stride ld_draft), then dH = g W_d
@@ -692,6 +721,11 @@ vsd_status vsd_weighted_loss_bwd(const vsd_dims* dims, const vsd_params* params,
     b.Vd = dims->v_draft;
     b.inv_tq = 1.0f / params->temp_draft;
     b.scale = params->loss_scale;
+    if (kl_on(params)) {
+      b.kl_idx = kl_idx;
+      b.kl_grad = kl_grad;
+      b.kl_k = params->kl_topk;
+    }
     hipError_t e = vsd::launch_lm_bwd(b, static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return hip_fail(e, "k_lm_bwd launch");
     return ok();

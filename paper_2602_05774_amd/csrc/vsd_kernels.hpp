@@ -155,6 +155,16 @@ struct LmPartial {
   int32_t pad;
 };
 
+// Top-K renormalised KL term on the fused head: every row segment of the
+// target pass keeps its kLmKlM best mapped target logits; a slice's record
+// holds the best kLmKlM of its segments' lists and an upper bound of every
+// value it dropped (-inf: none dropped).
+constexpr int kLmKlM = 8;
+struct LmKlEntry {
+  float val;                 // raw target logit
+  int32_t idx;               // its draft index
+};
+
 struct LmFwdArgs {
   const void* Hd;            // [R, H] bf16
   const void* Ht;            // [R, H] bf16
@@ -162,6 +172,8 @@ struct LmFwdArgs {
   const void* Wt;            // [Vt, H] bf16
   const int32_t* inv;        // [Vt] draft index of each target column (-1: none); null = identity
   LmPartial* part;           // [R, nslice_t + nslice_d], target slices first
+  LmKlEntry* kl_part;        // KL term: [R, nslice_t, kLmKlM] slice lists, or null (term off)
+  float* kl_bound;           // KL term: [R, nslice_t] bound of the dropped values
   int64_t R;
   int32_t H, Vd, Vt;
   int32_t nslice_t, nslice_d;
@@ -189,6 +201,15 @@ struct LmCombineArgs {
   int32_t L, H, Vd, Vt;
   int32_t nslice_t, nslice_d;
   float inv_tq, inv_tp;
+  // top-K renormalised KL term (kl_k > 0 turns it on)
+  int32_t kl_k;
+  const LmKlEntry* kl_part;  // [R, nslice_t, kLmKlM]
+  const float* kl_bound;     // [R, nslice_t]
+  int32_t* kl_flag;          // [R] 1: the slice lists may have dropped a member (exact recompute)
+  int32_t* kl_idx;           // [R, kl_k]
+  float* kl_grad;            // [R, kl_k]
+  float* kl_row;             // [R]
+  float kl_gscale;           // loss_scale * kl_weight / N / T_q
 };
 
 struct LmBwdArgs {
@@ -202,6 +223,9 @@ struct LmBwdArgs {
   const int32_t* tok_t;
   const float* coef_a;
   const float* coef_b;
+  const int32_t* kl_idx;     // [R, kl_k] or null: the KL term's sparse gradient, added to G
+  const float* kl_grad;      // [R, kl_k]
+  int32_t kl_k;
   int64_t R, ldg;
   int32_t H, Vd;
   float inv_tq, scale;
@@ -229,6 +253,7 @@ struct LmGemmNNArgs {
 hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32_t* err, hipStream_t s);
 hipError_t launch_lm_fwd(const LmFwdArgs& a, hipStream_t s);
 hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s);
+hipError_t launch_lm_kl_fallback(const LmCombineArgs& a, hipStream_t s);
 hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);

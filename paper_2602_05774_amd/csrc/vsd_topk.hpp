@@ -189,12 +189,34 @@ struct WaveTopK {
   __device__ __forceinline__ void finish(int lane) { compact(lane); }
 };
 
-// The KL term of one row (Eq. klv) from its top K, after WaveTopK::finish():
-// lane k < K takes the k-th entry (draft index v, target logit y); p_hat and
-// q_hat (from y / T_p and X[v] / T_q) are renormalised over the K, the row
-// term -sum p_hat log q_hat goes to *row_out (lane 0) and the gradient
-// coefficients gscale (q_hat - p_hat) with the indices to idx_out / grad_out.
-// Only finite values become entries (a -inf offer is dropped at the next
+// The KL term of one row (Eq. klv) from its members' values held by the
+// lanes: lane k < K holds member k (mine), its draft index v (-1: none),
+// target logit y and draft logit x.  p_hat and q_hat (from y / T_p and
+// x / T_q) are renormalised over the members, the row term
+// -sum p_hat log q_hat goes to *row_out (lane 0) and the gradient
+// coefficients gscale (q_hat - p_hat) with the indices to idx_out / grad_out
+// (index -1 and coefficient 0 past the members).
+__device__ inline void kl_row_term_xy(bool mine, int v, float y, float x, int K, float inv_tq, float inv_tp,
+                                      float gscale, int32_t* idx_out, float* grad_out, float* row_out, int lane) {
+  const float pa = mine ? y * inv_tp : -INFINITY;
+  const float qa = v >= 0 ? x * inv_tq : -INFINITY;
+  const float pm = wave_max(pa), qm = wave_max(qa);
+  const float pe = mine ? expf(pa - pm) : 0.0f;
+  const float qe = mine ? expf(qa - qm) : 0.0f;
+  const float ps = wave_sum(pe), qs = wave_sum(qe);
+  const float p_hat = pe / ps, q_hat = qe / qs;
+  const float log_q_hat = qa - qm - logf(qs);
+  const float term = wave_sum(mine ? -p_hat * log_q_hat : 0.0f);
+  if (lane < K) {
+    idx_out[lane] = mine ? v : -1;
+    grad_out[lane] = mine ? gscale * (q_hat - p_hat) : 0.0f;
+  }
+  if (lane == 0) *row_out = term;
+}
+
+// The same term from a materialised row's top K, after WaveTopK::finish():
+// lane k < K takes the k-th entry (draft index v, target logit y) and reads
+// x = X[v].  Only finite values become entries (a -inf offer is dropped at the next
 // compaction), so a row with fewer than K finite mapped target logits has
 // fewer than K entries: the distributions are renormalised over those, and
 // the slots past them get index -1 and coefficient 0.  An index is read from
@@ -205,20 +227,9 @@ __device__ void kl_row_term(const WaveTopK& tk, const T* X, int Vd, float inv_tq
   const bool mine = lane < tk.n && lane < tk.K;
   int v = mine ? tk.bi[lane] : -1;
   v = (uint32_t)v < (uint32_t)Vd ? v : -1;
-  const float pa = mine ? tk.bv[lane] * inv_tp : -INFINITY;
-  const float qa = v >= 0 ? load1(X + v) * inv_tq : -INFINITY;
-  const float pm = wave_max(pa), qm = wave_max(qa);
-  const float pe = mine ? expf(pa - pm) : 0.0f;
-  const float qe = mine ? expf(qa - qm) : 0.0f;
-  const float ps = wave_sum(pe), qs = wave_sum(qe);
-  const float p_hat = pe / ps, q_hat = qe / qs;
-  const float log_q_hat = qa - qm - logf(qs);
-  const float term = wave_sum(mine ? -p_hat * log_q_hat : 0.0f);
-  if (lane < tk.K) {
-    idx_out[lane] = mine ? v : -1;
-    grad_out[lane] = mine ? gscale * (q_hat - p_hat) : 0.0f;
-  }
-  if (lane == 0) *row_out = term;
+  const float y = mine ? tk.bv[lane] : -INFINITY;
+  const float x = v >= 0 ? load1(X + v) : -INFINITY;
+  kl_row_term_xy(mine, v, y, x, tk.K, inv_tq, inv_tp, gscale, idx_out, grad_out, row_out, lane);
 }
 
 }  // namespace vsd

@@ -217,7 +217,7 @@ def test_fused_lm_head_validation(lib):
 
 
 def test_kl_term_validation(lib):
-    """kl_weight / kl_topk checks of the scoring calls; the fused LM head does not compute the term."""
+    """kl_weight / kl_topk checks of the scoring calls, materialised and fused."""
     for kw in (dict(kl_weight=-0.1), dict(kl_weight=float("nan")), dict(kl_weight=0.5, kl_topk=0),
                dict(kl_weight=0.5, kl_topk=17)):
         assert _score(lib, params=_params(**kw)) == 3
@@ -230,14 +230,16 @@ def test_kl_term_validation(lib):
     head = _lib.VsdSrc(None, FAKE, FAKE)
     fdims = _dims(dtype=_lib.VSD_BF16, hidden_dim=128)
     pr = _params(kl_weight=0.5, kl_topk=10)
-    st = lib.vsd_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head), None,
-                             None, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
-    assert st == 6                                   # fused LM head: not with the KL term
-    st = lib.vsd_sample_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head),
-                                    None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(full), FAKE, 1 << 30, None)
-    assert st == 6                                   # one-pass call with the fused LM head: not with the KL term
     src = _lib.VsdSrc(FAKE, None, None)
     bare = _lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=FAKE, device_error=FAKE)
+    st = lib.vsd_score_paths(ctypes.byref(fdims), ctypes.byref(pr), ctypes.byref(head), ctypes.byref(head), None,
+                             None, FAKE, FAKE, FAKE, ctypes.byref(bare), FAKE, 1 << 30, None)
+    assert st == 1                                   # fused LM head: kl_idx / kl_grad required
+    fsmall = _dims(dtype=_lib.VSD_BF16, hidden_dim=128, v_draft=8, v_target=8, ld_draft=8, ld_target=8)
+    st = lib.vsd_sample_score_paths(ctypes.byref(fsmall), ctypes.byref(_params(kl_weight=0.5, kl_topk=9)),
+                                    ctypes.byref(head), ctypes.byref(head), None, None, 0, 0, FAKE, FAKE, FAKE,
+                                    ctypes.byref(full), FAKE, 1 << 30, None)
+    assert st == 3                                   # fused one-pass call: kl_topk beyond the draft vocabulary
     st = lib.vsd_sample_score_paths(ctypes.byref(_dims()), ctypes.byref(pr), ctypes.byref(src), ctypes.byref(src),
                                     None, None, 0, 0, FAKE, FAKE, FAKE, ctypes.byref(bare), FAKE, 1 << 30, None)
     assert st == 1                                   # one-pass call: kl_idx / kl_grad required
@@ -333,7 +335,7 @@ def test_static_scratch_variant_validates_before_touching_the_device(lib):
     assert call(out=_lib.VsdScoreOut(lse_draft=FAKE, coef_a=FAKE, coef_b=None, device_error=FAKE)) == 1
     assert call(dims=_dims(v_target=2000, ld_target=2000)) == 5
     # dims whose workspace exceeds the static scratch
-    limit = 64 << 20
+    limit = 256 << 20
     B = 1
     while True:
         d = _dims(B=B, T=512, N=8, L=6, v_draft=32000, v_target=128256, dtype=_lib.VSD_BF16, ld_draft=32000,
