@@ -218,8 +218,24 @@ def bench_lm_head(cfg, steps, warmup, dev):
     torch.cuda.synchronize()
     t_bwd_w = ew[0].elapsed_time(ew[1])
     del gw
-    if int(err.item()) != 0 or int(out.device_error.item()) != 0:
+    # the step once more with the top-K renormalised KL term (K = 10)
+    params_kl = vsd.Params(temp_draft=cfg.temp_draft, temp_target=cfg.temp_target, kl_weight=0.1, kl_topk=10)
+    out_kl = vsd.alloc_score_outputs(prob, dev, kl_topk=10)
+    ek = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for rep in range(2):  # the first run warms up
+        ek[0].record()
+        vsd.sample_score_paths(prob, params_kl, Xs, Ys, inp["d2t"], inp["valid_depth"], cfg.philox_seed,
+                               cfg.philox_offset, out=out_kl, workspace=ws, tokens=tok)
+        ek[1].record()
+        vsd.weighted_loss_bwd(prob, params_kl, Xs, out_kl.lse_draft, tok[0], tok[1], out_kl.coef_a, out_kl.coef_b,
+                              grad=grad, device_error=err, kl_idx=out_kl.kl_idx, kl_grad=out_kl.kl_grad)
+        ek[2].record()
+    torch.cuda.synchronize()
+    kl_variant = {"kl_topk": 10, "kl_weight": 0.1, "sample_score_ms": ek[0].elapsed_time(ek[1]),
+                  "bwd_ms": ek[1].elapsed_time(ek[2]), "ms_per_step": ek[0].elapsed_time(ek[2])}
+    if int(err.item()) != 0 or int(out.device_error.item()) != 0 or int(out_kl.device_error.item()) != 0:
         raise RuntimeError("device error reported during the LM-head benchmark")
+    del out_kl
     live = prob.R if inp["valid_depth"] is None else int((tok[0] >= 0).sum().item())
     R, H = prob.R, cfg.hidden
     # algorithmic flops: every row's draft and target logits once (forward);
@@ -237,6 +253,7 @@ def bench_lm_head(cfg, steps, warmup, dev):
                     "bwd_with_weight_grad": {"ms": t_bwd_w, "flop": bwd_flop * 1.5,
                                              "TFLOP/s": tf(bwd_flop * 1.5, t_bwd_w)}},
         "step_TFLOP/s": tf(fwd_flop + bwd_flop, t_fwd + t_bwd),
+        "kl_variant": kl_variant,
         "roofline": {"bound": "mfma", "kernel": "k_lm_fwd (forward call: GEMM tiles + sampling epilogue)",
                      "achieved": tf(fwd_flop, t_fwd), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tf(fwd_flop, t_fwd) / MFMA_BF16_PEAK_TFLOPS,
