@@ -4,7 +4,8 @@ Each mutant is a copy of an oracle module with one plausible mistake (a
 dropped term, a flipped sign or comparison, a wrong index or family, a
 transposed operand).  The checks below are the same kinds of pins as the
 oracle's own tests (hand-derived examples, closed forms, finite differences,
-distribution tests, float64 log accuracy); every mutant must fail at least one.
+distribution tests, float64 log accuracy, the generator's blocks against
+rocRAND's engine); every mutant must fail at least one.
 """
 import inspect
 import json
@@ -19,6 +20,7 @@ from scipy import stats
 import oracle.paths as paths_mod
 import oracle.sampler as sampler_mod
 import oracle.verify as verify_mod
+from tests import philox_ref
 
 GOLDEN = ["micro_example.json", "ragged_example.json", "car_example.json"]
 MODES = {"BASIC": 0, "ARW": 1, "ARW_CAR": 2, "ARW_CAR_LOGPROB": 2}
@@ -202,6 +204,18 @@ def _check_exact_ties(P):
     return True
 
 
+def _check_philox(S):
+    counters = np.array([[0, 0, 0, 0], [0xFFFFFFFF] * 4, [11, 22, 33, 44], [0x243F6A88, 0x85A308D3, 5, 7]],
+                        dtype=np.uint64)
+    keys = np.array([[0, 0], [0xFFFFFFFF, 0xFFFFFFFF], [99, 0], [0xA4093822, 0x299F31D0]], dtype=np.uint64)
+    ref = philox_ref.blocks(counters, keys)
+    for c, k, r in zip(counters, keys, ref):
+        got = S.philox4x32_10(*(int(v) for v in c), seed=int(k[0]) | (int(k[1]) << 32))
+        if [int(w) for w in got] != [int(w) for w in r]:
+            return False
+    return True
+
+
 def _check_sampler(S):
     w = (np.arange(2 ** 23, dtype=np.uint64) << np.uint64(9)).astype(np.uint32)
     ug = S.uniform_from_word(w)
@@ -309,6 +323,19 @@ PATH_MUTANTS = [
     ("c = beta * zeta", "c = beta + zeta - 1.0"),
 ]
 
+# the generator's constants, round count and word order (pinned by rocRAND's engine)
+PHILOX_MUTANTS = [
+    ("PHILOX_M0 = 0xD2511F53", "PHILOX_M0 = 0xD2511F57"),
+    ("PHILOX_M1 = 0xCD9E8D57", "PHILOX_M1 = 0xD2511F53"),
+    ("PHILOX_W0 = 0x9E3779B9", "PHILOX_W0 = 0xBB67AE85"),
+    ("PHILOX_W1 = 0xBB67AE85", "PHILOX_W1 = 0xBB67AE86"),
+    ("for j in range(10):", "for j in range(7):"),
+    ("x0, x1, x2, x3 = hi1 ^ x1 ^ rk0, lo1, hi0 ^ x3 ^ rk1, lo0", "x0, x1, x2, x3 = hi0 ^ x1 ^ rk0, lo0, hi1 ^ x3 ^ rk1, lo1"),
+    ("k0, k1 = seed & _MASK32, (seed >> 32) & _MASK32", "k1, k0 = seed & _MASK32, (seed >> 32) & _MASK32"),
+    ("return tuple(x.astype(np.uint32) for x in (x0, x1, x2, x3))",
+     "return tuple(x.astype(np.uint32) for x in (x1, x0, x3, x2))"),
+]
+
 SAMPLER_MUTANTS = [
     ("return -spec_log(e)", "return spec_log(e)"),
     ("inv_t = F32(1.0) / F32(temperature)", "inv_t = F32(temperature)"),
@@ -332,6 +359,8 @@ def test_unmutated_oracle_passes_every_check(golden_dir):
     assert _check_map(paths_mod)
     assert _check_ctx(paths_mod)
     assert _check_sampler(sampler_mod)
+    if philox_ref.available():
+        assert _check_philox(sampler_mod)
     assert _check_verify(verify_mod)
 
 
@@ -347,6 +376,13 @@ def test_path_mutant_is_caught(golden_dir, old, new):
     caught = (not _check_golden(P, golden_dir)) or (not _check_closed_form(P)) \
         or (not _check_fd(P)) or (not _check_map(P)) or (not _check_ctx(P)) or (not _check_exact_ties(P))
     assert caught, f"no pin caught mutant {new!r}"
+
+
+@pytest.mark.skipif(not philox_ref.available(), reason="hipcc or the rocRAND header is missing")
+@pytest.mark.parametrize("old,new", PHILOX_MUTANTS, ids=[f"philox{i}" for i in range(len(PHILOX_MUTANTS))])
+def test_philox_mutant_is_caught(old, new):
+    S = _mutant(sampler_mod, old, new)
+    assert not _check_philox(S), f"no pin caught mutant {new!r}"
 
 
 @pytest.mark.parametrize("old,new", SAMPLER_MUTANTS, ids=[f"sampler{i}" for i in range(len(SAMPLER_MUTANTS))])
