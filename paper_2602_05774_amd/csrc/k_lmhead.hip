@@ -792,9 +792,10 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     tk.init(kl_bv + wave * kTopKCap, kl_bi + wave * kTopKCap, a.kl_k);
     const int ne = a.nslice_t * kLmKlM;
     const LmKlEntry* ent = a.kl_part + r * ne;
+    typedef __attribute__((ext_vector_type(8))) int i32x8;  // a register vector, never a private array
     for (int e0 = 0; e0 < ne; e0 += 8 * kWave) {
       float x[8];
-      int ix[8];
+      i32x8 ix;
       uint32_t bits = 0;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {

@@ -280,10 +280,12 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       for (int k = 0; k < 8; ++k) tt[k] = (uint32_t)d2t[chunk + k * kWave + lane];
     };
     // map entries are range-checked before the launch (k_map_check reports
-    // an out-of-range entry); the clamp only keeps every access in bounds
+    // an out-of-range entry); the buffer's range check keeps every access in
+    // the row
+    const __amdgpu_buffer_rsrc_t yrow = row_rsrc(Y, row_bytes(Y, Vt));
     auto gather = [&](const uint32_t (&tt)[8]) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) g[k] = Y[min(tt[k], (uint32_t)Vt - 1u)];
+      for (int k = 0; k < 8; ++k) buf_gather(yrow, tt[k], g[k]);
     };
     if (MAPPED) {
       load_map(0, t);
@@ -323,7 +325,7 @@ __device__ void target_wave(const T* Y, const int32_t* d2t, T* tile, int Vd, int
       if (DRAW) f.draw8(base, y, ymax, it == 0);
       if (KL) {  // a slice whose largest mapped value is below the top-K threshold offers nothing
         if (it == 0) tk.seed_lane_max(ymax, lane);
-        if (it == 0 || __ballot(ymax >= tk.thv) != 0ull) tk.offer8(y, base, 0xFFu, same, lane);
+        if (it == 0 || __ballot(ymax >= tk.thv) != 0ull) tk.append8(y, base, 0xFFu, same, lane);
       }
       if (next) {
         if (MAPPED)
@@ -568,11 +570,6 @@ __global__ __launch_bounds__(256) void k_map_check(const int32_t* d2t, int Vd, i
   if (v < Vd && (uint32_t)d2t[v] >= (uint32_t)Vt) report_error(err, VSD_DEVERR_MAP_RANGE);
 }
 
-hipError_t launch_map_check(const int32_t* d2t, int Vd, int Vt, int32_t* err, hipStream_t s) {
-  hipLaunchKernelGGL(k_map_check, dim3((unsigned)((Vd + 255) / 256)), dim3(256), 0, s, d2t, Vd, Vt, err);
-  return hipGetLastError();
-}
-
 template <typename T>
 hipError_t launch_step_t(const SampleStepArgs& a, hipStream_t s) {
   if (a.d2t != nullptr) {
@@ -602,6 +599,11 @@ hipError_t launch_t(const SampleArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_map_check(const int32_t* d2t, int Vd, int Vt, int32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_map_check, dim3((unsigned)((Vd + 255) / 256)), dim3(256), 0, s, d2t, Vd, Vt, err);
+  return hipGetLastError();
+}
 
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s) {
   const bool fused = a.lse_q != nullptr;

@@ -111,10 +111,9 @@ __device__ __forceinline__ RowLse row_lse(const T* row, int V, float c, int lane
 // a map the streamed values themselves are offered.  Only values at or above
 // the top-K threshold are ever appended, so a slice whose largest value is
 // below it in every lane offers nothing: one ballot decides.  Map entries
-// outside [0, Vt) are reported and offer nothing.
+// outside [0, Vt) are reported by k_map_check, launched first.
 template <typename T, bool MAPPED>
-__device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const int32_t* d2t, int Vd,
-                               int32_t* err) {
+__device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK& tk, const int32_t* d2t, int Vd) {
   float mraw = kNegBig, mc = kNegBig, s = 0.0f;
   constexpr int U = 4;
   constexpr int step = 8 * kWave;
@@ -126,8 +125,8 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
       tk.offer8(x, base, bits, idx_of, lane);
       return;
     }
-    if (__ballot(vmax >= tk.thv) == 0ull) return;
-    tk.offer8(x, base, bits, idx_of, lane);
+    if (__ballot(vmax >= tk.thv) == 0ull) return;  // vmax: the lane's largest offered value
+    tk.append8(x, base, bits, idx_of, lane);
   };
   auto lse8 = [&](const float (&x)[8], float cm) {
     if (cm > mraw) {
@@ -143,35 +142,45 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
   // index 512 dc + 64 k + lane) is offered from gathered raw values.  Its map
   // entries are loaded one iteration ahead and its gathers are issued right
   // after the stream loads of the iteration that offers it, so the
-  // log-sum-exp work of the block covers their latency.
+  // log-sum-exp work of the block covers their latency.  The map's range is
+  // checked before the launch (k_map_check); the gathers go through the
+  // row's buffer resource, which keeps every access in the row.  Only the
+  // last chunk can hold indices past V_d (their slots offer nothing).
   const int ndc = MAPPED ? (Vd + step - 1) / step : 0;
+  const int nfull_dc = MAPPED ? Vd / step : 0;
   int dc = 0;
   uint32_t tmap[8];
   T graw[8];
-  bool map_bad = false;
+  const __amdgpu_buffer_rsrc_t yrow = row_rsrc(row, row_bytes(row, V));
   auto load_map = [&](int d) {
+    if (d < nfull_dc) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int v = d * step + k * kWave + lane;
-      tmap[k] = v < Vd ? (uint32_t)d2t[v] : 0xFFFFFFFFu;
+      for (int k = 0; k < 8; ++k) tmap[k] = (uint32_t)d2t[d * step + k * kWave + lane];
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int v = d * step + k * kWave + lane;
+        tmap[k] = v < Vd ? (uint32_t)d2t[v] : 0u;
+      }
     }
   };
-  auto gather = [&]() {  // map entries outside [0, Vt) offer nothing (reported)
+  auto gather = [&]() {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const bool ok = tmap[k] < (uint32_t)V;
-      map_bad |= !ok && tmap[k] != 0xFFFFFFFFu;
-      graw[k] = row[ok ? tmap[k] : 0u];
-    }
+    for (int k = 0; k < 8; ++k) buf_gather(yrow, tmap[k], graw[k]);
   };
   auto offer_gathered = [&](int d) {
     float y[8];
-    uint32_t bits = 0;
+    uint32_t bits = 0xFFu;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const bool ok = tmap[k] < (uint32_t)V;
-      y[k] = ok ? load1(&graw[k]) : -INFINITY;
-      bits |= ok ? (1u << k) : 0u;
+    for (int k = 0; k < 8; ++k) y[k] = load1(&graw[k]);
+    if (d >= nfull_dc) {
+      bits = 0u;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const bool in = d * step + k * kWave + lane < Vd;
+        y[k] = in ? y[k] : -INFINITY;
+        bits |= in ? (1u << k) : 0u;
+      }
     }
     const int base = d * step + lane;
     offer(y, 0, bits, max8(y), [&](int k) { return base + k * kWave; });
@@ -217,7 +226,6 @@ __device__ RowLse row_lse_topk(const T* row, int V, float c, int lane, WaveTopK&
     offer_gathered(dc);
     if (++dc < ndc) load_map(dc);
   }
-  if (map_bad) report_error(err, VSD_DEVERR_MAP_RANGE);
   wave_lse2(mc, s);
   mraw = wave_max(mraw);
   const float delta = fmaf(mraw, c, -mc);
@@ -267,7 +275,7 @@ __global__ __launch_bounds__(256) void k_score_rows(ScoreRowArgs a) {
   if (KL) {
     const int slot = wave_id();
     tk.init(kl_bv + slot * kTopKCap, kl_bi + slot * kTopKCap, a.kl_k);
-    p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.d2t, a.Vd, a.err);
+    p = row_lse_topk<T, MAPPED>(Y, a.Vt, a.inv_tp * kLog2e, lane, tk, a.d2t, a.Vd);
   } else {
     p = row_lse(Y, a.Vt, a.inv_tp * kLog2e, lane);
   }
@@ -442,6 +450,10 @@ __global__ __launch_bounds__(256) void k_loss_total(const float* loss_pos, int32
 template <typename T>
 hipError_t launch_rows_t(const ScoreRowArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.R + kRowsPerBlock - 1) / kRowsPerBlock));
+  if (a.kl_k > 0 && a.d2t != nullptr) {  // the top-K gathers through the map unchecked
+    const hipError_t e = launch_map_check(a.d2t, a.Vd, a.Vt, a.err, s);
+    if (e != hipSuccess) return e;
+  }
   if (a.kl_k > 0) {
     if (a.d2t != nullptr)
       hipLaunchKernelGGL((k_score_rows<T, true, true>), grid, dim3(256), 0, s, a);

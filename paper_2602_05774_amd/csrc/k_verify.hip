@@ -96,6 +96,7 @@ __global__ __launch_bounds__(kWavesPerPath * kWave) void k_verify(VerifyArgs a) 
   const float cq2 = a.inv_tq * kLog2e, cp2 = a.inv_tp * kLog2e;
   const float lq2 = a.lse_q[r] * kLog2e, lp2 = a.lse_p[r] * kLog2e;
   FamilyDraw f{(uint32_t)r, 3u, a.offset, a.k0, a.k1, 1.0f, kLog2e};
+  const __amdgpu_buffer_rsrc_t xrow = row_rsrc(X, row_bytes(X, a.Vd));
   // max(0, p - q) of target indices base .. base+7 (p from the target
   // logit, q from the draft logit through the inverse map, 0 if unmapped)
   auto load_res = [&](int base, float (&res)[8]) {
@@ -105,12 +106,15 @@ __global__ __launch_bounds__(kWavesPerPath * kWave) void k_verify(VerifyArgs a) 
     if (MAPPED) {
       int32_t iv[8];
       load8(a.inv + base, iv);
-      // every lane loads (an unmapped column reads element 0 and discards
-      // it), so the eight gathers issue together instead of one per branch
+      // every lane loads, so the eight gathers issue together instead of one
+      // per branch; they go through the draft row's buffer resource, which
+      // answers an unmapped column's index (-1) with 0 without an access
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         mapped[k] = (uint32_t)iv[k] < (uint32_t)a.Vd;
-        x[k] = load1(X + (mapped[k] ? iv[k] : 0));
+        T raw;
+        buf_gather(xrow, (uint32_t)iv[k], raw);
+        x[k] = load1(&raw);
       }
     } else {
       load8(X + base, x);

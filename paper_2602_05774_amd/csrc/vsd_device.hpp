@@ -130,6 +130,27 @@ __device__ __forceinline__ void load8(const int32_t* p, int32_t (&v)[8]) {
 __device__ __forceinline__ float load1(const float* p) { return *p; }
 __device__ __forceinline__ float load1(const bf16_t* p) { return __uint_as_float((uint32_t)(*p) << 16); }
 
+// Gathers from one row through a raw buffer resource (the row's base and
+// size wave-uniform, so the descriptor lives in scalar registers): the byte
+// offset is the only per-lane address arithmetic (no 64-bit address, no
+// clamp), and the hardware returns 0 for an offset at or past the row's
+// size, so no access leaves the row whatever the index.  Callers use it for
+// indices from a map whose range is checked and reported elsewhere.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* row, uint32_t bytes) {
+  // word 3 of a gfx9 buffer descriptor: 32-bit data format, no swizzle
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(row), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t row_bytes(const float*, int n) { return (uint32_t)n * 4u; }
+__device__ __forceinline__ uint32_t row_bytes(const bf16_t*, int n) { return (uint32_t)n * 2u; }
+// raw element idx of the row (the offset wraps modulo 2^32 for indices of
+// 2^31 and above: still inside the row's range check)
+__device__ __forceinline__ void buf_gather(__amdgpu_buffer_rsrc_t r, uint32_t idx, float& out) {
+  out = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(idx * 4u), 0, 0));
+}
+__device__ __forceinline__ void buf_gather(__amdgpu_buffer_rsrc_t r, uint32_t idx, bf16_t& out) {
+  out = __builtin_amdgcn_raw_buffer_load_b16(r, (int)(idx * 2u), 0, 0);
+}
+
 // fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = (__bf16)lo;

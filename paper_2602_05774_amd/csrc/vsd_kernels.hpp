@@ -256,6 +256,10 @@ hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s);
 hipError_t launch_lm_kl_fallback(const LmCombineArgs& a, hipStream_t s);
 hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 
+// Range check of a draft-to-target map: the first entry outside [0, Vt) is
+// reported as VSD_DEVERR_MAP_RANGE (kernels that gather through the map
+// without testing each entry run it first).
+hipError_t launch_map_check(const int32_t* d2t, int Vd, int Vt, int32_t* err, hipStream_t s);
 hipError_t launch_sample(const SampleArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_sample_step(const SampleStepArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_verify(const VerifyArgs& a, bool bf16, hipStream_t s);

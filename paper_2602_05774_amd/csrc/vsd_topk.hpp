@@ -77,11 +77,46 @@ struct WaveTopK {
     append8(x, base, bits, idx_of, lane);
   }
 
+  // append8 without the early exit: for callers that already know some
+  // lane's offered maximum reaches the threshold.
   template <class IdxOf>
-  __device__ void append8(const float (&x)[8], int base, uint32_t bits, IdxOf idx_of, int lane) {
+  __device__ __forceinline__ void append8(const float (&x)[8], int base, uint32_t bits, IdxOf idx_of, int lane) {
     uint32_t q = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) q |= (((bits >> k) & 1u) && x[k] >= thv) ? (1u << k) : 0u;
+    if (__ballot((q & (q - 1u)) != 0u) == 0ull) {
+      // At most one candidate per lane, the common case once the threshold
+      // has risen: one ballot places them, and the lane's entry is picked
+      // from its slice by selects.  (n <= 64 before the call, so the at
+      // most 64 new entries fit.)
+      const uint64_t has = __ballot(q != 0u);
+      const int total = __builtin_popcountll(has);
+      if (q != 0u) {
+        // the entry at slice position k = ctz(q), by a tree of selects on
+        // k's bits (no indexed access to the register arrays)
+        const uint32_t k = (uint32_t)__builtin_ctz(q);
+        const bool b0 = (k & 1u) != 0u, b1 = (k & 2u) != 0u, b2 = (k & 4u) != 0u;
+        const float v01 = b0 ? x[1] : x[0], v23 = b0 ? x[3] : x[2];
+        const float v45 = b0 ? x[5] : x[4], v67 = b0 ? x[7] : x[6];
+        const float v = b2 ? (b1 ? v67 : v45) : (b1 ? v23 : v01);
+        const int i01 = b0 ? idx_of(base + 1) : idx_of(base), i23 = b0 ? idx_of(base + 3) : idx_of(base + 2);
+        const int i45 = b0 ? idx_of(base + 5) : idx_of(base + 4), i67 = b0 ? idx_of(base + 7) : idx_of(base + 6);
+        const int id = b2 ? (b1 ? i67 : i45) : (b1 ? i23 : i01);
+        const int pos = n + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(has >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)has, 0u));
+        bv[pos] = v;
+        bi[pos] = id;
+      }
+      n += total;
+    } else {
+      append8_dense(x, base, q, idx_of);
+    }
+    if (n > kWave) compact(lane);  // keeps the threshold close to the K-th best so far
+  }
+
+  // The general append: q holds each lane's candidate positions.
+  template <class IdxOf>
+  __device__ __forceinline__ void append8_dense(const float (&x)[8], int base, uint32_t q, IdxOf idx_of) {
     // positions by slice position k, then by lane: one ballot per k and the
     // count of lower lanes in it (the buffer's order is irrelevant to the
     // selection, which orders by value and index)
@@ -92,8 +127,7 @@ struct WaveTopK {
       bal[k] = __ballot((q >> k) & 1u);
       total += __builtin_popcountll(bal[k]);
     }
-    if (n + total > kTopKCap) compact(lane);
-    int pos0 = n;
+    int pos0 = n;  // n <= 64 before the call and total <= 512: the buffer holds them
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       if ((q >> k) & 1u) {
@@ -105,7 +139,6 @@ struct WaveTopK {
       pos0 += __builtin_popcountll(bal[k]);
     }
     n += total;
-    if (n > kWave) compact(lane);  // keeps the threshold close to the K-th best so far
   }
 
   // Keep the K best buffered entries, in order, at the front.  Selected
