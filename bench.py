@@ -770,7 +770,8 @@ def main_lm_head(args, cfg):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": r["workload"], "path_tokens_per_step": r["path_tokens_per_step"],
                    "parallelism": "single GPU"},
-        "kernels": r["kernels"], "step_TFLOP/s": r["step_TFLOP/s"], "roofline": r["roofline"], "cpu_baseline": base,
+        "kernels": r["kernels"], "step_TFLOP/s": r["step_TFLOP/s"], "kl_variant": r["kl_variant"],
+        "roofline": r["roofline"], "cpu_baseline": base,
     }
     print(json.dumps(line), flush=True)
 

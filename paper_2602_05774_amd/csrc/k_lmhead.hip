@@ -53,7 +53,8 @@ static_assert(TM * LDK == TK * LDN, "both operand layouts fill the same stage sl
 static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit the operand buffers");
 static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
 static_assert(2 * kStageNT * 2 <= kLdsBytes, "two direct-loaded NT stages fit");
-static_assert(TM * 4 * (32 + kLmKlM * 8 + 4) <= kLdsBytes, "the slice merge's row states and KL lists fit");
+constexpr int kLmSegM = 6;                   // KL term: list length of one row segment
+static_assert(TM * 4 * (32 + kLmSegM * 8 + 4) <= kLdsBytes, "the slice merge's row states and KL lists fit");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -370,19 +371,20 @@ __device__ __forceinline__ void state_merge(RowState& a, const RowState& b) {
 }
 
 // KL term (Eq. klv): the M best (value, draft index) pairs offered to one row
-// segment, ordered as the top-K orders them (larger value first, equal
-// values by the smaller index); n counts the finite values offered, so
-// n > M means some were dropped, every one of them at most v[M - 1].  Only
-// finite values take part (a token of zero target probability is not a
-// member).
+// segment (M = kLmSegM) or kept by one slice (M = kLmKlM), ordered as the
+// top-K orders them (larger value first, equal values by the smaller index);
+// n counts the finite values offered, so n > M means some were dropped,
+// every one of them at most v[M - 1].  Only finite values take part (a token
+// of zero target probability is not a member).
+template <int M>
 struct KlList {
-  float v[kLmKlM];
-  int i[kLmKlM];
+  float v[M];
+  int i[M];
   int n;
 
   __device__ __forceinline__ void init() {
 #pragma unroll
-    for (int j = 0; j < kLmKlM; ++j) {
+    for (int j = 0; j < M; ++j) {
       v[j] = -INFINITY;
       i[j] = 0x7FFFFFFF;
     }
@@ -394,11 +396,11 @@ struct KlList {
   __device__ __forceinline__ void offer(float x, int idx) {
     if (!(x > -INFINITY)) return;
     ++n;
-    if (!beats(x, idx, v[kLmKlM - 1], i[kLmKlM - 1])) return;
-    v[kLmKlM - 1] = x;
-    i[kLmKlM - 1] = idx;
+    if (!beats(x, idx, v[M - 1], i[M - 1])) return;
+    v[M - 1] = x;
+    i[M - 1] = idx;
 #pragma unroll
-    for (int j = kLmKlM - 1; j > 0; --j) {  // one bubble pass keeps the list ordered
+    for (int j = M - 1; j > 0; --j) {  // one bubble pass keeps the list ordered
       const bool up = beats(v[j], i[j], v[j - 1], i[j - 1]);
       const float tv = v[j];
       const int ti = i[j];
@@ -409,7 +411,7 @@ struct KlList {
     }
   }
   // an upper bound of every dropped value (-inf: nothing dropped)
-  __device__ __forceinline__ float bound() const { return n > kLmKlM ? v[kLmKlM - 1] : -INFINITY; }
+  __device__ __forceinline__ float bound() const { return n > M ? v[M - 1] : -INFINITY; }
 };
 
 // Fold eight consecutive columns c .. c+7 of row r (values x; columns past
@@ -423,7 +425,7 @@ struct KlList {
 // call is made once per four mapped columns.
 template <bool TARGET, bool KL>
 __device__ __forceinline__ void fold8(const LmFwdArgs& a, const float (&x)[8], uint32_t r, int c, int nvalid,
-                                      float inv_t, float c2, RowState& st, int& cg, uint4& cw, KlList& kl) {
+                                      float inv_t, float c2, RowState& st, int& cg, uint4& cw, KlList<kLmSegM>& kl) {
   float cm = x[0];
 #pragma unroll
   for (int k = 1; k < 8; ++k) cm = fmaxf(cm, x[k]);
@@ -511,7 +513,7 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
   const float inv_t = TARGET ? a.inv_tp : a.inv_tq;
   const float c2 = inv_t * kLog2e;
   RowState st[2] = {empty_state(), empty_state()};
-  KlList kl[2];
+  KlList<kLmSegM> kl[2];
   if (TARGET && KL) {
     kl[0].init();
     kl[1].init();
@@ -553,15 +555,15 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
     }
   }
   RowState* red = reinterpret_cast<RowState*>(T);  // [TM rows][4 segments]
-  LmKlEntry* klred = reinterpret_cast<LmKlEntry*>(red + TM * 4);  // [TM rows][4 segments][kLmKlM]
-  float* klbnd = reinterpret_cast<float*>(klred + TM * 4 * kLmKlM);  // [TM rows][4 segments]
+  LmKlEntry* klred = reinterpret_cast<LmKlEntry*>(red + TM * 4);  // [TM rows][4 segments][kLmSegM]
+  float* klbnd = reinterpret_cast<float*>(klred + TM * 4 * kLmSegM);  // [TM rows][4 segments]
 #pragma unroll
   for (int rd = 0; rd < 2; ++rd) {
     const int q = (hb * 128 + rd * 64 + lane) * 4 + seg;
     red[q] = st[rd];
     if (TARGET && KL) {
 #pragma unroll
-      for (int j = 0; j < kLmKlM; ++j) klred[q * kLmKlM + j] = LmKlEntry{kl[rd].v[j], kl[rd].i[j]};
+      for (int j = 0; j < kLmSegM; ++j) klred[q * kLmSegM + j] = LmKlEntry{kl[rd].v[j], kl[rd].i[j]};
       klbnd[q] = kl[rd].bound();
     }
   }
@@ -569,7 +571,7 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
   if (TARGET && KL && threadIdx.x < TM && row0 + threadIdx.x < a.R) {
     // the slice's list: the best kLmKlM of its four segments' lists; its
     // bound covers what the segments dropped and what this merge drops
-    KlList m;
+    KlList<kLmKlM> m;
     m.init();
     float bnd = -INFINITY;
 #pragma unroll 1
@@ -577,8 +579,8 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
       const int q = threadIdx.x * 4 + sg;
       bnd = fmaxf(bnd, klbnd[q]);
 #pragma unroll
-      for (int j = 0; j < kLmKlM; ++j) {
-        const LmKlEntry e = klred[q * kLmKlM + j];
+      for (int j = 0; j < kLmSegM; ++j) {
+        const LmKlEntry e = klred[q * kLmSegM + j];
         m.offer(e.val, e.idx);
       }
     }

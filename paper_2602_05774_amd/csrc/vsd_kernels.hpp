@@ -156,9 +156,9 @@ struct LmPartial {
 };
 
 // Top-K renormalised KL term on the fused head: every row segment of the
-// target pass keeps its kLmKlM best mapped target logits; a slice's record
-// holds the best kLmKlM of its segments' lists and an upper bound of every
-// value it dropped (-inf: none dropped).
+// target pass keeps its few best mapped target logits; a slice's record
+// holds the best kLmKlM of its four segments' lists and an upper bound of
+// every value they dropped (-inf: none dropped).
 constexpr int kLmKlM = 8;
 struct LmKlEntry {
   float val;                 // raw target logit
