@@ -70,11 +70,13 @@
  *   call returns a non-zero vsd_status, launches nothing and writes nothing.
  *   vsd_last_error() then holds a message naming the offending argument.
  *   Data errors only visible on the device (a token outside [-1, v_draft), a
- *   d2t entry outside [0, v_target), a depth outside [1, L]) make the kernels
- *   skip the offending access and atomically store the first VSD_DEVERR_* code
- *   into *device_error (a slot the caller zeroes beforehand; the library only
- *   ever replaces 0 by a non-zero code).  The outputs of such a call are
- *   unspecified.  A failed HIP launch returns VSD_ERR_HIP.
+ *   d2t entry outside [0, v_target), a depth outside [1, L]) never make a
+ *   kernel access memory outside the arrays it was given (the offending
+ *   access is skipped, clamped into the array, or answered with zero by the
+ *   hardware range check of a row's buffer descriptor), and the first
+ *   VSD_DEVERR_* code is stored atomically into *device_error (a slot the
+ *   caller zeroes beforehand; the library only ever replaces 0 by a non-zero
+ *   code).  The outputs of such a call are unspecified.  A failed HIP launch returns VSD_ERR_HIP.
  *
  * Determinism
  * -----------

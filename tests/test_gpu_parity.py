@@ -293,6 +293,16 @@ def test_device_errors_are_reported_without_faults():
     s3 = vsd.sample_paths(prob, inp["X"], inp["Y"], bad_map, None, 1.0, 1.0, 0, 0)
     torch.cuda.synchronize()
     assert int(s3.device_error.item()) == 2
+    log("[err] map entries out of range with the KL term (gathers through the map)")
+    kl = params_of(cfg, kl_weight=0.5, kl_topk=4)
+    for bad_val in (cfg.v_target + 1, -7, 0x40000000, -0x7FFFFFF0):
+        bad_map = inp["d2t"].clone()
+        bad_map[3] = bad_val
+        sc_kl = vsd.score_paths(prob, kl, inp["X"], inp["Y"], *smp[:3], bad_map)
+        _, sc_1p = vsd.sample_score_paths(prob, kl, inp["X"], inp["Y"], bad_map, None, 0, 0)
+        torch.cuda.synchronize()
+        assert int(sc_kl.device_error.item()) == 2, bad_val
+        assert int(sc_1p.device_error.item()) == 2, bad_val
     log("[err] depth out of range")
     depth = torch.tensor([2, 9], dtype=torch.int32, device=DEV)
     s4 = vsd.sample_paths(prob, inp["X"], inp["Y"], inp["d2t"], depth, 1.0, 1.0, 0, 0)
