@@ -10,7 +10,8 @@ C3-recipe positions at the full vocabularies (the residual runs over the whole
 target vocabulary, unmapped tokens included), C4-recipe positions (ragged,
 peaked, T_q = 0.5), ragged and odd vocabulary sizes, maps that are not ascending (in random
 order, and ascending but for a few exchanges), equal models (every token
-kept).  At the full C3 size the mean accepted length over all paths matches
+kept); every path of the full C2 and C4 batches, with the oracle's own draft
+paths.  At the full C3 size the mean accepted length over all paths matches
 the mean expected accepted length sum_k S_k from scoring (the Monte-Carlo
 cross-check of Eq. accepted_len_cond), and the draws are deterministic.
 """
@@ -131,3 +132,71 @@ def test_full_size_mean_matches_expected_accepted_length():
     # with a replacement exactly when fewer than L tokens are kept
     res = a.resample_tok.cpu().numpy()
     assert np.array_equal(res >= 0, acc < cfg.L)
+
+
+@pytest.mark.parametrize("name", ["C2", "C4"])
+def test_full_batch_every_path(name):
+    """Every path of the full C2 and C4 batches: the oracle draws its own
+    draft paths (compared bit-exactly with the GPU's), verifies them and the
+    accepted lengths and replacements are compared exactly, under the same
+    near-tie exclusions as above (capped at 0.2 % of the paths)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from oracle import reference
+    from tests.gpu_common import oracle_threads
+    cfg = CONFIGS[name]
+    params = params_of(cfg)
+    prob = problem_of(cfg)
+    inp = make_inputs(cfg, DEV)
+    gpu = run_step(cfg, inp, params)
+    sc = gpu["score"]
+    ver = vsd.verify_paths(prob, params, inp["X"], inp["Y"], sc, inp["d2t"], inp["valid_depth"],
+                           cfg.philox_seed, cfg.philox_offset)
+    torch.cuda.synchronize()
+    assert int(ver.device_error.item()) == 0 and int(sc.device_error.item()) == 0
+    N, L = cfg.N, cfg.L
+    acc_g = ver.accept_len.cpu().numpy()
+    res_g = ver.resample_tok.cpu().numpy()
+    tok_g = gpu["tokens"][0].cpu().numpy().reshape(-1, N, L)
+    d2t = None if inp["d2t"] is None else inp["d2t"].cpu().numpy()
+    depth_all = (np.full((cfg.P, N), L) if inp["valid_depth"] is None
+                 else inp["valid_depth"].reshape(-1, N).cpu().numpy())
+    excused = 0
+    chunk = 128
+    with ThreadPoolExecutor(oracle_threads()) as ex:
+        for p0 in range(0, cfg.P, chunk):
+            positions = list(range(p0, min(cfg.P, p0 + chunk)))
+            rows = (np.asarray(positions)[:, None] * N * L + np.arange(N * L)[None]).reshape(-1)
+            X = rows_to_host(inp["X"], rows, cfg.v_draft).reshape(len(positions), N, L, -1)
+            Y = rows_to_host(inp["Y"], rows, cfg.v_target).reshape(len(positions), N, L, -1)
+
+            def one(k):
+                pos = positions[k]
+                Ym = Y[k] if d2t is None else Y[k][..., d2t]
+                toks = reference.sample_position(X[k], Ym, depth_all[pos], pos * N * L, params.temp_draft,
+                                                 params.temp_target, cfg.philox_seed, cfg.philox_offset)
+                return (toks[0],) + verify.verify_position(X[k], Y[k], d2t, depth_all[pos], toks[0], pos * N * L,
+                                                           params.temp_draft, params.temp_target,
+                                                           cfg.philox_seed, cfg.philox_offset)
+
+            for k, (tok_o, acc, res, margin, gap) in enumerate(ex.map(one, range(len(positions)))):
+                pos = positions[k]
+                assert np.array_equal(tok_g[pos], tok_o), f"{name} position {pos}: draft paths differ"
+                for s in range(N):
+                    path = pos * N + s
+                    if margin[s] < MARGIN:
+                        excused += 1
+                        continue
+                    assert acc_g[path] == acc[s], f"{name} path {path}: accept_len gpu {acc_g[path]} oracle {acc[s]}"
+                    if gap[s] >= GAP:
+                        assert res_g[path] == res[s], f"{name} path {path}: resample gpu {res_g[path]} oracle {res[s]}"
+                    else:
+                        excused += 1
+            if p0 % 512 == 0:
+                log(f"[verify full] {name}: positions up to {positions[-1]} checked")
+    cap = max(2, int(np.ceil(2e-3 * cfg.P * N)))
+    log(f"[verify full] {name}: {cfg.P * N} paths, {excused} near-ties left out (cap {cap}); "
+        f"mean accepted {acc_g.mean():.3f}")
+    assert excused <= cap
+    del inp, gpu
+    torch.cuda.empty_cache()
