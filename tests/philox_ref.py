@@ -8,8 +8,10 @@ ten-round block function is called on given counters and keys.  Where hipcc
 or the rocRAND header is missing, `available()` is False and the tests that
 need it are skipped.
 """
+import atexit
 import functools
 import os
+import shutil
 import subprocess
 import tempfile
 
@@ -28,7 +30,9 @@ def available():
 
 @functools.lru_cache(maxsize=1)
 def _binary():
-    out = os.path.join(tempfile.mkdtemp(prefix="philox_ref_"), "philox_ref")
+    tmp = tempfile.mkdtemp(prefix="philox_ref_")
+    atexit.register(shutil.rmtree, tmp, True)
+    out = os.path.join(tmp, "philox_ref")
     subprocess.run([HIPCC, "-O1", "-std=c++17", f"-I{os.path.join(ROCM, 'include')}", SRC, "-o", out],
                    check=True, capture_output=True, timeout=300)
     return out
