@@ -13,7 +13,9 @@ per-family rows).
     shift tables, draws bit-identical tokens; scoring and both gradients then
     match the oracle under the usual bars.  Cases: C1 (fp32, shared
     vocabulary), the C3 recipe at full vocabularies (mapped), the C4 recipe
-    (ragged, peaked bf16 with ties, T_q = 0.5), and C3 with the KL term.
+    (ragged, peaked bf16 with ties, T_q = 0.5), and C3 with the KL term;
+    sixteen positions of C3 and of C4 (with the KL term) at their full
+    vocabularies.
 """
 import numpy as np
 import pytest
@@ -149,6 +151,16 @@ def test_rollout_mapped_full_vocabularies():
 def test_rollout_ragged_peaked():
     cfg = scaled("C4", B=1, T=2, v_draft=4000, v_target=4000)
     check_rollout(cfg, params_of(cfg, loss_scale=0.5), "C4s ctx")
+
+
+@pytest.mark.parametrize("name", ["C3", "C4"])
+def test_rollout_sixteen_positions_full_vocabularies(name):
+    """Sixteen positions of the C3 and C4 recipes at their full
+    vocabularies (C4: ragged, peaked bf16 rows with ties, T_q = 0.5, and the
+    KL term on)."""
+    cfg = scaled(name, B=1, T=16)
+    params = params_of(cfg) if name == "C3" else params_of(cfg, kl_weight=0.3, kl_topk=10)
+    check_rollout(cfg, params, f"{name} 16-position ctx")
 
 
 def test_rollout_mapped_with_kl():
