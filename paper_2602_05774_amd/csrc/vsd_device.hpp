@@ -142,8 +142,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* row, uint
 }
 __device__ __forceinline__ uint32_t row_bytes(const float*, int n) { return (uint32_t)n * 4u; }
 __device__ __forceinline__ uint32_t row_bytes(const bf16_t*, int n) { return (uint32_t)n * 2u; }
-// raw element idx of the row (the offset wraps modulo 2^32 for indices of
-// 2^31 and above: still inside the row's range check)
+// raw element idx of the row (the byte offset is formed modulo 2^32; any
+// value of it is inside the row or answered with zero by the range check)
 __device__ __forceinline__ void buf_gather(__amdgpu_buffer_rsrc_t r, uint32_t idx, float& out) {
   out = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(idx * 4u), 0, 0));
 }
