@@ -54,6 +54,8 @@ static_assert(2 * 64 * LDT * 4 <= kLdsBytes, "two 64-row epilogue buffers fit th
 static_assert(kLmTile == TN && kLmTile == TM, "tile width shared with the host");
 static_assert(2 * kStageNT * 2 <= kLdsBytes, "two direct-loaded NT stages fit");
 constexpr int kLmSegM = 6;                   // KL term: list length of one row segment
+static_assert(kLmRedoM >= kMaxTopK, "a recompute record holds every member a slice can have");
+static_assert(TM * 4 * kLmRedoM * 8 <= kLdsBytes, "the recompute's segment lists fit");
 static_assert(TM * 4 * (32 + kLmSegM * 8 + 4) <= kLdsBytes, "the slice merge's row states and KL lists fit");
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
@@ -99,6 +101,12 @@ struct Core {
   int64_t lda, ldb;
   int64_t row0, nrow;
   int col0, ncol, K;
+  // NT only: tile row i reads row arow[i] of A and tile column j row
+  // brow[j] of B (null: i and j themselves); a B row index outside
+  // [0, brow_n) reads row 0 (its results are the caller's to discard)
+  const int32_t* arow = nullptr;
+  const int32_t* brow = nullptr;
+  int brow_n = 0;
 
   __device__ __forceinline__ uint4 load_a(int64_t r, int k) const {
     if (r >= nrow) return make_uint4(0, 0, 0, 0);
@@ -187,8 +195,15 @@ struct Core {
     for (int j = 0; j < 4; ++j) {
       const int r = w * 32 + j * 8 + lr;
       const int cg = (lc ^ r) & 7;
-      s.a[j] = A + min(row0 + r, nrow - 1) * lda + cg * 8;
-      s.b[j] = B + (int64_t)min(col0 + r, ncol - 1) * ldb + cg * 8;
+      int64_t ra = min(row0 + r, nrow - 1);
+      int rb = min(col0 + r, ncol - 1);
+      if (arow != nullptr) ra = arow[ra];
+      if (brow != nullptr) {
+        rb = brow[rb];
+        rb = (uint32_t)rb < (uint32_t)brow_n ? rb : 0;
+      }
+      s.a[j] = A + ra * lda + cg * 8;
+      s.b[j] = B + (int64_t)rb * ldb + cg * 8;
     }
     return s;
   }
@@ -584,10 +599,10 @@ __device__ void lm_pass(const LmFwdArgs& a, int64_t row0, int slice, bf16_t* lds
         m.offer(e.val, e.idx);
       }
     }
-    const int64_t rec = (row0 + threadIdx.x) * a.nslice_t + slice;
+    const int64_t row = row0 + threadIdx.x;
 #pragma unroll
-    for (int j = 0; j < kLmKlM; ++j) a.kl_part[rec * kLmKlM + j] = LmKlEntry{m.v[j], m.i[j]};
-    a.kl_bound[rec] = fmaxf(bnd, m.bound());
+    for (int j = 0; j < kLmKlM; ++j) a.kl_part[row * a.kl_stride + slice * kLmKlM + j] = LmKlEntry{m.v[j], m.i[j]};
+    a.kl_bound[row * a.nslice_t + slice] = fmaxf(bnd, m.bound());
   }
   if (threadIdx.x < TM && row0 + threadIdx.x < a.R) {
     RowState m = red[threadIdx.x * 4];
@@ -647,19 +662,6 @@ __device__ __forceinline__ float wave_dot(const bf16_t* x, const bf16_t* y, int 
   return wave_sum(acc);
 }
 
-// Dot product of two bf16 rows of length H by one lane (H % 8 == 0).
-__device__ __forceinline__ float lane_dot(const bf16_t* x, const bf16_t* y, int H) {
-  float acc = 0.0f;
-  for (int k = 0; k < H; k += 8) {
-    float xv[8], yv[8];
-    load8(x + k, xv);
-    load8(y + k, yv);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc = fmaf(xv[j], yv[j], acc);
-  }
-  return acc;
-}
-
 // The KL term of row r from its members in tk (after finish()): the draft
 // logits at the members by dot products, then the row term (Eq. klv).
 __device__ void lm_kl_row(const LmCombineArgs& a, const WaveTopK& tk, int64_t r, int lane) {
@@ -680,11 +682,31 @@ __device__ void lm_kl_row(const LmCombineArgs& a, const WaveTopK& tk, int64_t r,
                  a.kl_grad + r * a.kl_k, a.kl_row + r, lane);
 }
 
+// Offer ne (value, draft index) entries to tk, 8 per lane per round
+// (non-finite values take no part).
+__device__ __forceinline__ void offer_entries(WaveTopK& tk, const LmKlEntry* ent, int ne, int lane) {
+  typedef __attribute__((ext_vector_type(8))) int i32x8;  // a register vector, never a private array
+  for (int e0 = 0; e0 < ne; e0 += 8 * kWave) {
+    float x[8];
+    i32x8 ix;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e = e0 + lane * 8 + k;
+      const LmKlEntry en = e < ne ? ent[e] : LmKlEntry{-INFINITY, 0x7FFFFFFF};
+      x[k] = en.val;
+      ix[k] = en.idx;
+      bits |= en.val > -INFINITY ? (1u << k) : 0u;
+    }
+    tk.offer8(x, 0, bits, [&](int k) { return ix[k]; }, lane);
+  }
+}
+
 // Merge the slices of both models, write tokens (sampling) and the row
 // statistics.  One wavefront per row.  With the KL term, the slices' lists
 // are merged into the row's top-K set: exact unless some slice dropped a
-// value reaching the set's K-th value (then kl_flag[r] = 1 and
-// k_lm_kl_fallback recomputes the row).
+// value reaching the set's K-th value; such a row is appended to kl_list
+// and its term is left to k_lm_kl_redo and k_lm_kl_redo_select.
 template <bool KL>
 __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
   __shared__ float kl_bv[KL ? 4 * kTopKCap : 1];
@@ -720,7 +742,6 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
       }
       if (lane == 0) {
         a.kl_row[r] = 0.0f;
-        a.kl_flag[r] = 0;
       }
     }
     return;
@@ -793,22 +814,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     WaveTopK tk;
     tk.init(kl_bv + wave * kTopKCap, kl_bi + wave * kTopKCap, a.kl_k);
     const int ne = a.nslice_t * kLmKlM;
-    const LmKlEntry* ent = a.kl_part + r * ne;
-    typedef __attribute__((ext_vector_type(8))) int i32x8;  // a register vector, never a private array
-    for (int e0 = 0; e0 < ne; e0 += 8 * kWave) {
-      float x[8];
-      i32x8 ix;
-      uint32_t bits = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int e = e0 + lane * 8 + k;
-        const LmKlEntry en = e < ne ? ent[e] : LmKlEntry{-INFINITY, 0x7FFFFFFF};
-        x[k] = en.val;
-        ix[k] = en.idx;
-        bits |= en.val > -INFINITY ? (1u << k) : 0u;
-      }
-      tk.offer8(x, 0, bits, [&](int k) { return ix[k]; }, lane);
-    }
+    offer_entries(tk, a.kl_part + r * a.kl_stride, ne, lane);
     tk.finish(lane);
     const float tau = tk.n >= a.kl_k ? tk.bv[a.kl_k - 1] : -INFINITY;
     float bmax = -INFINITY;
@@ -817,38 +823,118 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombineArgs a) {
     // a dropped value at or above the K-th member (or any, with fewer than K
     // members) might belong to the set
     const bool redo = tk.n >= a.kl_k ? bmax >= tau : bmax > -INFINITY;
-    if (lane == 0) a.kl_flag[r] = redo ? 1 : 0;
-    if (!redo) lm_kl_row(a, tk, r, lane);
+    if (redo) {
+      if (lane == 0) a.kl_list[atomicAdd(a.kl_count, 1)] = (int)r;
+    } else {
+      lm_kl_row(a, tk, r, lane);
+    }
   }
 }
 
-// The KL term of the rows flagged by k_lm_combine, from every mapped target
-// logit of the row (each lane a dot product per draft index), exactly.  One
-// wavefront per row; unflagged rows return at once.
-__global__ __launch_bounds__(256) void k_lm_kl_fallback(LmCombineArgs a) {
+__global__ void k_lm_kl_reset(int32_t* count) {
+  if (threadIdx.x == 0) *count = 0;
+}
+
+// Exact recompute of the rows k_lm_combine<KL> listed.  A workgroup takes
+// 256 listed rows (tile row i: H_t row kl_list[row0 + i]) and one of
+// kl_nslice slices of the draft vocabulary's 256-column tiles (tile column
+// j: draft index v, W_t row d2t[v]).  Operands, K order and matrix-core
+// arithmetic are those of the forward's target tiles, so each value equals
+// the one the forward formed for (row, d2t[v]).  Each thread keeps the
+// kLmRedoM best (value, v) of its row segment (64 columns of every tile),
+// which holds every member of the row's top-K that lies there, since K <=
+// kLmRedoM; the four segments of a row merge into the slice's record,
+// written over the row's (already consumed) slice lists in kl_part.
+// Workgroups past the listed rows return at once (the grid is sized for
+// every row listed).
+__global__ __launch_bounds__(kThreads, 1) void k_lm_kl_redo(LmCombineArgs a) {
+  __shared__ __align__(16) unsigned char smem[kLdsBytes];
+  const int n = *a.kl_count;
+  const int nrt = (int)((a.R + TM - 1) / TM);
+  int rt, sl;
+  tile_of(blockIdx.x, nrt, a.kl_nslice, rt, sl);
+  const int64_t row0 = (int64_t)rt * TM;
+  if (row0 >= n) return;
+  bf16_t* lds = reinterpret_cast<bf16_t*>(smem);
+  float* T = reinterpret_cast<float*>(smem);
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hb = w & 1, seg = w >> 1;
+  const int ntiles = (a.Vd + TN - 1) / TN;
+  const int per = (ntiles + a.kl_nslice - 1) / a.kl_nslice;
+  const int t_end = min(ntiles, (sl + 1) * per);
+  KlList<kLmRedoM> kl[2];
+  kl[0].init();
+  kl[1].init();
+  Core<false> g{static_cast<const bf16_t*>(a.Ht), static_cast<const bf16_t*>(a.Wt), a.H, a.H, row0, n, 0, a.Vd,
+                a.H};
+  g.arow = a.kl_list;
+  g.brow = a.d2t;
+  g.brow_n = a.Vt;
+  for (int tile = sl * per; tile < t_end; ++tile) {
+    g.col0 = tile * TN;
+    f32x16 acc[8];
+    g.run(lds, acc);
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) {
+      if (rd == 0)
+        spill<0>(acc, T);
+      else
+        spill<1>(acc, T);
+      __syncthreads();
+      if (row0 + hb * 128 + rd * 64 + lane < n) {
+        const float* src = T + (hb * 64 + lane) * LDT + seg * 64;
+#pragma unroll 1
+        for (int ch = 0; ch < 8; ++ch) {
+          const int c = g.col0 + seg * 64 + ch * 8;
+          if (c >= a.Vd) break;
+          float x[8];
+          load8(src + ch * 8, x);
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (c + k < a.Vd) kl[rd].offer(x[k], c + k);
+        }
+      }
+      __syncthreads();  // the buffers are the next round's (or the next GEMM's)
+    }
+  }
+  LmKlEntry* klred = reinterpret_cast<LmKlEntry*>(smem);  // [TM rows][4 segments][kLmRedoM]
+#pragma unroll
+  for (int rd = 0; rd < 2; ++rd) {
+    const int q = (hb * 128 + rd * 64 + lane) * 4 + seg;
+#pragma unroll
+    for (int j = 0; j < kLmRedoM; ++j) klred[q * kLmRedoM + j] = LmKlEntry{kl[rd].v[j], kl[rd].i[j]};
+  }
+  __syncthreads();
+  if (threadIdx.x < TM && row0 + threadIdx.x < n) {
+    KlList<kLmRedoM> m;
+    m.init();
+#pragma unroll 1
+    for (int e = 0; e < 4 * kLmRedoM; ++e) {
+      const LmKlEntry en = klred[threadIdx.x * 4 * kLmRedoM + e];
+      m.offer(en.val, en.idx);
+    }
+    const int64_t r = a.kl_list[row0 + threadIdx.x];
+    LmKlEntry* rec = a.kl_part + r * a.kl_stride + sl * kLmRedoM;
+#pragma unroll
+    for (int j = 0; j < kLmRedoM; ++j) rec[j] = LmKlEntry{m.v[j], m.i[j]};
+  }
+}
+
+// The KL term of each listed row from its slice records: an exact wavefront
+// top-K over the records' entries, then the row term.  One wavefront per
+// listed row; the grid is sized for every row listed.
+__global__ __launch_bounds__(256) void k_lm_kl_redo_select(LmCombineArgs a) {
   __shared__ float kl_bv[4 * kTopKCap];
   __shared__ int kl_bi[4 * kTopKCap];
   const int lane = threadIdx.x & 63;
   const int wave = wave_id();
-  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
-  if (r >= a.R || a.kl_flag[r] == 0) return;
-  const bf16_t* ht = static_cast<const bf16_t*>(a.Ht) + r * a.H;
-  const bf16_t* Wt = static_cast<const bf16_t*>(a.Wt);
+  const int64_t f = (int64_t)blockIdx.x * 4 + wave;
+  if (f >= *a.kl_count) return;
   WaveTopK tk;
   tk.init(kl_bv + wave * kTopKCap, kl_bi + wave * kTopKCap, a.kl_k);
-  for (int v0 = 0; v0 < a.Vd; v0 += 8 * kWave) {
-    float y[8];
-    uint32_t bits = 0;
-#pragma unroll 1
-    for (int k = 0; k < 8; ++k) {
-      const int v = v0 + lane * 8 + k;
-      const int t = v < a.Vd ? (a.d2t != nullptr ? a.d2t[v] : v) : -1;
-      const bool ok = (uint32_t)t < (uint32_t)a.Vt;
-      y[k] = ok ? lane_dot(ht, Wt + (int64_t)t * a.H, a.H) : -INFINITY;
-      bits |= ok && y[k] > -INFINITY ? (1u << k) : 0u;
-    }
-    tk.offer8(y, v0 + lane * 8, bits, [](int col) { return col; }, lane);
-  }
+  const int64_t r = a.kl_list[f];
+  offer_entries(tk, a.kl_part + r * a.kl_stride, a.kl_nslice * kLmRedoM, lane);
   tk.finish(lane);
   lm_kl_row(a, tk, r, lane);
 }
@@ -1032,8 +1118,17 @@ hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_lm_kl_fallback(const LmCombineArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_lm_kl_fallback, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
+hipError_t launch_lm_kl_reset(const LmCombineArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_lm_kl_reset, dim3(1), dim3(64), 0, s, a.kl_count);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_kl_redo(const LmCombineArgs& a, hipStream_t s) {
+  const unsigned nrt = (unsigned)((a.R + TM - 1) / TM);
+  hipLaunchKernelGGL(k_lm_kl_redo, dim3(nrt * (unsigned)a.kl_nslice), dim3(kThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_lm_kl_redo_select, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

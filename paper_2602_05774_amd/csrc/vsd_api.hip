@@ -179,14 +179,15 @@ vsd_status hip_fail(hipError_t e, const char* what) {
 }
 
 struct WorkspaceLayout {
-  size_t la, lq, loss, klrow, inv, part, klpart, klbound, klflag, total;
+  size_t la, lq, loss, klrow, inv, part, klpart, klbound, klcount, kllist, total;
 };
 
 // la [R,3], lq [R,3], loss [P], KL row terms [R] fp32; the inverse map
 // [v_target] int32 (fused LM head draws, verification); fused LM head also
 // the slice partials [R, nslice_t + nslice_d] and, for the KL term, the
-// target slices' lists [R, nslice_t, kLmKlM], their bounds [R, nslice_t] and
-// the per-row recompute flags [R].
+// target slices' lists [R, lm_kl_stride] (a recomputed row's records take
+// their place), their bounds [R, nslice_t] and the count [1] and list [R]
+// of the rows to recompute.
 WorkspaceLayout workspace_layout(const vsd_dims* d) {
   const int64_t R = rows_of(d);
   const int64_t P = (int64_t)d->B * d->T;
@@ -197,14 +198,16 @@ WorkspaceLayout workspace_layout(const vsd_dims* d) {
   w.klrow = w.loss + align_up((size_t)P * sizeof(float));
   w.inv = w.klrow + align_up((size_t)R * sizeof(float));
   w.part = w.inv + align_up((size_t)d->v_target * sizeof(int32_t));
-  w.total = w.klpart = w.klbound = w.klflag = w.part;
+  w.total = w.klpart = w.klbound = w.klcount = w.kllist = w.part;
   if (d->hidden_dim > 0) {
     const size_t nst = (size_t)vsd::lm_nslice(d->v_target);
     const size_t nsl = nst + (size_t)vsd::lm_nslice(d->v_draft);
+    const size_t stride = (size_t)vsd::lm_kl_stride(d->v_draft, d->v_target);
     w.klpart = w.part + align_up((size_t)R * nsl * sizeof(vsd::LmPartial));
-    w.klbound = w.klpart + align_up((size_t)R * nst * vsd::kLmKlM * sizeof(vsd::LmKlEntry));
-    w.klflag = w.klbound + align_up((size_t)R * nst * sizeof(float));
-    w.total = w.klflag + align_up((size_t)R * sizeof(int32_t));
+    w.klbound = w.klpart + align_up((size_t)R * stride * sizeof(vsd::LmKlEntry));
+    w.klcount = w.klbound + align_up((size_t)R * nst * sizeof(float));
+    w.kllist = w.klcount + align_up(sizeof(int32_t));
+    w.total = w.kllist + align_up((size_t)R * sizeof(int32_t));
   }
   return w;
 }
@@ -372,6 +375,7 @@ vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_
   f.offset = offset;
   if (kl_on(params)) {
     f.kl_part = reinterpret_cast<vsd::LmKlEntry*>(ws + wl.klpart);
+    f.kl_stride = vsd::lm_kl_stride(dims->v_draft, dims->v_target);
     f.kl_bound = reinterpret_cast<float*>(ws + wl.klbound);
   }
   e = vsd::launch_lm_fwd(f, s);
@@ -406,17 +410,24 @@ vsd_status lm_forward(const vsd_dims* dims, const vsd_params* params, const vsd_
     c.kl_k = params->kl_topk;
     c.kl_part = f.kl_part;
     c.kl_bound = f.kl_bound;
-    c.kl_flag = reinterpret_cast<int32_t*>(ws + wl.klflag);
+    c.kl_count = reinterpret_cast<int32_t*>(ws + wl.klcount);
+    c.kl_list = reinterpret_cast<int32_t*>(ws + wl.kllist);
+    c.kl_stride = f.kl_stride;
+    c.kl_nslice = vsd::lm_redo_nslice(dims->v_draft, dims->v_target);
     c.kl_idx = out->kl_idx;
     c.kl_grad = out->kl_grad;
     c.kl_row = kl_row;
     c.kl_gscale = params->loss_scale * params->kl_weight / (float)dims->N / params->temp_draft;
   }
+  if (kl_on(params)) {
+    e = vsd::launch_lm_kl_reset(c, s);
+    if (e != hipSuccess) return hip_fail(e, "k_lm_kl_reset launch");
+  }
   e = vsd::launch_lm_combine(c, s);
   if (e != hipSuccess) return hip_fail(e, "k_lm_combine launch");
   if (kl_on(params)) {
-    e = vsd::launch_lm_kl_fallback(c, s);
-    if (e != hipSuccess) return hip_fail(e, "k_lm_kl_fallback launch");
+    e = vsd::launch_lm_kl_redo(c, s);
+    if (e != hipSuccess) return hip_fail(e, "k_lm_kl_redo launch");
   }
   return VSD_OK;
 }

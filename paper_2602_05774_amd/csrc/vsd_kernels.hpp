@@ -165,6 +165,23 @@ struct LmKlEntry {
   int32_t idx;               // its draft index
 };
 
+// A row the slice lists cannot decide is recomputed exactly over slices of
+// the draft vocabulary, whose records (kLmRedoM entries each) take the place
+// of the row's target-slice lists once the combine has read them: as many
+// slices as fit there (at least one; the row's region is padded when one
+// does not fit).
+constexpr int kLmRedoM = 16;
+inline int lm_redo_nslice(int Vd, int Vt) {
+  const int tiles = (Vd + kLmTile - 1) / kLmTile;
+  const int fit = lm_nslice(Vt) * kLmKlM / kLmRedoM;
+  return fit < 1 ? 1 : fit < tiles ? fit : tiles;
+}
+// LmKlEntry records per row of the KL lists' region.
+inline int lm_kl_stride(int Vd, int Vt) {
+  const int lists = lm_nslice(Vt) * kLmKlM, redo = lm_redo_nslice(Vd, Vt) * kLmRedoM;
+  return lists > redo ? lists : redo;
+}
+
 struct LmFwdArgs {
   const void* Hd;            // [R, H] bf16
   const void* Ht;            // [R, H] bf16
@@ -172,9 +189,11 @@ struct LmFwdArgs {
   const void* Wt;            // [Vt, H] bf16
   const int32_t* inv;        // [Vt] draft index of each target column (-1: none); null = identity
   LmPartial* part;           // [R, nslice_t + nslice_d], target slices first
-  LmKlEntry* kl_part;        // KL term: [R, nslice_t, kLmKlM] slice lists, or null (term off)
+  LmKlEntry* kl_part;        // KL term: [R, kl_stride] rows of nslice_t slice lists of kLmKlM, or
+                             // null (term off)
   float* kl_bound;           // KL term: [R, nslice_t] bound of the dropped values
   int64_t R;
+  int32_t kl_stride;         // KL term: LmKlEntry records per row of kl_part
   int32_t H, Vd, Vt;
   int32_t nslice_t, nslice_d;
   int32_t sample;            // 0: log-sum-exp only (scoring given tokens)
@@ -203,9 +222,13 @@ struct LmCombineArgs {
   float inv_tq, inv_tp;
   // top-K renormalised KL term (kl_k > 0 turns it on)
   int32_t kl_k;
-  const LmKlEntry* kl_part;  // [R, nslice_t, kLmKlM]
+  LmKlEntry* kl_part;        // [R, kl_stride]: the forward's slice lists; rows listed for the
+                             // recompute then hold its kl_nslice records of kLmRedoM
+  int32_t kl_stride;         // lm_kl_stride(Vd, Vt)
   const float* kl_bound;     // [R, nslice_t]
-  int32_t* kl_flag;          // [R] 1: the slice lists may have dropped a member (exact recompute)
+  int32_t* kl_count;         // [1] rows the slice lists could not decide (reset before the combine)
+  int32_t* kl_list;          // [R] those rows, in the order they were found
+  int32_t kl_nslice;         // lm_redo_nslice(Vd, Vt)
   int32_t* kl_idx;           // [R, kl_k]
   float* kl_grad;            // [R, kl_k]
   float* kl_row;             // [R]
@@ -253,7 +276,8 @@ struct LmGemmNNArgs {
 hipError_t launch_lm_inv(const int32_t* d2t, int Vd, int Vt, int32_t* inv, int32_t* err, hipStream_t s);
 hipError_t launch_lm_fwd(const LmFwdArgs& a, hipStream_t s);
 hipError_t launch_lm_combine(const LmCombineArgs& a, hipStream_t s);
-hipError_t launch_lm_kl_fallback(const LmCombineArgs& a, hipStream_t s);
+hipError_t launch_lm_kl_reset(const LmCombineArgs& a, hipStream_t s);
+hipError_t launch_lm_kl_redo(const LmCombineArgs& a, hipStream_t s);
 hipError_t launch_lm_bwd(const LmBwdArgs& a, hipStream_t s);
 
 // Range check of a draft-to-target map: the first entry outside [0, Vt) is

@@ -14,8 +14,8 @@ Cases: a scaled C5 batch checked on every position (one-pass and scoring on
 the oracle's tokens); K = 1 and K = 16 with ragged depths and temperatures;
 a head whose first 64 target columns carry much larger weights, so that a
 row's best logits crowd one segment of the forward's column tiles and the
-row goes through the exact recompute; the full 49 152 x 4096 shape on 32
-positions.
+row goes through the exact recompute (48 rows, and 768 rows over three
+row tiles of it); the full 49 152 x 4096 shape on 32 positions.
 """
 import numpy as np
 import pytest
@@ -162,15 +162,29 @@ def test_kl_ragged_tempered(K):
                     f"C5 KL K={K}")
 
 
-def test_kl_crowded_segment_goes_through_the_exact_recompute():
+@pytest.mark.parametrize("vocab", [(3000, 9000), (900, 1000)])
+def test_kl_crowded_segment_goes_through_the_exact_recompute(vocab):
     """The first 64 target columns get weights 8x larger: every row's best
     mapped logits crowd the first column segment of the first tile, more
     than a segment's list keeps, so the slice lists cannot decide the set and
-    the row is recomputed from every mapped logit."""
-    cfg = scaled("C5", B=1, T=4, N=4, L=3, v_draft=3000, v_target=9000, hidden=128, seed=62)
+    the row is recomputed from every mapped logit.  With 1000 target columns
+    (one slice) the recompute's record is larger than the row's slice lists
+    and the row's region is padded for it."""
+    cfg = scaled("C5", B=1, T=4, N=4, L=3, v_draft=vocab[0], v_target=vocab[1], hidden=128, seed=62)
     inp = make_inputs(cfg, DEV)
     inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
     check_lmhead_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.7, kl_topk=16), "C5 KL crowded")
+
+
+def test_kl_crowded_many_rows():
+    """As above with 768 rows, every one undecided by the slice lists: the
+    listed rows fill three row tiles of the recompute, whose order in the
+    list varies from call to call while every row's result stays the same."""
+    cfg = scaled("C5", B=2, T=32, N=4, L=3, v_draft=3000, v_target=9000, hidden=128, seed=63)
+    assert cfg.R > 512
+    inp = make_inputs(cfg, DEV)
+    inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
+    check_lmhead_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.7, kl_topk=12), "C5 KL crowded 768")
 
 
 def test_kl_full_size_32_positions():
