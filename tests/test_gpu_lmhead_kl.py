@@ -176,6 +176,18 @@ def test_kl_crowded_segment_goes_through_the_exact_recompute(vocab):
     check_lmhead_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.7, kl_topk=16), "C5 KL crowded")
 
 
+def test_kl_crowded_ragged_tempered():
+    """Crowded rows with ragged depths (masked rows are never listed for the
+    recompute) and temperatures other than 1, K = 16 (the recompute
+    records' length)."""
+    cfg = scaled("C5", B=2, T=4, N=8, L=4, v_draft=2000, v_target=7000, hidden=192, ragged=True,
+                 temp_draft=0.5, temp_target=1.3, seed=64)
+    inp = make_inputs(cfg, DEV)
+    inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
+    check_lmhead_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=1.2, kl_topk=16, loss_scale=0.5),
+                    "C5 KL crowded ragged")
+
+
 def test_kl_crowded_many_rows():
     """As above with 768 rows, every one undecided by the slice lists: the
     listed rows fill three row tiles of the recompute, whose order in the
