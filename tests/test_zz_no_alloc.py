@@ -1,7 +1,8 @@
 """vsd_sample_score_paths_static (no workspace argument: the library's
 static device scratch) against vsd_sample_score_paths with a caller
 workspace, through the C ABI: two calls in a row, the second on a smaller
-input, then a fused LM-head call; every output must be identical (the same
+input, then fused LM-head calls (the second with the KL term on rows that
+need its exact recompute); every output must be identical (the same
 kernels run on the same inputs).  The scratch keeps the previous call's
 contents, so the smaller second call also shows that nothing stale is read.
 """
@@ -26,8 +27,10 @@ def _sources(cfg, inp):
     return inp["X"], inp["Y"]
 
 
-def _check_same(cfg, params, label):
+def _check_same(cfg, params, label, prep=None):
     inp = make_inputs(cfg, DEV)
+    if prep is not None:
+        prep(inp)
     prob = problem_of(cfg)
     X, Y = _sources(cfg, inp)
     kl = params.kl_topk if params.kl_weight > 0 else 0
@@ -63,3 +66,11 @@ def test_static_scratch_matches_the_workspace_call():
     # 3. the fused LM head (slice partials in the scratch)
     cfg3 = scaled("C5", name="na3", B=1, T=4, N=4, L=3, v_draft=3000, v_target=9000, hidden=256)
     _check_same(cfg3, params_of(cfg3), "fused LM head")
+    # 4. the fused LM head with the KL term on crowded rows (the exact
+    #    recompute's list and records in the scratch)
+    cfg4 = scaled("C5", name="na4", B=1, T=4, N=4, L=3, v_draft=3000, v_target=9000, hidden=128, seed=62)
+
+    def crowd(inp):
+        inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
+
+    _check_same(cfg4, params_of(cfg4, kl_weight=0.7, kl_topk=16), "fused LM head, KL, crowded rows", crowd)
