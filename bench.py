@@ -259,6 +259,9 @@ def bench_lm_head(cfg, steps, warmup, dev):
                      "frac": tf(fwd_flop, t_fwd) / MFMA_BF16_PEAK_TFLOPS,
                      "traffic": measured_traffic(cfg.name, "lm_fwd")},
     }
+    rec = profile_record("mfma", cfg.name, "lm_fwd")
+    if rec is not None:  # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs), same sources
+        res["roofline"]["mfma_counters"] = {"busy": rec["mfma_busy"], "clock_GHz": rec["clock_GHz"]}
     del inp, out, ws, grad
     torch.cuda.empty_cache()
     return res
