@@ -178,8 +178,14 @@ struct Core {
   // directly (global_load_lds_dwordx4: lane i's 16 bytes land at the
   // instruction's LDS base + 16 i), 8 rows of 64 K values per instruction;
   // rows are unpadded (128 B) and lane i of a row loads global 16-byte chunk
-  // (i ^ row) & 7, so chunk c of row r sits at position c ^ (r & 7): the
-  // fragment reads of 8 consecutive rows then cover all banks.  Rows past
+  // (i ^ row) & 7, so chunk c of row r sits at position c ^ (r & 7).  The
+  // LDS serves a 16-byte read to 16 lanes at a time from 64 four-byte banks,
+  // so a fragment read of 16 consecutive rows meets each bank twice (rows r
+  // and r + 8 coincide).  A swizzle by (r >> 1) & 7 removes that two-way
+  // conflict and halves the LDS busy cycles, but left the forward's time
+  // unchanged and raised what it fetches from beyond L2 by about 1.7x (the
+  // workgroups sharing operand tiles drift further apart), so this one
+  // stays.  Rows past
   // nrow / ncol read the last valid row (their results are never used); K is
   // a multiple of TK.  The lane's source addresses at K offset 0 are formed
   // once per tile (row clamp and row stride); a stage only adds k0.
