@@ -855,10 +855,12 @@ __global__ void k_lm_kl_reset(int32_t* count) {
 // every row listed).
 __global__ __launch_bounds__(kThreads, 1) void k_lm_kl_redo(LmCombineArgs a) {
   __shared__ __align__(16) unsigned char smem[kLdsBytes];
+  // workgroup ids row tile by row tile (slices fastest): the busy ones, the
+  // first ceil(n / 256) row tiles, are the lowest ids, which the dispatcher
+  // deals round-robin over all the XCDs (a per-XCD regrouping as in the
+  // forward would put them all on the first XCDs)
   const int n = *a.kl_count;
-  const int nrt = (int)((a.R + TM - 1) / TM);
-  int rt, sl;
-  tile_of(blockIdx.x, nrt, a.kl_nslice, rt, sl);
+  const int rt = (int)(blockIdx.x / (unsigned)a.kl_nslice), sl = (int)(blockIdx.x % (unsigned)a.kl_nslice);
   const int64_t row0 = (int64_t)rt * TM;
   if (row0 >= n) return;
   bf16_t* lds = reinterpret_cast<bf16_t*>(smem);

@@ -15,7 +15,8 @@ the oracle's tokens); K = 1 and K = 16 with ragged depths and temperatures;
 a head whose first 64 target columns carry much larger weights, so that a
 row's best logits crowd one segment of the forward's column tiles and the
 row goes through the exact recompute (48 rows, and 768 rows over three
-row tiles of it); the full 49 152 x 4096 shape on 32 positions.
+row tiles of it; at the full shape, every row); the full 49 152 x 4096
+shape on 32 positions.
 """
 import numpy as np
 import pytest
@@ -197,6 +198,19 @@ def test_kl_crowded_many_rows():
     inp = make_inputs(cfg, DEV)
     inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
     check_lmhead_kl(cfg, inp, list(range(cfg.P)), params_of(cfg, kl_weight=0.7, kl_topk=12), "C5 KL crowded 768")
+
+
+def test_kl_full_size_crowded_32_positions():
+    """The full C5 shape with the first 64 target columns' weights 8x larger:
+    every live row of the batch is left undecided by the slice lists and
+    recomputed (192 row tiles of the recompute); 32 positions against the
+    oracle."""
+    cfg = CONFIGS["C5"]
+    inp = make_inputs(cfg, DEV)
+    inp["Wt"][:64] = (inp["Wt"][:64].float() * 8.0).to(torch.bfloat16)
+    rng = np.random.default_rng(57)
+    positions = sorted(set([0, cfg.P - 1] + list(rng.choice(np.arange(1, cfg.P - 1), 30, replace=False))))
+    check_lmhead_kl(cfg, inp, positions, params_of(cfg, kl_weight=0.1, kl_topk=10), "C5 full KL crowded")
 
 
 def test_kl_full_size_32_positions():
