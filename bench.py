@@ -267,8 +267,8 @@ def bench_lm_head(cfg, steps, warmup, dev):
     return res
 
 
-PROFILE_FILES = [os.path.join(ROOT, "profiles", f) for f in ("hbm_traffic.md", "lm_head_c5.md",
-                                                               "sample_score_valu.md")]
+PROFILE_FILES = [os.path.join(ROOT, "profiles", f) for f in ("c3_hbm_traffic.md", "lm_head_c5.md",
+                                                               "c3_sample_score_valu.md")]
 KERNEL_SOURCES = {"sample_score": ["k_sample.hip", "vsd_draw.hpp", "vsd_topk.hpp", "vsd_device.hpp", "vsd_kernels.hpp"],
                   "bwd": ["k_bwd.hip", "vsd_topk.hpp", "vsd_device.hpp", "vsd_kernels.hpp"],
                   "lm_fwd": ["k_lmhead.hip", "vsd_device.hpp", "vsd_kernels.hpp"]}
